@@ -1,0 +1,277 @@
+"""Pins of the CPU oracle against references that do not share its code.
+
+Each pin is chosen so that a plausible mistake in the oracle (a dropped term,
+a wrong sign or index, a transposed operand, an off-by-one position) fails at
+least one of them; tests/test_oracle_mutations.py plants such mistakes and
+checks that they are caught.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_14498_amd import configs, inputs
+from tests.pin_helpers import brute_force, hf_qwen2
+
+SMALL = configs.ModelShape(n_layers=2, d_model=64, n_q_heads=4, n_kv_heads=2, head_dim=16,
+                           ffn_dim=96, vocab=97, dtype="f32")
+
+
+def _setup(model=SMALL, P=(23,), Vis=(15,), S=(9,), index=7, norm="random", bias=True):
+    w = configs.custom(model, P, Vis, S, index=index)
+    W = inputs.make_weights(w, norm=norm, bias=bias).as_f32()
+    bt = inputs.make_batch(w)
+    return w, W, bt
+
+
+def _seq(bt, b):
+    cp, cs = bt.cu_prefix, bt.cu_suffix
+    ids = bt.token_ids[cp[b]:cp[b + 1]]
+    vo = sum(bt.visual_lens[:b])
+    vis = inputs.to_f32(bt.visual[vo:vo + bt.visual_lens[b]])
+    return ids, vis, bt.response_ids[cs[b]:cs[b + 1]]
+
+
+# ----------------------------------------------------------------------------------------
+# whole pipeline vs the transformers Qwen2 implementation (float64)
+# ----------------------------------------------------------------------------------------
+# The library forms RoPE angles in float32 (positions < 64 here: angle error ~1e-6 rad),
+# so agreement is to ~1e-7 (observed: 2.4e-8 on log-probs, 1.1e-7 on keys), not to float64
+# rounding.  Any of the mistakes planted in test_oracle_mutations.py moves results by >1e-3.
+HF_TOL = 1e-6
+
+
+@pytest.mark.parametrize("P,Vis,S", [((23,), (15,), (9,)), ((1,), (0,), (4,)), ((40,), (40,), (1,))])
+def test_oracle_matches_hf_qwen2(P, Vis, S):
+    w, W, bt = _setup(P=P, Vis=Vis, S=S)
+    ids, vis, resp = _seq(bt, 0)
+    lp_hf, keys, vals, h_hf = hf_qwen2(W, SMALL, ids, vis, resp)
+    lp_unsplit = oracle.unsplit_logprob_one(W, SMALL, ids, vis, resp)
+    K, V, h_last, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+    lp_split = oracle.suffix_logprob_one(W, SMALL, K, V, h_last, resp)
+    assert np.max(np.abs(lp_unsplit - lp_hf)) < HF_TOL
+    assert np.max(np.abs(lp_split - lp_hf)) < HF_TOL
+    for l in range(SMALL.n_layers):
+        np.testing.assert_allclose(K[l], keys[l][:P[0]], atol=HF_TOL, rtol=0)
+        np.testing.assert_allclose(V[l], vals[l][:P[0]], atol=HF_TOL, rtol=0)
+    np.testing.assert_allclose(h_last, h_hf, atol=HF_TOL, rtol=0)
+
+
+def test_oracle_matches_brute_force():
+    tiny = configs.ModelShape(n_layers=2, d_model=8, n_q_heads=2, n_kv_heads=1, head_dim=4,
+                              ffn_dim=6, vocab=11, dtype="f32")
+    w, W, bt = _setup(model=tiny, P=(5,), Vis=(3,), S=(3,), index=3)
+    ids, vis, resp = _seq(bt, 0)
+    lp_bf = brute_force(W, tiny, ids, vis, resp)
+    K, V, h, _ = oracle.prefix_forward_one(W, tiny, ids, vis)
+    lp = oracle.suffix_logprob_one(W, tiny, K, V, h, resp)
+    assert np.max(np.abs(lp - lp_bf)) < 1e-12
+
+
+# ----------------------------------------------------------------------------------------
+# split invariant: prefix + suffix == unsplit forward
+# ----------------------------------------------------------------------------------------
+@pytest.mark.parametrize("P,S", [(1, 0), (1, 1), (2, 2), (17, 5), (64, 16)])
+def test_split_invariant(P, S):
+    w, W, bt = _setup(P=(P,), Vis=(P // 2,), S=(S,), index=11)
+    ids, vis, resp = _seq(bt, 0)
+    K, V, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+    a = oracle.suffix_logprob_one(W, SMALL, K, V, h, resp)
+    b = oracle.unsplit_logprob_one(W, SMALL, ids, vis, resp)
+    assert a.shape == (S,)
+    assert np.max(np.abs(a - b), initial=0.0) < 1e-10
+
+
+# ----------------------------------------------------------------------------------------
+# closed forms
+# ----------------------------------------------------------------------------------------
+def test_zero_lm_head_gives_uniform():
+    w, W, bt = _setup(P=(7,), Vis=(3,), S=(5,))
+    W.lm_head = np.zeros_like(W.lm_head)
+    ids, vis, resp = _seq(bt, 0)
+    K, V, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+    lp = oracle.suffix_logprob_one(W, SMALL, K, V, h, resp)
+    assert np.all(lp == -math.log(SMALL.vocab))
+    # the value quoted for the production vocabulary
+    assert abs(-math.log(152064) - (-11.932056763842207)) < 1e-15
+    assert abs(-math.log(2048) - (-7.6246189861593985)) < 1e-15
+
+
+def test_identity_layers_reduce_to_log_softmax():
+    """Wo = Wd = 0 make every layer the identity on the residual stream."""
+    w, W, bt = _setup(P=(9,), Vis=(4,), S=(6,))
+    for lw in W.layers:
+        lw["wo"] = np.zeros_like(lw["wo"])
+        lw["w_down"] = np.zeros_like(lw["w_down"])
+    ids, vis, resp = _seq(bt, 0)
+    K, V, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+    lp = oracle.suffix_logprob_one(W, SMALL, K, V, h, resp)
+    E = torch.tensor(W.embed, dtype=torch.float64)
+    last = torch.tensor(vis[-1], dtype=torch.float64) if ids[-1] < 0 else E[int(ids[-1])]
+    rows = torch.cat([last[None], torch.nn.functional.embedding(torch.tensor(resp[:-1]).long(), E)])
+    z = torch.nn.functional.rms_norm(rows, (SMALL.d_model,),
+                                     torch.tensor(W.final_norm, dtype=torch.float64), SMALL.rms_eps)
+    ref = torch.log_softmax(z @ torch.tensor(W.lm_head, dtype=torch.float64).T, dim=-1)
+    ref = ref[torch.arange(len(resp)), torch.tensor(resp).long()].numpy()
+    assert np.max(np.abs(lp - ref)) < 1e-12
+
+
+def test_rmsnorm_constant_vector_and_library():
+    d, eps = 64, 1e-6
+    for c in (0.0, 1e-4, 0.5, -3.0):
+        w = np.linspace(0.5, 1.5, d)
+        got = oracle.rmsnorm(np.full((1, d), c), w, eps)[0]
+        np.testing.assert_allclose(got, c / math.sqrt(c * c + eps) * w, rtol=1e-14, atol=0)
+    x = np.random.default_rng(0).standard_normal((5, d))
+    w = np.random.default_rng(1).standard_normal(d)
+    ref = torch.nn.functional.rms_norm(torch.tensor(x), (d,), torch.tensor(w), eps).numpy()
+    np.testing.assert_allclose(oracle.rmsnorm(x, w, eps), ref, rtol=1e-13, atol=1e-14)
+
+
+# ----------------------------------------------------------------------------------------
+# RoPE
+# ----------------------------------------------------------------------------------------
+def test_rope_matches_complex_rotation():
+    """Rotate-half RoPE is multiplication of (x_i + i x_{i+D/2}) by exp(i t f_i), f_i = theta^(-2i/D)."""
+    rng = np.random.default_rng(5)
+    D, theta = 16, 1e6
+    x = rng.standard_normal((6, 3, D))
+    pos = np.array([0, 1, 2, 100, 4095, 16383])
+    got = oracle.apply_rope(x, oracle.rope_angles(pos, D, theta))
+    for t in range(len(pos)):
+        for h in range(3):
+            for i in range(D // 2):
+                f = theta ** (-(2 * i) / D)
+                z = complex(x[t, h, i], x[t, h, i + D // 2]) * complex(math.cos(pos[t] * f),
+                                                                      math.sin(pos[t] * f))
+                assert abs(got[t, h, i] - z.real) < 1e-12
+                assert abs(got[t, h, i + D // 2] - z.imag) < 1e-12
+
+
+def test_rope_identities():
+    rng = np.random.default_rng(6)
+    D = 128
+    q, k = rng.standard_normal((1, 1, D)), rng.standard_normal((1, 1, D))
+    a0 = oracle.rope_angles([0], D, 1e6)
+    np.testing.assert_array_equal(oracle.apply_rope(q, a0), q)          # position 0 = identity
+    assert np.allclose(oracle.rope_angles([1], D, 1e6)[0, 0], 1.0)      # first pair turns 1 rad/step
+    m, n, s = 37, 12, 1000
+    r = lambda x, p: oracle.apply_rope(x, oracle.rope_angles([p], D, 1e6))
+    for p in (m, n):                                                    # pair norms preserved
+        x = r(q, p)[0, 0]
+        half = D // 2
+        np.testing.assert_allclose(x[:half] ** 2 + x[half:] ** 2,
+                                   q[0, 0, :half] ** 2 + q[0, 0, half:] ** 2, rtol=1e-12)
+    d1 = np.dot(r(q, m)[0, 0], r(k, n)[0, 0])                           # relative position
+    d2 = np.dot(r(q, m + s)[0, 0], r(k, n + s)[0, 0])
+    assert abs(d1 - d2) < 1e-10
+
+
+# ----------------------------------------------------------------------------------------
+# attention
+# ----------------------------------------------------------------------------------------
+@pytest.mark.parametrize("nq,nk_past,Hq,Hkv", [(13, 0, 4, 2), (7, 21, 6, 2), (1, 0, 2, 2)])
+def test_attention_matches_torch_sdpa(nq, nk_past, Hq, Hkv):
+    rng = np.random.default_rng(nq + nk_past)
+    D = 16
+    q = rng.standard_normal((nq, Hq, D))
+    k = rng.standard_normal((nk_past + nq, Hkv, D))
+    v = rng.standard_normal((nk_past + nq, Hkv, D))
+    qpos = nk_past + np.arange(nq)
+    kpos = np.arange(nk_past + nq)
+    got = oracle.attention(q, k, v, qpos, kpos)
+    mask = torch.tensor(kpos[None, :] <= qpos[:, None])
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.tensor(q).transpose(0, 1)[None], torch.tensor(k).transpose(0, 1)[None],
+        torch.tensor(v).transpose(0, 1)[None], attn_mask=mask, enable_gqa=True)
+    np.testing.assert_allclose(got, ref[0].transpose(0, 1).numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_attention_special_cases():
+    rng = np.random.default_rng(9)
+    v = rng.standard_normal((1, 1, 8))
+    q = rng.standard_normal((1, 2, 8))
+    out = oracle.attention(q, rng.standard_normal((1, 1, 8)), v, [0], [0])
+    np.testing.assert_allclose(out[0, 0], v[0, 0])                      # one key: o = v0
+    np.testing.assert_allclose(out[0, 1], v[0, 0])
+    k = np.repeat(rng.standard_normal((1, 1, 8)), 6, axis=0)            # equal keys: mean of visible v
+    v = rng.standard_normal((6, 1, 8))
+    q = rng.standard_normal((6, 1, 8))
+    out = oracle.attention(q, k, v, np.arange(6), np.arange(6))
+    for t in range(6):
+        np.testing.assert_allclose(out[t, 0], v[:t + 1, 0].mean(axis=0), rtol=1e-12)
+
+
+def test_gqa_equals_replicated_mha():
+    w, W, bt = _setup(P=(11,), Vis=(6,), S=(4,))
+    ids, vis, resp = _seq(bt, 0)
+    G = SMALL.group
+    mha = configs.ModelShape(**{**SMALL.__dict__, "n_kv_heads": SMALL.n_q_heads})
+    import copy
+    W2 = copy.deepcopy(W)
+    Dh = SMALL.head_dim
+    for lw in W2.layers:
+        for key in ("wk", "wv"):
+            heads = lw[key].reshape(SMALL.n_kv_heads, Dh, -1)
+            lw[key] = np.repeat(heads, G, axis=0).reshape(SMALL.n_q_heads * Dh, -1)
+        for key in ("bk", "bv"):
+            lw[key] = np.repeat(lw[key].reshape(SMALL.n_kv_heads, Dh), G, axis=0).reshape(-1)
+    a = oracle.unsplit_logprob_one(W, SMALL, ids, vis, resp)
+    b = oracle.unsplit_logprob_one(W2, mha, ids, vis, resp)
+    assert np.max(np.abs(a - b)) < 1e-12
+
+
+# ----------------------------------------------------------------------------------------
+# batching invariants and the decode step
+# ----------------------------------------------------------------------------------------
+def test_packed_batch_equals_each_alone_and_permutation():
+    w, W, bt = _setup(P=(9, 1, 17), Vis=(5, 0, 16), S=(3, 0, 4), index=21)
+    K, V, H = oracle.prefix_forward(W, SMALL, bt.cu_prefix, bt.token_ids, inputs.to_f32(bt.visual))
+    lp = oracle.suffix_logprob(W, SMALL, bt.cu_prefix, bt.cu_suffix, K, V, H, bt.response_ids)
+    lpu = oracle.unsplit_logprob(W, SMALL, bt.cu_prefix, bt.cu_suffix, bt.token_ids,
+                                 inputs.to_f32(bt.visual), bt.response_ids)
+    assert np.max(np.abs(lp - lpu)) < 1e-10
+    for b in range(3):
+        ids, vis, resp = _seq(bt, b)
+        k, v, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+        cp = bt.cu_prefix
+        np.testing.assert_array_equal(K[:, cp[b]:cp[b + 1]], k)
+        np.testing.assert_array_equal(H[b], h)
+
+
+def test_prefix_is_response_independent():
+    w, W, bt = _setup(P=(12,), Vis=(8,), S=(5,))
+    ids, vis, resp = _seq(bt, 0)
+    K, V, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+    lp1 = oracle.suffix_logprob_one(W, SMALL, K, V, h, resp)
+    resp2 = resp.copy()
+    resp2[2:] = (resp2[2:] + 5) % SMALL.vocab
+    lp2 = oracle.suffix_logprob_one(W, SMALL, K, V, h, resp2)
+    # tokens before the change are scored identically, later ones are not
+    np.testing.assert_array_equal(lp1[:2], lp2[:2])
+    assert np.all(lp1[2:] != lp2[2:])
+
+
+def test_decode_step_equals_suffix_of_length_two():
+    w, W, bt = _setup(P=(10, 6), Vis=(7, 2), S=(2, 2), index=31)
+    B, L = 2, SMALL.n_layers
+    cap = 12
+    ck = np.zeros((L, B, cap, SMALL.n_kv_heads, SMALL.head_dim))
+    cv = np.zeros_like(ck)
+    kv_len = np.array(bt.prefix_lens)
+    toks = np.empty(B, np.int64)
+    ref_lp = []
+    for b in range(B):
+        ids, vis, resp = _seq(bt, b)
+        K, V, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+        ck[:, b, :len(ids)], cv[:, b, :len(ids)] = K, V
+        toks[b] = resp[0]
+        ref_lp.append(oracle.suffix_logprob_one(W, SMALL, K, V, h, resp)[1])
+    logits, nxt, nk, nv = oracle.decode_step(W, SMALL, ck, cv, kv_len, toks)
+    for b in range(B):
+        resp = _seq(bt, b)[2]
+        lp = logits[b] - (logits[b].max() + np.log(np.exp(logits[b] - logits[b].max()).sum()))
+        assert abs(lp[resp[1]] - ref_lp[b]) < 1e-10
+        assert nxt[b] == int(np.argmax(logits[b]))
