@@ -1,0 +1,205 @@
+/*
+ * rollplex.h -- C ABI of the MI355X (gfx950) prefix/suffix backbone path.
+ *
+ * Rollplex (arXiv 2608.14498) splits every model invocation of VLM RL at the
+ * first response position (Section "Observation and Opportunity"): the prefix
+ * pass (prompt prefill over visual + text tokens) depends only on the input
+ * and the weights, produces boundary KV state and the prefix's log-probability
+ * state, and can run while rollout still decodes; the suffix pass continues
+ * from the retained boundary and scores the response tokens (Section
+ * "Cross-Phase Execution", Phases 1 and 2).  This library runs both passes of
+ * a Qwen2-style decoder backbone (RMSNorm, rotate-half RoPE, grouped-query
+ * attention, SwiGLU MLP, untied lm_head) with hand-written HIP kernels, plus
+ * the rollout-side decode step and a CU-masked stream helper for running the
+ * prefix pass beside decode on one GPU (Eq. (1) and Section "Resource Sharing
+ * Policy").
+ *
+ * Conventions shared by every entry point
+ *   - Ownership: the caller owns all weights, inputs, outputs, KV buffers and
+ *     workspaces.  The library keeps only the pointers given to rp_create and
+ *     a few host-side constants; it never frees, reallocates or retains
+ *     caller memory beyond rp_destroy.
+ *   - Asynchrony: compute calls enqueue kernels on the given HIP stream
+ *     (passed as void*, a hipStream_t; NULL = the null stream) and return
+ *     without synchronising.  Outputs are valid once the stream reaches that
+ *     point; inputs must stay alive until then.  Concurrent calls need
+ *     separate workspaces; one model handle may be shared across streams.
+ *   - Errors: no exception crosses the ABI.  Host-side validation runs before
+ *     any HIP call and returns RP_ERR_INVALID_ARG (null/misaligned pointer,
+ *     bad enum), RP_ERR_SHAPE (bad lengths or offsets), RP_ERR_UNSUPPORTED
+ *     (shape outside what the kernels implement) or RP_ERR_WORKSPACE
+ *     (workspace too small).  A failed launch returns RP_ERR_HIP.  The text
+ *     of the last non-OK status of the calling thread is rp_last_error().
+ *   - Dtypes: weights, visual embeddings and KV share rp_config.dtype (fp32
+ *     or bf16, row-major, nn.Linear layout [out, in] for projections).
+ *     h_last, hidden_out, logprobs and logits are always fp32.  Token ids are
+ *     int32.  Length tables (cu_seqlens) are HOST int32 arrays.
+ *   - Device-side data the host cannot see (token ids, kv_len) is clamped to
+ *     valid ranges inside the kernels, so bad values give unspecified numbers
+ *     but never an out-of-bounds access.
+ *   - Device pointers must be 16-byte aligned (workspaces 256-byte aligned).
+ */
+#ifndef ROLLPLEX_H
+#define ROLLPLEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RP_MAX_SEQS 256 /* sequences per prefix/suffix call */
+
+typedef enum {
+  RP_OK = 0,
+  RP_ERR_INVALID_ARG = 1,
+  RP_ERR_SHAPE = 2,
+  RP_ERR_UNSUPPORTED = 3,
+  RP_ERR_WORKSPACE = 4,
+  RP_ERR_HIP = 5
+} rp_status;
+
+typedef enum { RP_F32 = 0, RP_BF16 = 1 } rp_dtype;
+
+/* Backbone hyper-parameters.  head_dim must be 64 or 128; n_q_heads a
+ * multiple of n_kv_heads (q head h reads kv head h / (n_q_heads/n_kv_heads)).
+ * For bf16, d_model, ffn_dim and n_q_heads*head_dim must be multiples of 64.
+ * rms_eps is the RMSNorm epsilon (1e-6 for the Qwen2 family); rope_theta the
+ * RoPE base (1e6).  max_position bounds every position a call may use. */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab, max_position;
+  float rms_eps;
+  double rope_theta;
+  rp_dtype dtype;
+} rp_config;
+
+/* One decoder layer, device pointers, nn.Linear layout [out, in]:
+ * wq [Hq*Dh, d], wk/wv [Hkv*Dh, d], wo [d, Hq*Dh], w_gate/w_up [F, d],
+ * w_down [d, F]; attn_norm/mlp_norm [d]; biases bq [Hq*Dh], bk/bv [Hkv*Dh]
+ * are optional (NULL = none). */
+typedef struct {
+  const void *attn_norm, *wq, *wk, *wv, *bq, *bk, *bv, *wo;
+  const void *mlp_norm, *w_gate, *w_up, *w_down;
+} rp_layer_weights;
+
+/* embed [V, d], final_norm [d], lm_head [V, d] (untied), layers: HOST array
+ * of n_layers entries (copied by rp_create). */
+typedef struct {
+  const void *embed, *final_norm, *lm_head;
+  const rp_layer_weights *layers;
+} rp_weights;
+
+/* Per-layer K and V buffers: layer l starts at k + l*layer_stride elements
+ * (of rp_config.dtype); within a layer, rows of [n_kv_heads][head_dim].
+ * K is stored after RoPE. */
+typedef struct {
+  void *k, *v;
+  int64_t layer_stride;
+} rp_kv;
+
+typedef struct rp_model rp_model;
+
+/* Validates cfg and weights and binds the pointers (no device memory is
+ * allocated; no HIP call is made).  *out receives a handle freed by
+ * rp_destroy. */
+rp_status rp_create(const rp_config *cfg, const rp_weights *weights, rp_model **out);
+void rp_destroy(rp_model *model);
+
+/* ---------------------------------------------------------------------------
+ * Prefix pass (Section "Observation and Opportunity": the response-independent
+ * part of the invocation, prompt prefill producing boundary KV and prefix
+ * log-probability state; Phase 1 of Section "Cross-Phase Execution").
+ *
+ * B sequences are packed: sequence b occupies rows cu_seqlens[b] ..
+ * cu_seqlens[b+1]-1 (cu_seqlens[0] = 0, strictly increasing: every prefix
+ * has at least one token), at positions 0 .. P_b-1.
+ * token_ids  dev int32 [T]: a vocabulary id, or -1 for a visual slot; visual
+ *            slots take the rows of visual_embeds in order over the packed
+ *            batch (n_visual rows of [d]; slots beyond n_visual read zeros).
+ * kv_out     dev, caller-allocated: K/V of every layer and prefix row, post
+ *            RoPE; layer_stride >= T*n_kv_heads*head_dim.
+ * h_last     dev fp32 [B, d]: the residual stream at each sequence's last
+ *            prefix position after the last layer, before the final norm.
+ *            It determines the boundary distribution that scores the first
+ *            response token.
+ * hidden_out optional dev fp32 [T, d]: the full last-layer residual stream.
+ * workspace  dev, >= rp_prefix_workspace_bytes(); contents are scratch.
+ * ------------------------------------------------------------------------- */
+rp_status rp_prefix_workspace_bytes(const rp_model *model, int32_t B, const int32_t *cu_seqlens_host,
+                                    size_t *bytes);
+rp_status rp_prefix_forward(const rp_model *model, void *stream, int32_t B,
+                            const int32_t *cu_seqlens_host, const int32_t *token_ids,
+                            const void *visual_embeds, int64_t n_visual, rp_kv kv_out,
+                            float *h_last, float *hidden_out, void *workspace,
+                            size_t workspace_bytes);
+
+/* ---------------------------------------------------------------------------
+ * Suffix pass (Phase 2 of Section "Cross-Phase Execution": the suffix
+ * continues from the retained boundary and scores the response without
+ * recomputing the prompt; prefix and suffix log-probabilities together form
+ * the full-sequence values).
+ *
+ * Sequence b's response r_b,0 .. r_b,S_b-1 occupies rows suffix_cu[b] ..
+ * suffix_cu[b+1]-1 (non-decreasing; S_b = 0 allowed) at positions P_b + j;
+ * its prefix is rows prefix_cu[b] .. of kv (read only) and h_last[b].
+ * logprobs[suffix_cu[b]+j] = log p(r_b,j | prefix_b, r_b,<j), scored with the
+ * full vocabulary at temperature 1: j = 0 from h_last[b], j > 0 from the
+ * hidden state of response token j-1.
+ * ------------------------------------------------------------------------- */
+rp_status rp_suffix_workspace_bytes(const rp_model *model, int32_t B, const int32_t *prefix_cu_host,
+                                    const int32_t *suffix_cu_host, size_t *bytes);
+rp_status rp_suffix_logprob(const rp_model *model, void *stream, int32_t B,
+                            const int32_t *prefix_cu_host, const int32_t *suffix_cu_host, rp_kv kv,
+                            const float *h_last, const int32_t *response_ids, float *logprobs,
+                            void *workspace, size_t workspace_bytes);
+
+/* ---------------------------------------------------------------------------
+ * Rollout decode step (the memory-bound phase that the prefix pass overlaps
+ * with; Section "Observation and Opportunity" and Eq. (1)).  One new token
+ * per sequence: token_ids[b] runs at position kv_len[b], its K/V are written
+ * to slot kv_len[b] of cache (layout [L][B][cap][n_kv_heads][head_dim],
+ * layer_stride >= B*cap*n_kv_heads*head_dim), it attends to slots
+ * 0..kv_len[b], and next_ids[b] = argmax of its logits (lowest id on ties).
+ * kv_len is a device int32 [B] array, values clamped to [0, cap-1] (and to
+ * max_position-1).  logits (optional) receives fp32 [B, V].
+ * ------------------------------------------------------------------------- */
+rp_status rp_decode_workspace_bytes(const rp_model *model, int32_t B, int32_t cap, size_t *bytes);
+rp_status rp_decode_step(const rp_model *model, void *stream, int32_t B, rp_kv cache, int32_t cap,
+                         const int32_t *kv_len, const int32_t *token_ids, float *logits,
+                         int32_t *next_ids, void *workspace, size_t workspace_bytes);
+
+/* ---------------------------------------------------------------------------
+ * Co-location helpers (Section "Resource Sharing Policy": decode and prefix
+ * share one GPU; static partitions are the analog of the paper's SM
+ * partitions).  mask: n_words 32-bit words, bit i = compute unit i may run
+ * this stream's work.  The stream has the default priority.
+ * ------------------------------------------------------------------------- */
+rp_status rp_stream_create_cu_masked(int device, const uint32_t *mask, uint32_t n_words, void **out);
+rp_status rp_stream_destroy(void *stream);
+int rp_device_cu_count(int device);
+
+/* ---------------------------------------------------------------------------
+ * Per-launch timing (measurement aid, off by default; not thread-safe).
+ * While enabled, every kernel launch of the compute entry points is bracketed
+ * by two HIP events recorded on the launch stream.  rp_profile_collect waits
+ * for those events and accumulates, per kernel name, the launch count and the
+ * summed duration; rp_profile_read(i) returns entry i (0 <= i < count).
+ * max_launches bounds the number of bracketed launches until the next collect
+ * (later launches run untimed).  Enabling creates the events (a HIP call);
+ * disabling destroys them.
+ * ------------------------------------------------------------------------- */
+rp_status rp_profile_enable(int enable, int32_t max_launches);
+rp_status rp_profile_collect(void);
+int32_t rp_profile_count(void);
+rp_status rp_profile_read(int32_t i, const char **name, int64_t *launches, double *total_ms);
+void rp_profile_reset(void);
+
+const char *rp_last_error(void);
+const char *rp_status_string(rp_status status);
+const char *rp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ROLLPLEX_H */

@@ -1,0 +1,609 @@
+// Host runtime behind include/rollplex.h: validation, workspace carving and the
+// per-layer launch sequence of the prefix pass, the suffix pass and the decode step.
+// Every compute entry point validates all host-visible arguments before its first HIP
+// call, then only enqueues kernels on the caller's stream (no allocation, no sync).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include <hip/hip_ext.h>
+
+#include "rp_internal.h"
+
+struct rp_model {
+  rp_config cfg;
+  const void* embed;
+  const void* final_norm;
+  const void* lm_head;
+  std::vector<rp_layer_weights> layers;
+  rp::RopeFreq rope;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+rp_status fail(rp_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+bool fault_injected() {
+  const char* e = getenv("RP_FAULT_INJECT");
+  return e && *e && strcmp(e, "0") != 0;
+}
+
+// ---- per-launch event timing (rp_profile_*) ----
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> ev;        // 2 per bracketed launch
+  std::vector<const char*> pending;  // kernel name per bracketed launch
+  std::vector<std::string> names;
+  std::vector<int64_t> count;
+  std::vector<double> ms;
+};
+Profiler g_prof;
+
+bool prof_begin(hipStream_t s, const char* name, int* slot) {
+  *slot = -1;
+  if (!g_prof.on) return true;
+  const size_t k = g_prof.pending.size();
+  if (2 * k + 1 >= g_prof.ev.size()) return true;
+  if (hipEventRecord(g_prof.ev[2 * k], s) != hipSuccess) return false;
+  g_prof.pending.push_back(name);
+  *slot = (int)k;
+  return true;
+}
+
+bool prof_end(hipStream_t s, int slot) {
+  if (slot < 0) return true;
+  return hipEventRecord(g_prof.ev[2 * slot + 1], s) == hipSuccess;
+}
+
+// Launch `expr` (a launcher returning hipError_t) on stream `s`, timing it when profiling.
+#define RP_TRY_LAUNCH_N(name, expr)                                                             \
+  do {                                                                                          \
+    if (fault_injected()) return fail(RP_ERR_HIP, "injected launch fault (RP_FAULT_INJECT)");   \
+    int slot_;                                                                                  \
+    if (!prof_begin(s, name, &slot_)) return fail(RP_ERR_HIP, "profiling event record failed"); \
+    hipError_t e_ = (expr);                                                                     \
+    if (e_ != hipSuccess) return fail(RP_ERR_HIP, "%s failed: %s", name, hipGetErrorString(e_)); \
+    if (!prof_end(s, slot_)) return fail(RP_ERR_HIP, "profiling event record failed");          \
+  } while (0)
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t elem_size(const rp_config& c) { return c.dtype == RP_BF16 ? 2 : 4; }
+
+// Bump allocator over the caller's workspace (sizing pass when base == nullptr).
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    off = (off + 255) & ~(size_t)255;
+    void* p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+struct LayerWS {
+  float* X;   // fp32 residual [M, d]
+  void* N;    // normed activations [M, d]
+  void* QKV;  // [M, qkv]
+  void* O;    // attention output [M, Hq*D]
+  void* GU;   // [M, 2F]
+  void* ACT;  // [M, F]
+};
+
+void carve_layer(Carver& c, const rp_config& cfg, int64_t M, bool need_x, LayerWS* w) {
+  const size_t es = elem_size(cfg);
+  const int64_t d = cfg.d_model, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
+  w->X = need_x ? (float*)c.take(M * d * 4) : nullptr;
+  w->N = c.take(M * d * es);
+  w->QKV = c.take(M * qkv * es);
+  w->O = c.take(M * (int64_t)cfg.n_q_heads * cfg.head_dim * es);
+  w->GU = c.take(M * 2 * (int64_t)cfg.ffn_dim * es);
+  w->ACT = c.take(M * (int64_t)cfg.ffn_dim * es);
+}
+
+rp_status check_config(const rp_config* c) {
+  if (!c) return fail(RP_ERR_INVALID_ARG, "config is NULL");
+  if (c->dtype != RP_F32 && c->dtype != RP_BF16) return fail(RP_ERR_INVALID_ARG, "bad dtype %d", (int)c->dtype);
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn_dim < 1 ||
+      c->vocab < 1 || c->max_position < 1)
+    return fail(RP_ERR_SHAPE, "config sizes must be positive");
+  if (c->n_q_heads % c->n_kv_heads != 0)
+    return fail(RP_ERR_SHAPE, "n_q_heads %d not a multiple of n_kv_heads %d", c->n_q_heads, c->n_kv_heads);
+  if (c->n_q_heads / c->n_kv_heads > 16)
+    return fail(RP_ERR_UNSUPPORTED, "query group size %d > 16", c->n_q_heads / c->n_kv_heads);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(RP_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
+  if (c->d_model % 8 || c->ffn_dim % 8) return fail(RP_ERR_UNSUPPORTED, "d_model and ffn_dim must be multiples of 8");
+  if (c->dtype == RP_BF16 &&
+      (c->d_model % 64 || c->ffn_dim % 64 || (c->n_q_heads * c->head_dim) % 64))
+    return fail(RP_ERR_UNSUPPORTED, "bf16 needs d_model, ffn_dim and n_q_heads*head_dim multiples of 64");
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.0)) return fail(RP_ERR_SHAPE, "rms_eps and rope_theta must be > 0");
+  const int64_t qkv = (int64_t)(c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
+  if (qkv > (1 << 30) || (int64_t)c->ffn_dim * 2 > (1 << 30)) return fail(RP_ERR_UNSUPPORTED, "dimension too large");
+  return RP_OK;
+}
+
+rp_status check_prefix_cu(const rp_model* m, int32_t B, const int32_t* cu, const char* what) {
+  if (B < 1 || B > RP_MAX_SEQS) return fail(RP_ERR_SHAPE, "%s: batch %d outside [1, %d]", what, B, RP_MAX_SEQS);
+  if (!cu) return fail(RP_ERR_INVALID_ARG, "%s: cu_seqlens is NULL", what);
+  if (cu[0] != 0) return fail(RP_ERR_SHAPE, "%s: cu_seqlens[0] = %d, must be 0", what, cu[0]);
+  for (int b = 0; b < B; ++b) {
+    if (cu[b + 1] <= cu[b])
+      return fail(RP_ERR_SHAPE, "%s: sequence %d has length %d (prefixes need >= 1 token)", what, b,
+                  cu[b + 1] - cu[b]);
+    if (cu[b + 1] - cu[b] > m->cfg.max_position)
+      return fail(RP_ERR_SHAPE, "%s: sequence %d length %d exceeds max_position %d", what, b, cu[b + 1] - cu[b],
+                  m->cfg.max_position);
+  }
+  return RP_OK;
+}
+
+rp_status check_suffix_cu(const rp_model* m, int32_t B, const int32_t* pcu, const int32_t* scu) {
+  rp_status s = check_prefix_cu(m, B, pcu, "prefix_cu");
+  if (s != RP_OK) return s;
+  if (!scu) return fail(RP_ERR_INVALID_ARG, "suffix_cu is NULL");
+  if (scu[0] != 0) return fail(RP_ERR_SHAPE, "suffix_cu[0] = %d, must be 0", scu[0]);
+  for (int b = 0; b < B; ++b) {
+    const int S = scu[b + 1] - scu[b];
+    if (S < 0) return fail(RP_ERR_SHAPE, "suffix sequence %d has negative length %d", b, S);
+    const int64_t last = (int64_t)(pcu[b + 1] - pcu[b]) + S;
+    if (last > m->cfg.max_position)
+      return fail(RP_ERR_SHAPE, "sequence %d: prefix + suffix = %lld exceeds max_position %d", b, (long long)last,
+                  m->cfg.max_position);
+  }
+  return RP_OK;
+}
+
+rp::SeqTable make_table(int32_t B, const int32_t* q_cu, const int32_t* k_cu) {
+  rp::SeqTable t;
+  memset(&t, 0, sizeof t);
+  t.n = B;
+  for (int b = 0; b <= B; ++b) {
+    t.q_cu[b] = q_cu[b];
+    t.k_cu[b] = k_cu ? k_cu[b] : 0;
+  }
+  return t;
+}
+
+size_t prefix_ws(const rp_model* m, int64_t T, void* base, bool need_x, LayerWS* w, int32_t** vis_idx) {
+  Carver c(base);
+  int32_t* vi = (int32_t*)c.take(T * 4);
+  if (vis_idx) *vis_idx = vi;
+  LayerWS tmp;
+  carve_layer(c, m->cfg, T, need_x, w ? w : &tmp);
+  return c.off + 256;
+}
+
+struct SuffixWS {
+  LayerWS L;
+  void* Ks;
+  void* Vs;
+  float* logits;
+};
+
+size_t suffix_ws(const rp_model* m, int64_t R, void* base, SuffixWS* w) {
+  Carver c(base);
+  SuffixWS tmp;
+  SuffixWS* s = w ? w : &tmp;
+  carve_layer(c, m->cfg, R, true, &s->L);
+  const int64_t kvrow = (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim;
+  s->Ks = c.take(R * kvrow * elem_size(m->cfg));
+  s->Vs = c.take(R * kvrow * elem_size(m->cfg));
+  s->logits = (float*)c.take(R * (int64_t)m->cfg.vocab * 4);
+  return c.off + 256;
+}
+
+// split-K factor for small-M GEMMs (decode): aim for >= 2 workgroups per CU.
+int decode_splitk(const rp_config& cfg, int32_t M, int32_t N, int32_t K) {
+  if (cfg.dtype != RP_BF16) return 1;
+  const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  int s = (512 + tiles - 1) / tiles;
+  s = s < 1 ? 1 : s;
+  s = s > 8 ? 8 : s;
+  const int kb = K / 64;
+  return s > kb ? kb : s;
+}
+
+struct DecodeWS {
+  LayerWS L;
+  float* logits;
+  float* attn_part;
+  float* gemm_part;
+};
+
+size_t decode_ws(const rp_model* m, int32_t B, int32_t cap, void* base, DecodeWS* w) {
+  Carver c(base);
+  DecodeWS tmp;
+  DecodeWS* s = w ? w : &tmp;
+  const rp_config& cfg = m->cfg;
+  carve_layer(c, cfg, B, true, &s->L);
+  s->logits = (float*)c.take((int64_t)B * cfg.vocab * 4);
+  s->attn_part = (float*)c.take(rp::decode_attn_partial_floats(B, cfg.n_q_heads, cfg.head_dim, cap) * 4);
+  const int64_t d = cfg.d_model, F = cfg.ffn_dim, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
+  const int64_t hq = (int64_t)cfg.n_q_heads * cfg.head_dim;
+  size_t need = 0;
+  const int64_t shapes[4][2] = {{qkv, d}, {d, hq}, {2 * F, d}, {d, F}};
+  for (auto& sh : shapes) {
+    size_t f = rp::gemm_partial_floats(B, (int32_t)sh[0], decode_splitk(cfg, B, (int32_t)sh[0], (int32_t)sh[1]));
+    need = f > need ? f : need;
+  }
+  s->gemm_part = (float*)c.take(need * 4);
+  return c.off + 256;
+}
+
+rp_status check_kv(const rp_model* m, const rp_kv& kv, int64_t rows, const char* what) {
+  if (!kv.k || !kv.v) return fail(RP_ERR_INVALID_ARG, "%s: k or v is NULL", what);
+  const int64_t per = rows * m->cfg.n_kv_heads * m->cfg.head_dim;
+  if (kv.layer_stride < per)
+    return fail(RP_ERR_SHAPE, "%s: layer_stride %lld < %lld elements", what, (long long)kv.layer_stride, (long long)per);
+  if (!aligned16(kv.k) || !aligned16(kv.v) || (kv.layer_stride % 8))
+    return fail(RP_ERR_INVALID_ARG, "%s: KV must be 16-byte aligned (layer_stride multiple of 8)", what);
+  return RP_OK;
+}
+
+rp_status check_ws(void* ws, size_t have, size_t need) {
+  if (have < need) return fail(RP_ERR_WORKSPACE, "workspace %zu bytes < required %zu", have, need);
+  if (need && !ws) return fail(RP_ERR_INVALID_ARG, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(RP_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  return RP_OK;
+}
+
+void* layer_ptr(const rp_model* m, void* base, int64_t stride, int l) {
+  return (char*)base + (size_t)l * stride * elem_size(m->cfg);
+}
+
+// One decoder layer over M rows; keys/values go to k_out/v_out (rows aligned with
+// the query rows); attention reads segment 0 from k0/v0 as described by st.
+rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, const rp::SeqTable& st,
+                    int32_t M, const LayerWS& w, void* k_out, void* v_out, const void* k0, const void* v0,
+                    int splitk_ok, float* gemm_part) {
+  const rp_config& c = m->cfg;
+  const bool bf = c.dtype == RP_BF16;
+  const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
+  const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
+  auto sk = [&](int N, int K) { return splitk_ok ? decode_splitk(c, M, N, K) : 1; };
+  RP_TRY_LAUNCH_N("rmsnorm", rp::launch_rmsnorm(s, bf, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
+  rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
+  RP_TRY_LAUNCH_N("gemm_qkv", rp::launch_gemm(s, bf, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE, sk(qkv, d), gemm_part));
+  RP_TRY_LAUNCH_N("rope_kv", rp::launch_rope_kv(s, bf, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position,
+                                   k_out, v_out));
+  rp::AttnArgs a;
+  a.q = w.QKV;
+  a.q_ld = qkv;
+  a.k0 = k0;
+  a.v0 = v0;
+  a.k1 = k_out;
+  a.v1 = v_out;
+  a.o = w.O;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.D = D;
+  a.scale = (float)(1.0 / sqrt((double)D));
+  RP_TRY_LAUNCH_N("attention", rp::launch_attention(s, bf, st, a, M));
+  rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
+  RP_TRY_LAUNCH_N("gemm_o_proj", rp::launch_gemm(s, bf, M, d, hq, w.O, hq, bo, hq, w.X, d, rp::EPI_ADD_F32, sk(d, hq), gemm_part));
+  RP_TRY_LAUNCH_N("rmsnorm", rp::launch_rmsnorm(s, bf, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
+  rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
+  RP_TRY_LAUNCH_N("gemm_gate_up", rp::launch_gemm(s, bf, M, 2 * F, d, w.N, d, bgu, d, w.GU, 2 * F, rp::EPI_STORE, sk(2 * F, d),
+                                gemm_part));
+  RP_TRY_LAUNCH_N("swiglu", rp::launch_swiglu(s, bf, w.GU, M, F, w.ACT));
+  rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
+  RP_TRY_LAUNCH_N("gemm_down", rp::launch_gemm(s, bf, M, d, F, w.ACT, F, bd, F, w.X, d, rp::EPI_ADD_F32, sk(d, F), gemm_part));
+  return RP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rp_last_error(void) { return g_err.c_str(); }
+
+const char* rp_status_string(rp_status s) {
+  switch (s) {
+    case RP_OK: return "RP_OK";
+    case RP_ERR_INVALID_ARG: return "RP_ERR_INVALID_ARG";
+    case RP_ERR_SHAPE: return "RP_ERR_SHAPE";
+    case RP_ERR_UNSUPPORTED: return "RP_ERR_UNSUPPORTED";
+    case RP_ERR_WORKSPACE: return "RP_ERR_WORKSPACE";
+    case RP_ERR_HIP: return "RP_ERR_HIP";
+  }
+  return "RP_UNKNOWN";
+}
+
+const char* rp_version(void) { return "rollplex-mi355x 0.1 (gfx950)"; }
+
+rp_status rp_create(const rp_config* cfg, const rp_weights* w, rp_model** out) {
+  if (!out) return fail(RP_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  rp_status st = check_config(cfg);
+  if (st != RP_OK) return st;
+  if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers)
+    return fail(RP_ERR_INVALID_ARG, "weights: embed, final_norm, lm_head and layers are required");
+  const bool bf = cfg->dtype == RP_BF16;
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const rp_layer_weights& lw = w->layers[l];
+    const void* req[] = {lw.attn_norm, lw.wq, lw.wk, lw.wv, lw.wo, lw.mlp_norm, lw.w_gate, lw.w_up, lw.w_down};
+    for (const void* p : req) {
+      if (!p) return fail(RP_ERR_INVALID_ARG, "layer %d: a required weight pointer is NULL", l);
+      if (!aligned16(p)) return fail(RP_ERR_INVALID_ARG, "layer %d: weights must be 16-byte aligned", l);
+    }
+  }
+  if (!aligned16(w->embed) || !aligned16(w->lm_head) || !aligned16(w->final_norm))
+    return fail(RP_ERR_INVALID_ARG, "embed/lm_head/final_norm must be 16-byte aligned");
+  (void)bf;
+  rp_model* m = new rp_model;
+  m->cfg = *cfg;
+  m->embed = w->embed;
+  m->final_norm = w->final_norm;
+  m->lm_head = w->lm_head;
+  m->layers.assign(w->layers, w->layers + cfg->n_layers);
+  memset(&m->rope, 0, sizeof m->rope);
+  for (int i = 0; i < cfg->head_dim / 2; ++i)
+    m->rope.inv_freq[i] = pow(cfg->rope_theta, -2.0 * (double)i / (double)cfg->head_dim);
+  *out = m;
+  return RP_OK;
+}
+
+void rp_destroy(rp_model* m) { delete m; }
+
+rp_status rp_prefix_workspace_bytes(const rp_model* m, int32_t B, const int32_t* cu, size_t* bytes) {
+  if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
+  rp_status s = check_prefix_cu(m, B, cu, "cu_seqlens");
+  if (s != RP_OK) return s;
+  *bytes = prefix_ws(m, cu[B], nullptr, true, nullptr, nullptr);
+  return RP_OK;
+}
+
+rp_status rp_prefix_forward(const rp_model* m, void* stream, int32_t B, const int32_t* cu, const int32_t* token_ids,
+                            const void* visual, int64_t n_visual, rp_kv kv_out, float* h_last, float* hidden_out,
+                            void* ws, size_t ws_bytes) {
+  if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  rp_status st = check_prefix_cu(m, B, cu, "cu_seqlens");
+  if (st != RP_OK) return st;
+  const int64_t T = cu[B];
+  if (!token_ids || !h_last) return fail(RP_ERR_INVALID_ARG, "token_ids and h_last are required");
+  if (n_visual < 0) return fail(RP_ERR_SHAPE, "n_visual %lld < 0", (long long)n_visual);
+  if (n_visual > 0 && !visual) return fail(RP_ERR_INVALID_ARG, "visual_embeds is NULL with n_visual > 0");
+  if (visual && !aligned16(visual)) return fail(RP_ERR_INVALID_ARG, "visual_embeds must be 16-byte aligned");
+  if ((hidden_out && !aligned16(hidden_out)) || !aligned16(h_last))
+    return fail(RP_ERR_INVALID_ARG, "h_last / hidden_out must be 16-byte aligned");
+  if ((st = check_kv(m, kv_out, T, "kv_out")) != RP_OK) return st;
+  const size_t need = prefix_ws(m, T, nullptr, hidden_out == nullptr, nullptr, nullptr);
+  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
+
+  hipStream_t s = (hipStream_t)stream;
+  const rp_config& c = m->cfg;
+  const bool bf = c.dtype == RP_BF16;
+  LayerWS w;
+  int32_t* vis_idx = nullptr;
+  prefix_ws(m, T, ws, hidden_out == nullptr, &w, &vis_idx);
+  if (hidden_out) w.X = hidden_out;
+  const rp::SeqTable tab = make_table(B, cu, nullptr);
+
+  RP_TRY_LAUNCH_N("visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
+  RP_TRY_LAUNCH_N("embed", rp::launch_embed(s, bf, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
+                                 c.d_model, w.X));
+  for (int l = 0; l < c.n_layers; ++l) {
+    void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
+    void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, 0, nullptr);
+    if (st != RP_OK) return st;
+  }
+  RP_TRY_LAUNCH_N("gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
+  return RP_OK;
+}
+
+rp_status rp_suffix_workspace_bytes(const rp_model* m, int32_t B, const int32_t* pcu, const int32_t* scu,
+                                    size_t* bytes) {
+  if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
+  rp_status s = check_suffix_cu(m, B, pcu, scu);
+  if (s != RP_OK) return s;
+  *bytes = suffix_ws(m, scu[B], nullptr, nullptr);
+  return RP_OK;
+}
+
+rp_status rp_suffix_logprob(const rp_model* m, void* stream, int32_t B, const int32_t* pcu, const int32_t* scu,
+                            rp_kv kv, const float* h_last, const int32_t* response_ids, float* logprobs, void* ws,
+                            size_t ws_bytes) {
+  if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  rp_status st = check_suffix_cu(m, B, pcu, scu);
+  if (st != RP_OK) return st;
+  const int64_t T = pcu[B], R = scu[B];
+  if ((st = check_kv(m, kv, T, "kv")) != RP_OK) return st;
+  if (!h_last) return fail(RP_ERR_INVALID_ARG, "h_last is NULL");
+  if (!aligned16(h_last)) return fail(RP_ERR_INVALID_ARG, "h_last must be 16-byte aligned");
+  if (R > 0 && (!response_ids || !logprobs)) return fail(RP_ERR_INVALID_ARG, "response_ids and logprobs are required");
+  const size_t need = suffix_ws(m, R, nullptr, nullptr);
+  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
+  if (R == 0) return RP_OK;
+
+  hipStream_t s = (hipStream_t)stream;
+  const rp_config& c = m->cfg;
+  const bool bf = c.dtype == RP_BF16;
+  SuffixWS w;
+  suffix_ws(m, R, ws, &w);
+  const rp::SeqTable tab = make_table(B, scu, pcu);
+  RP_TRY_LAUNCH_N("embed", rp::launch_decode_embed(s, bf, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const void* kl = layer_ptr(m, kv.k, kv.layer_stride, l);
+    const void* vl = layer_ptr(m, kv.v, kv.layer_stride, l);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, 0, nullptr);
+    if (st != RP_OK) return st;
+  }
+  RP_TRY_LAUNCH_N("final_norm", rp::launch_final_norm_rows(s, bf, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
+                                           c.d_model, w.L.N));
+  rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
+  RP_TRY_LAUNCH_N("gemm_lm_head", rp::launch_gemm(s, bf, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
+                                c.vocab, rp::EPI_STORE_F32, 1, nullptr));
+  RP_TRY_LAUNCH_N("logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
+  return RP_OK;
+}
+
+rp_status rp_decode_workspace_bytes(const rp_model* m, int32_t B, int32_t cap, size_t* bytes) {
+  if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
+  if (B < 1 || cap < 1) return fail(RP_ERR_SHAPE, "batch and cap must be >= 1");
+  *bytes = decode_ws(m, B, cap, nullptr, nullptr);
+  return RP_OK;
+}
+
+rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache, int32_t cap, const int32_t* kv_len,
+                         const int32_t* token_ids, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes) {
+  if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  if (B < 1 || cap < 1) return fail(RP_ERR_SHAPE, "batch and cap must be >= 1");
+  if ((int64_t)B * cap > (int64_t)1 << 31) return fail(RP_ERR_UNSUPPORTED, "batch * cap too large");
+  rp_status st = check_kv(m, cache, (int64_t)B * cap, "cache");
+  if (st != RP_OK) return st;
+  if (!kv_len || !token_ids || !next_ids) return fail(RP_ERR_INVALID_ARG, "kv_len, token_ids and next_ids are required");
+  const size_t need = decode_ws(m, B, cap, nullptr, nullptr);
+  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
+
+  hipStream_t s = (hipStream_t)stream;
+  const rp_config& c = m->cfg;
+  const bool bf = c.dtype == RP_BF16;
+  DecodeWS w;
+  decode_ws(m, B, cap, ws, &w);
+  float* lg = logits ? logits : w.logits;
+  const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
+  const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
+  const float scale = (float)(1.0 / sqrt((double)D));
+  RP_TRY_LAUNCH_N("decode_embed", rp::launch_decode_embed(s, bf, token_ids, m->embed, c.vocab, B, d, w.L.X));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const rp_layer_weights& lw = m->layers[l];
+    void* kl = layer_ptr(m, cache.k, cache.layer_stride, l);
+    void* vl = layer_ptr(m, cache.v, cache.layer_stride, l);
+    RP_TRY_LAUNCH_N("decode_rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.attn_norm, c.rms_eps, B, d, w.L.N));
+    rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
+    RP_TRY_LAUNCH_N("decode_gemm_qkv", rp::launch_gemm(s, bf, B, qkv, d, w.L.N, d, bqkv, d, w.L.QKV, qkv, rp::EPI_STORE,
+                                  decode_splitk(c, B, qkv, d), w.gemm_part));
+    RP_TRY_LAUNCH_N("decode_rope_kv", rp::launch_decode_rope_kv(s, bf, w.L.QKV, B, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, kv_len, cap,
+                                            c.max_position, kl, vl));
+    RP_TRY_LAUNCH_N("decode_attention", rp::launch_decode_attention(s, bf, w.L.QKV, qkv, kl, vl, kv_len, cap, c.max_position, B, Hq, Hkv,
+                                              D, scale, w.attn_part, w.L.O));
+    rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
+    RP_TRY_LAUNCH_N("decode_gemm_o_proj", rp::launch_gemm(s, bf, B, d, hq, w.L.O, hq, bo, hq, w.L.X, d, rp::EPI_ADD_F32,
+                                  decode_splitk(c, B, d, hq), w.gemm_part));
+    RP_TRY_LAUNCH_N("decode_rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.mlp_norm, c.rms_eps, B, d, w.L.N));
+    rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
+    RP_TRY_LAUNCH_N("decode_gemm_gate_up", rp::launch_gemm(s, bf, B, 2 * F, d, w.L.N, d, bgu, d, w.L.GU, 2 * F, rp::EPI_STORE,
+                                  decode_splitk(c, B, 2 * F, d), w.gemm_part));
+    RP_TRY_LAUNCH_N("decode_swiglu", rp::launch_swiglu(s, bf, w.L.GU, B, F, w.L.ACT));
+    rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
+    RP_TRY_LAUNCH_N("decode_gemm_down", rp::launch_gemm(s, bf, B, d, F, w.L.ACT, F, bd, F, w.L.X, d, rp::EPI_ADD_F32,
+                                  decode_splitk(c, B, d, F), w.gemm_part));
+  }
+  RP_TRY_LAUNCH_N("decode_final_norm", rp::launch_rmsnorm(s, bf, w.L.X, m->final_norm, c.rms_eps, B, d, w.L.N));
+  rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
+  RP_TRY_LAUNCH_N("decode_gemm_lm_head", rp::launch_gemm(s, bf, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
+                                decode_splitk(c, B, c.vocab, d), w.gemm_part));
+  RP_TRY_LAUNCH_N("argmax", rp::launch_argmax(s, lg, B, c.vocab, next_ids));
+  return RP_OK;
+}
+
+rp_status rp_profile_enable(int enable, int32_t max_launches) {
+  for (hipEvent_t e : g_prof.ev) hipEventDestroy(e);
+  g_prof.ev.clear();
+  g_prof.pending.clear();
+  g_prof.on = false;
+  if (!enable) return RP_OK;
+  if (max_launches < 1) return fail(RP_ERR_INVALID_ARG, "max_launches must be >= 1");
+  g_prof.ev.resize(2 * (size_t)max_launches + 2);
+  for (auto& e : g_prof.ev) {
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      g_prof.ev.clear();
+      return fail(RP_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(r));
+    }
+  }
+  g_prof.on = true;
+  return RP_OK;
+}
+
+rp_status rp_profile_collect(void) {
+  for (size_t k = 0; k < g_prof.pending.size(); ++k) {
+    hipError_t r = hipEventSynchronize(g_prof.ev[2 * k + 1]);
+    float ms = 0.f;
+    if (r == hipSuccess) r = hipEventElapsedTime(&ms, g_prof.ev[2 * k], g_prof.ev[2 * k + 1]);
+    if (r != hipSuccess) {
+      g_prof.pending.clear();
+      return fail(RP_ERR_HIP, "profiling: %s", hipGetErrorString(r));
+    }
+    size_t i = 0;
+    while (i < g_prof.names.size() && g_prof.names[i] != g_prof.pending[k]) ++i;
+    if (i == g_prof.names.size()) {
+      g_prof.names.push_back(g_prof.pending[k]);
+      g_prof.count.push_back(0);
+      g_prof.ms.push_back(0.0);
+    }
+    g_prof.count[i] += 1;
+    g_prof.ms[i] += ms;
+  }
+  g_prof.pending.clear();
+  return RP_OK;
+}
+
+int32_t rp_profile_count(void) { return (int32_t)g_prof.names.size(); }
+
+rp_status rp_profile_read(int32_t i, const char** name, int64_t* launches, double* total_ms) {
+  if (i < 0 || i >= (int32_t)g_prof.names.size()) return fail(RP_ERR_INVALID_ARG, "profile index %d out of range", i);
+  if (name) *name = g_prof.names[i].c_str();
+  if (launches) *launches = g_prof.count[i];
+  if (total_ms) *total_ms = g_prof.ms[i];
+  return RP_OK;
+}
+
+void rp_profile_reset(void) {
+  g_prof.names.clear();
+  g_prof.count.clear();
+  g_prof.ms.clear();
+  g_prof.pending.clear();
+}
+
+rp_status rp_stream_create_cu_masked(int device, const uint32_t* mask, uint32_t n_words, void** out) {
+  if (!out || !mask || n_words == 0) return fail(RP_ERR_INVALID_ARG, "mask, n_words and out are required");
+  *out = nullptr;
+  bool any = false;
+  for (uint32_t i = 0; i < n_words; ++i) any |= mask[i] != 0;
+  if (!any) return fail(RP_ERR_INVALID_ARG, "CU mask selects no compute unit");
+  int prev = 0;
+  hipError_t e = hipGetDevice(&prev);
+  if (e != hipSuccess) return fail(RP_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if ((e = hipSetDevice(device)) != hipSuccess) return fail(RP_ERR_HIP, "hipSetDevice(%d): %s", device, hipGetErrorString(e));
+  hipStream_t s = nullptr;
+  e = hipExtStreamCreateWithCUMask(&s, n_words, mask);
+  hipSetDevice(prev);
+  if (e != hipSuccess) return fail(RP_ERR_HIP, "hipExtStreamCreateWithCUMask: %s", hipGetErrorString(e));
+  *out = (void*)s;
+  return RP_OK;
+}
+
+rp_status rp_stream_destroy(void* stream) {
+  if (!stream) return fail(RP_ERR_INVALID_ARG, "stream is NULL");
+  hipError_t e = hipStreamDestroy((hipStream_t)stream);
+  if (e != hipSuccess) return fail(RP_ERR_HIP, "hipStreamDestroy: %s", hipGetErrorString(e));
+  return RP_OK;
+}
+
+int rp_device_cu_count(int device) {
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) return -1;
+  return n;
+}
+
+}  // extern "C"

@@ -1,0 +1,453 @@
+// Bandwidth-bound kernels of the prefix/suffix path: embedding with visual
+// splice, RMSNorm (+ boundary row assembly), RoPE + KV materialisation,
+// SwiGLU, boundary-state gather, fused log-softmax + gather, argmax.
+// One row per workgroup; 16-byte vector accesses where the row allows.
+#include "device_common.h"
+#include "rp_internal.h"
+
+namespace rp {
+
+// ------------------------------------------------------------------------------------
+// Visual-slot numbering: vis_idx[t] = number of visual slots (id < 0) before t, or -1.
+// One workgroup; each thread scans a contiguous chunk (T is small next to the GEMMs).
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_visual_index(const int32_t* __restrict__ ids, int T,
+                                                       int32_t* __restrict__ vis_idx) {
+  __shared__ int32_t sc[1024];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int chunk = (T + nt - 1) / nt;
+  const int lo = min(T, tid * chunk), hi = min(T, lo + chunk);
+  int c = 0;
+  for (int i = lo; i < hi; ++i) c += ids[i] < 0;
+  sc[tid] = c;
+  __syncthreads();
+  for (int off = 1; off < nt; off <<= 1) {  // inclusive Hillis-Steele scan
+    int v = tid >= off ? sc[tid - off] : 0;
+    __syncthreads();
+    sc[tid] += v;
+    __syncthreads();
+  }
+  int run = sc[tid] - c;
+  for (int i = lo; i < hi; ++i) vis_idx[i] = ids[i] < 0 ? run++ : -1;
+}
+
+hipError_t launch_visual_index(hipStream_t s, const int32_t* ids, int32_t T, int32_t* vis_idx) {
+  k_visual_index<<<1, 1024, 0, s>>>(ids, T, vis_idx);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Embedding + visual splice -> fp32 residual rows.
+// ------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ ids,
+                                               const int32_t* __restrict__ vis_idx,
+                                               const T* __restrict__ visual, int64_t n_visual,
+                                               const T* __restrict__ embed, int vocab, int d,
+                                               float* __restrict__ X) {
+  const int t = blockIdx.x;
+  const int id = ids[t];
+  const T* src = nullptr;
+  if (id < 0) {
+    const int vi = vis_idx[t];
+    if (vi >= 0 && vi < n_visual) src = visual + (int64_t)vi * d;
+  } else {
+    src = embed + (int64_t)min(id, vocab - 1) * d;
+  }
+  float* dst = X + (int64_t)t * d;
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (src) load8(src + c, v);
+    store8(dst + c, v);
+  }
+}
+
+hipError_t launch_embed(hipStream_t s, bool bf16, const int32_t* ids, const int32_t* vis_idx,
+                        const void* visual, int64_t n_visual, const void* embed, int32_t vocab,
+                        int32_t T, int32_t d, float* X) {
+  if (T <= 0) return hipSuccess;
+  if (bf16)
+    k_embed<bf16_t><<<T, 256, 0, s>>>(ids, vis_idx, (const bf16_t*)visual, n_visual,
+                                      (const bf16_t*)embed, vocab, d, X);
+  else
+    k_embed<float><<<T, 256, 0, s>>>(ids, vis_idx, (const float*)visual, n_visual,
+                                     (const float*)embed, vocab, d, X);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_decode_embed(const int32_t* __restrict__ ids,
+                                                      const T* __restrict__ embed, int vocab, int d,
+                                                      float* __restrict__ X) {
+  const int b = blockIdx.x;
+  const T* src = embed + (int64_t)min(max(ids[b], 0), vocab - 1) * d;
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8];
+    load8(src + c, v);
+    store8(X + (int64_t)b * d + c, v);
+  }
+}
+
+hipError_t launch_decode_embed(hipStream_t s, bool bf16, const int32_t* ids, const void* embed,
+                               int32_t vocab, int32_t B, int32_t d, float* X) {
+  if (bf16)
+    k_decode_embed<bf16_t><<<B, 256, 0, s>>>(ids, (const bf16_t*)embed, vocab, d, X);
+  else
+    k_decode_embed<float><<<B, 256, 0, s>>>(ids, (const float*)embed, vocab, d, X);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// RMSNorm: out = x / sqrt(mean(x^2) + eps) * w, fp32 math, stored as T.
+// ------------------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ void rmsnorm_row(const float* __restrict__ x, const T* __restrict__ w,
+                                            float eps, int d, T* __restrict__ out, float* red) {
+  float ss = 0.f;
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8];
+    load8(x + c, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
+  }
+  const float tot = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8], g[8];
+    load8(x + c, v);
+    load8(w + c, g);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = v[i] * inv * g[i];
+    store8(out + c, v);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X, const T* __restrict__ w,
+                                                 float eps, int d, T* __restrict__ out) {
+  __shared__ float red[16];
+  const int64_t r = blockIdx.x;
+  rmsnorm_row(X + r * d, w, eps, d, out + r * d, red);
+}
+
+hipError_t launch_rmsnorm(hipStream_t s, bool bf16, const float* X, const void* w, float eps, int32_t M,
+                          int32_t d, void* out) {
+  if (M <= 0) return hipSuccess;
+  if (bf16)
+    k_rmsnorm<bf16_t><<<M, 256, 0, s>>>(X, (const bf16_t*)w, eps, d, (bf16_t*)out);
+  else
+    k_rmsnorm<float><<<M, 256, 0, s>>>(X, (const float*)w, eps, d, (float*)out);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_final_norm_rows(SeqTable st, const float* __restrict__ Y,
+                                                         const float* __restrict__ h_last,
+                                                         const T* __restrict__ w, float eps, int d,
+                                                         T* __restrict__ out) {
+  __shared__ float red[16];
+  const int r = blockIdx.x;
+  const int b = seq_of_row(st, r);
+  const float* src = (r == st.q_cu[b]) ? h_last + (int64_t)b * d : Y + (int64_t)(r - 1) * d;
+  rmsnorm_row(src, w, eps, d, out + (int64_t)r * d, red);
+}
+
+hipError_t launch_final_norm_rows(hipStream_t s, bool bf16, const SeqTable& st, const float* Y,
+                                  const float* h_last, const void* w, float eps, int32_t R, int32_t d,
+                                  void* out) {
+  if (R <= 0) return hipSuccess;
+  if (bf16)
+    k_final_norm_rows<bf16_t><<<R, 256, 0, s>>>(st, Y, h_last, (const bf16_t*)w, eps, d, (bf16_t*)out);
+  else
+    k_final_norm_rows<float><<<R, 256, 0, s>>>(st, Y, h_last, (const float*)w, eps, d, (float*)out);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// RoPE (rotate-half pairs (i, i+D/2)) + optional q/k/v bias + KV materialisation.
+// q is rotated in place inside the qkv rows; k (rotated) and v go to k_out/v_out.
+// ------------------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ void rope_row(T* __restrict__ row, int pos, int Hq, int Hkv, int D,
+                                         const T* __restrict__ bq, const T* __restrict__ bk,
+                                         const T* __restrict__ bv, const RopeFreq& rf,
+                                         T* __restrict__ k_dst, T* __restrict__ v_dst, float* cs) {
+  const int half = D >> 1;
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    float c, s;
+    rope_cs(pos, rf.inv_freq[i], &c, &s);
+    cs[i] = c;
+    cs[64 + i] = s;
+  }
+  __syncthreads();
+  const int nq = Hq * half, nk = Hkv * half;
+  for (int p = threadIdx.x; p < nq + nk; p += blockDim.x) {
+    const bool isq = p < nq;
+    const int pp = isq ? p : p - nq;
+    const int h = pp / half, i = pp - h * half;
+    const int col = (isq ? 0 : Hq * D) + h * D + i;
+    float x1 = ldf(row + col), x2 = ldf(row + col + half);
+    const T* b = isq ? bq : bk;
+    if (b) {
+      x1 += ldf(b + h * D + i);
+      x2 += ldf(b + h * D + i + half);
+    }
+    const float c = cs[i], s = cs[64 + i];
+    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+    if (isq) {
+      stf(row + col, y1);
+      stf(row + col + half, y2);
+    } else {
+      stf(k_dst + h * D + i, y1);
+      stf(k_dst + h * D + i + half, y2);
+    }
+  }
+  const int vbase = (Hq + Hkv) * D;
+  for (int e = threadIdx.x; e < Hkv * D; e += blockDim.x) {
+    float v = ldf(row + vbase + e);
+    if (bv) v += ldf(bv + e);
+    stf(v_dst + e, v);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_rope_kv(SeqTable st, T* __restrict__ qkv, int Hq, int Hkv, int D,
+                                                 const T* __restrict__ bq, const T* __restrict__ bk,
+                                                 const T* __restrict__ bv, RopeFreq rf, int max_pos,
+                                                 T* __restrict__ k_out, T* __restrict__ v_out) {
+  __shared__ float cs[128];
+  const int r = blockIdx.x;
+  const int b = seq_of_row(st, r);
+  const int pos = min(st.pos0(b) + (r - st.q_cu[b]), max_pos - 1);
+  const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
+  rope_row<T>(qkv + r * ld, pos, Hq, Hkv, D, bq, bk, bv, rf, k_out + (int64_t)r * Hkv * D,
+              v_out + (int64_t)r * Hkv * D, cs);
+}
+
+hipError_t launch_rope_kv(hipStream_t s, bool bf16, const SeqTable& st, void* qkv, int32_t M,
+                          int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
+                          const void* bv, const RopeFreq& rf, int32_t max_pos, void* k_out,
+                          void* v_out) {
+  if (M <= 0) return hipSuccess;
+  if (bf16)
+    k_rope_kv<bf16_t><<<M, 256, 0, s>>>(st, (bf16_t*)qkv, Hq, Hkv, D, (const bf16_t*)bq,
+                                        (const bf16_t*)bk, (const bf16_t*)bv, rf, max_pos,
+                                        (bf16_t*)k_out, (bf16_t*)v_out);
+  else
+    k_rope_kv<float><<<M, 256, 0, s>>>(st, (float*)qkv, Hq, Hkv, D, (const float*)bq,
+                                       (const float*)bk, (const float*)bv, rf, max_pos,
+                                       (float*)k_out, (float*)v_out);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_decode_rope_kv(T* __restrict__ qkv, int Hq, int Hkv, int D,
+                                                        const T* __restrict__ bq, const T* __restrict__ bk,
+                                                        const T* __restrict__ bv, RopeFreq rf,
+                                                        const int32_t* __restrict__ kv_len, int cap,
+                                                        int max_pos, T* __restrict__ ck,
+                                                        T* __restrict__ cv) {
+  __shared__ float cs[128];
+  const int b = blockIdx.x;
+  const int slot = min(max(kv_len[b], 0), min(cap, max_pos) - 1);
+  const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
+  const int64_t dst = ((int64_t)b * cap + slot) * Hkv * D;
+  rope_row<T>(qkv + b * ld, slot, Hq, Hkv, D, bq, bk, bv, rf, ck + dst, cv + dst, cs);
+}
+
+hipError_t launch_decode_rope_kv(hipStream_t s, bool bf16, void* qkv, int32_t B, int32_t Hq, int32_t Hkv,
+                                 int32_t D, const void* bq, const void* bk, const void* bv,
+                                 const RopeFreq& rf, const int32_t* kv_len, int32_t cap, int32_t max_pos,
+                                 void* cache_k, void* cache_v) {
+  if (bf16)
+    k_decode_rope_kv<bf16_t><<<B, 256, 0, s>>>((bf16_t*)qkv, Hq, Hkv, D, (const bf16_t*)bq,
+                                               (const bf16_t*)bk, (const bf16_t*)bv, rf, kv_len, cap,
+                                               max_pos, (bf16_t*)cache_k, (bf16_t*)cache_v);
+  else
+    k_decode_rope_kv<float><<<B, 256, 0, s>>>((float*)qkv, Hq, Hkv, D, (const float*)bq,
+                                              (const float*)bk, (const float*)bv, rf, kv_len, cap,
+                                              max_pos, (float*)cache_k, (float*)cache_v);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// SwiGLU: act[m, j] = silu(gu[m, j]) * gu[m, F + j]
+// ------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_swiglu(const T* __restrict__ gu, int64_t M, int F,
+                                                T* __restrict__ act) {
+  const int64_t per_row = F / 8;
+  const int64_t n = M * per_row;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t m = i / per_row;
+    const int j = (int)(i - m * per_row) * 8;
+    float g[8], u[8], o[8];
+    load8(gu + m * 2 * F + j, g);
+    load8(gu + m * 2 * F + F + j, u);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = g[e] / (1.0f + expf(-g[e])) * u[e];
+    store8(act + m * F + j, o);
+  }
+}
+
+hipError_t launch_swiglu(hipStream_t s, bool bf16, const void* gu, int32_t M, int32_t F, void* act) {
+  if (M <= 0) return hipSuccess;
+  const int64_t n = (int64_t)M * (F / 8);
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 256 * 64);
+  if (bf16)
+    k_swiglu<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)gu, M, F, (bf16_t*)act);
+  else
+    k_swiglu<float><<<blocks, 256, 0, s>>>((const float*)gu, M, F, (float*)act);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Boundary state: h_last[b] = X[q_cu[b+1]-1].
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_gather_rows(SeqTable st, const float* __restrict__ X, int d,
+                                                     float* __restrict__ h_last) {
+  const int b = blockIdx.x;
+  const float* src = X + (int64_t)(st.q_cu[b + 1] - 1) * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) h_last[(int64_t)b * d + c] = src[c];
+}
+
+hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X, int32_t d, float* h_last) {
+  k_gather_rows<<<st.n, 256, 0, s>>>(st, X, d, h_last);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Fused log-softmax + gather: lp[r] = l[r, id_r] - (m + log sum exp(l - m)), one pass
+// over the row with a running (max, scaled sum) per thread, merged across the block.
+// ------------------------------------------------------------------------------------
+__device__ __forceinline__ void lse_merge(float& m, float& s, float mo, float so) {
+  const float mn = fmaxf(m, mo);
+  if (mn == -INFINITY) return;
+  s = (m == -INFINITY ? 0.f : s * exp2f(m - mn)) + (mo == -INFINITY ? 0.f : so * exp2f(mo - mn));
+  m = mn;
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <int NT>
+__global__ __launch_bounds__(NT) void k_logsoftmax_gather(const float* __restrict__ logits,
+                                                          const int32_t* __restrict__ ids, int V,
+                                                          float* __restrict__ lp) {
+  const int r = blockIdx.x;
+  const float* row = logits + (int64_t)r * V;
+  float m = -INFINITY, s = 0.f;  // in log2 units
+  if ((V & 3) == 0) {
+    const f32x4_t* row4 = reinterpret_cast<const f32x4_t*>(row);
+    const int n4 = V >> 2;
+    int i = threadIdx.x;
+    for (; i + 3 * NT < n4; i += 4 * NT) {
+      f32x4_t a[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a[u] = __builtin_nontemporal_load(row4 + i + u * NT);
+      float mx = m;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        mx = fmaxf(mx, fmaxf(fmaxf(a[u].x, a[u].y), fmaxf(a[u].z, a[u].w)) * kLog2e);
+      float acc = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        acc += exp2f(fmaf(a[u].x, kLog2e, -mx)) + exp2f(fmaf(a[u].y, kLog2e, -mx)) +
+               exp2f(fmaf(a[u].z, kLog2e, -mx)) + exp2f(fmaf(a[u].w, kLog2e, -mx));
+      }
+      s = (m == -INFINITY ? 0.f : s * exp2f(m - mx)) + acc;
+      m = mx;
+    }
+    for (; i < n4; i += NT) {
+      const f32x4_t a = row4[i];
+      const float mx = fmaxf(m, fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w)) * kLog2e);
+      const float acc = exp2f(fmaf(a.x, kLog2e, -mx)) + exp2f(fmaf(a.y, kLog2e, -mx)) +
+                        exp2f(fmaf(a.z, kLog2e, -mx)) + exp2f(fmaf(a.w, kLog2e, -mx));
+      s = (m == -INFINITY ? 0.f : s * exp2f(m - mx)) + acc;
+      m = mx;
+    }
+  } else {
+    for (int i = threadIdx.x; i < V; i += NT) {
+      const float x = row[i] * kLog2e;
+      const float mx = fmaxf(m, x);
+      s = (m == -INFINITY ? 0.f : s * exp2f(m - mx)) + exp2f(x - mx);
+      m = mx;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float mo = __shfl_xor(m, o, kWave), so = __shfl_xor(s, o, kWave);
+    lse_merge(m, s, mo, so);
+  }
+  __shared__ float sm[NT / 64], ss[NT / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) {
+    sm[w] = m;
+    ss[w] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = sm[0], S = ss[0];
+    for (int k = 1; k < NT / 64; ++k) lse_merge(M, S, sm[k], ss[k]);
+    const int id = min(max(ids[r], 0), V - 1);
+    lp[r] = row[id] - (M + log2f(S)) * kLn2;
+  }
+}
+
+hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const int32_t* ids, int32_t R,
+                                    int32_t V, float* lp) {
+  if (R <= 0) return hipSuccess;
+  k_logsoftmax_gather<256><<<R, 256, 0, s>>>(logits, ids, V, lp);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------
+// Greedy argmax per row (lowest index on ties).
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_argmax(const float* __restrict__ logits, int V,
+                                                int32_t* __restrict__ out) {
+  const int b = blockIdx.x;
+  const float* row = logits + (int64_t)b * V;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int i = threadIdx.x; i < V; i += blockDim.x) {
+    const float x = row[i];
+    if (x > best) {  // i increases per thread: strict > keeps the lowest index
+      best = x;
+      bi = i;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float vb = __shfl_xor(best, o, kWave);
+    const int ib = __shfl_xor(bi, o, kWave);
+    if (vb > best || (vb == best && ib < bi)) {
+      best = vb;
+      bi = ib;
+    }
+  }
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) {
+    sv[w] = best;
+    si[w] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < 4; ++k)
+      if (sv[k] > best || (sv[k] == best && si[k] < bi)) {
+        best = sv[k];
+        bi = si[k];
+      }
+    out[b] = bi == 0x7fffffff ? -1 : bi;
+  }
+}
+
+hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t V, int32_t* out) {
+  k_argmax<<<B, 256, 0, s>>>(logits, V, out);
+  return hipGetLastError();
+}
+
+}  // namespace rp

@@ -1,0 +1,111 @@
+// Internal interface between the host runtime (api.cpp) and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/rollplex.h"
+
+namespace rp {
+
+// Per-call sequence table passed by value as a kernel argument, so that launch
+// geometry and row->sequence lookups need no device copy of the host lengths.
+// The position of sequence b's first query row equals the length of its first key
+// segment (0 in the prefix pass, P_b in the suffix pass).
+struct SeqTable {
+  int32_t n;                       // sequences
+  int32_t q_cu[RP_MAX_SEQS + 1];   // query rows of sequence b: q_cu[b] .. q_cu[b+1]-1
+  int32_t k_cu[RP_MAX_SEQS + 1];   // rows of the first key segment (prefix KV) of sequence b
+  __host__ __device__ int32_t pos0(int b) const { return k_cu[b + 1] - k_cu[b]; }
+};
+
+// Row r of the packed queries -> sequence index (binary search over q_cu).
+__host__ __device__ inline int seq_of_row(const SeqTable& t, int r) {
+  int lo = 0, hi = t.n - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (t.q_cu[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+struct RopeFreq {
+  double inv_freq[64];  // theta^(-2i/Dh), i < Dh/2 (host float64)
+};
+
+enum Epi : int {
+  EPI_STORE = 0,      // C[T] = acc
+  EPI_STORE_F32 = 1,  // C[f32] = acc
+  EPI_ADD_F32 = 2,    // C[f32] += acc  (residual stream)
+};
+
+// B operand of a GEMM given as up to three row segments of nn.Linear weights:
+// logical row n < n1 -> b0 + n*ldb; n < n2 -> b1 + (n-n1)*ldb; else b2 + (n-n2)*ldb.
+struct BSeg {
+  const void* b0;
+  const void* b1;
+  const void* b2;
+  int32_t n1, n2;
+};
+
+// ---- launchers (return hipGetLastError() of the launch) ----
+hipError_t launch_visual_index(hipStream_t s, const int32_t* ids, int32_t T, int32_t* vis_idx);
+hipError_t launch_embed(hipStream_t s, bool bf16, const int32_t* ids, const int32_t* vis_idx,
+                        const void* visual, int64_t n_visual, const void* embed, int32_t vocab,
+                        int32_t T, int32_t d, float* X);
+hipError_t launch_rmsnorm(hipStream_t s, bool bf16, const float* X, const void* w, float eps, int32_t M,
+                          int32_t d, void* out);
+// Final norm of the suffix rows with boundary assembly: row r of sequence b reads
+// h_last[b] if it is the sequence's first response row, else Y[r-1].
+hipError_t launch_final_norm_rows(hipStream_t s, bool bf16, const SeqTable& st, const float* Y,
+                                  const float* h_last, const void* w, float eps, int32_t R, int32_t d,
+                                  void* out);
+hipError_t launch_rope_kv(hipStream_t s, bool bf16, const SeqTable& st, void* qkv, int32_t M,
+                          int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
+                          const void* bv, const RopeFreq& rf, int32_t max_pos, void* k_out, void* v_out);
+hipError_t launch_swiglu(hipStream_t s, bool bf16, const void* gu, int32_t M, int32_t F, void* act);
+hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X, int32_t d, float* h_last);
+hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const int32_t* ids, int32_t R,
+                                    int32_t V, float* lp);
+hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t V, int32_t* out);
+
+// GEMM: C[M,N] (epi)= A[M,K] . B[N,K]^T, fp32 accumulation.
+hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K, const void* A,
+                       int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
+                       int32_t splitk, float* partials);
+// Required float count of `partials` for a split-K GEMM.
+size_t gemm_partial_floats(int32_t M, int32_t N, int32_t splitk);
+
+// Attention over packed sequences.  Queries: rows st.q_cu[b].. of q (row stride q_ld,
+// head h at column h*D), positions st.pos0(b) + i.  Keys: segment 0 = rows st.k_cu[b]..
+// (st.k_cu[b+1]-st.k_cu[b] rows, positions 0..) of k0/v0; segment 1 = the query rows
+// themselves of k1/v1 (positions st.pos0(b)+j).  Key visible iff key pos <= query pos.
+// k/v rows are [Hkv][D] contiguous.  Output o rows [Hq*D].
+struct AttnArgs {
+  const void* q;
+  int32_t q_ld;
+  const void* k0;
+  const void* v0;
+  const void* k1;
+  const void* v1;
+  void* o;
+  int32_t Hq, Hkv, D;
+  float scale;
+};
+hipError_t launch_attention(hipStream_t s, bool bf16, const SeqTable& st, const AttnArgs& a,
+                            int32_t total_q);
+
+// Decode step pieces.
+hipError_t launch_decode_embed(hipStream_t s, bool bf16, const int32_t* ids, const void* embed,
+                               int32_t vocab, int32_t B, int32_t d, float* X);
+hipError_t launch_decode_rope_kv(hipStream_t s, bool bf16, void* qkv, int32_t B, int32_t Hq, int32_t Hkv,
+                                 int32_t D, const void* bq, const void* bk, const void* bv,
+                                 const RopeFreq& rf, const int32_t* kv_len, int32_t cap, int32_t max_pos,
+                                 void* cache_k, void* cache_v);
+size_t decode_attn_partial_floats(int32_t B, int32_t Hq, int32_t D, int32_t cap);
+hipError_t launch_decode_attention(hipStream_t s, bool bf16, const void* q, int32_t q_ld,
+                                   const void* cache_k, const void* cache_v, const int32_t* kv_len,
+                                   int32_t cap, int32_t max_pos, int32_t B, int32_t Hq, int32_t Hkv,
+                                   int32_t D, float scale, float* partials, void* o);
+
+}  // namespace rp

@@ -1,0 +1,190 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared symbol,
+and rejects bad arguments (with a message) before making any HIP call."""
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+from paper_2608_14498_amd import binding as rb
+from paper_2608_14498_amd import configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rollplex.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rb.LIB_PATH):
+        pytest.fail("librollplex.so is not built (python -m paper_2608_14498_amd.build)")
+    return rb.lib()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:rp_status|void|int|int32_t|const char \*)\s*(rp_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_what_binding_wraps():
+    assert declared_symbols() == sorted(rb.SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", rb.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (rp_\w+)", out))
+    missing = [s for s in declared_symbols() if s not in exported]
+    assert not missing, missing
+    assert "gfx950" in rb.rp_version()
+
+
+FAKE = 0x7f0000000000  # never dereferenced: every call below fails validation first
+
+
+def fake_weights(model, align=256):
+    layers = (rb.RpLayerWeights * model.n_layers)()
+    addr = FAKE
+    for i in range(model.n_layers):
+        for name, _ in rb.RpLayerWeights._fields_:
+            if name in ("bq", "bk", "bv"):
+                continue
+            setattr(layers[i], name, addr)
+            addr += align * 64
+    w = rb.RpWeights(addr, addr + align * 64, addr + align * 128, layers)
+    return w, layers
+
+
+def make(model=configs.TINY, max_pos=1024, **over):
+    cfg = rb.make_config(model, max_pos)
+    for k, v in over.items():
+        setattr(cfg, k, v)
+    w, keep = fake_weights(model)
+    return rb.rp_create(cfg, w), (w, keep)
+
+
+def status_of(fn, *args):
+    try:
+        fn(*args)
+    except rb.RollplexError as e:
+        return e.status, str(e)
+    return rb.RP_OK, ""
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("dtype", 7, rb.RP_ERR_INVALID_ARG),
+    ("head_dim", 96, rb.RP_ERR_UNSUPPORTED),
+    ("n_kv_heads", 3, rb.RP_ERR_SHAPE),
+    ("n_layers", 0, rb.RP_ERR_SHAPE),
+    ("rms_eps", 0.0, rb.RP_ERR_SHAPE),
+    ("d_model", 100, rb.RP_ERR_UNSUPPORTED),
+])
+def test_create_rejects_bad_config(lib, field, value, status):
+    cfg = rb.make_config(configs.TINY, 1024)
+    setattr(cfg, field, value)
+    w, _ = fake_weights(configs.TINY)
+    st, msg = status_of(rb.rp_create, cfg, w)
+    assert st == status and len(msg) > 12
+
+
+def test_create_rejects_missing_and_misaligned_weights(lib):
+    cfg = rb.make_config(configs.QWEN7B_SLICE, 8192)
+    w, layers = fake_weights(configs.QWEN7B_SLICE)
+    layers[1].w_up = None
+    assert status_of(rb.rp_create, cfg, w)[0] == rb.RP_ERR_INVALID_ARG
+    w, layers = fake_weights(configs.QWEN7B_SLICE)
+    layers[0].wq = FAKE + 2
+    st, msg = status_of(rb.rp_create, cfg, w)
+    assert st == rb.RP_ERR_INVALID_ARG and "aligned" in msg
+
+
+def test_create_and_workspace_sizes(lib):
+    h, keep = make()
+    try:
+        n = rb.rp_prefix_workspace_bytes(h, 2, [0, 512, 1024])
+        assert n > 1024 * 256 * 4
+        s = rb.rp_suffix_workspace_bytes(h, 2, [0, 512, 1024], [0, 64, 128])
+        assert s > 128 * 2048 * 4  # holds the fp32 logits
+        assert rb.rp_suffix_workspace_bytes(h, 2, [0, 512, 1024], [0, 0, 0]) > 0
+        assert rb.rp_decode_workspace_bytes(h, 4, 100) > 4 * 2048 * 4
+    finally:
+        rb.rp_destroy(h)
+
+
+@pytest.mark.parametrize("B,cu,status", [
+    (0, [0], rb.RP_ERR_SHAPE),
+    (2, [1, 5, 9], rb.RP_ERR_SHAPE),
+    (2, [0, 5, 5], rb.RP_ERR_SHAPE),
+    (2, [0, 7, 3], rb.RP_ERR_SHAPE),
+    (1, [0, 2000], rb.RP_ERR_SHAPE),          # longer than max_position
+    (rb.RP_MAX_SEQS + 1, list(range(rb.RP_MAX_SEQS + 2)), rb.RP_ERR_SHAPE),
+])
+def test_bad_prefix_lengths(lib, B, cu, status):
+    h, keep = make()
+    try:
+        st, msg = status_of(rb.rp_prefix_workspace_bytes, h, B, cu)
+        assert st == status and msg
+    finally:
+        rb.rp_destroy(h)
+
+
+def test_bad_suffix_lengths(lib):
+    h, keep = make()
+    try:
+        assert status_of(rb.rp_suffix_workspace_bytes, h, 2, [0, 4, 8], [0, 3, 2])[0] == rb.RP_ERR_SHAPE
+        assert status_of(rb.rp_suffix_workspace_bytes, h, 1, [0, 1000], [0, 30])[0] == rb.RP_ERR_SHAPE
+        assert status_of(rb.rp_suffix_workspace_bytes, h, 1, [0, 10], [1, 30])[0] == rb.RP_ERR_SHAPE
+    finally:
+        rb.rp_destroy(h)
+
+
+def _prefix_args(h, T=64, ws_bytes=None, stride=None, tokens=FAKE, ws=FAKE + (1 << 30)):
+    m = configs.TINY
+    kv = rb.make_kv(FAKE + (1 << 32), FAKE + (1 << 33),
+                    stride if stride is not None else T * m.n_kv_heads * m.head_dim)
+    need = rb.rp_prefix_workspace_bytes(h, 1, [0, T])
+    return (h, None, 1, [0, T], tokens, None, 0, kv, FAKE + (1 << 34), None, ws,
+            need if ws_bytes is None else ws_bytes)
+
+
+def test_prefix_forward_validation(lib):
+    h, keep = make()
+    try:
+        args = list(_prefix_args(h))
+        args[4] = None
+        assert status_of(rb.rp_prefix_forward, *args)[0] == rb.RP_ERR_INVALID_ARG
+        assert status_of(rb.rp_prefix_forward, *_prefix_args(h, stride=10))[0] == rb.RP_ERR_SHAPE
+        st, msg = status_of(rb.rp_prefix_forward, *_prefix_args(h, ws_bytes=1000))
+        assert st == rb.RP_ERR_WORKSPACE and "workspace" in msg
+        assert status_of(rb.rp_prefix_forward, *_prefix_args(h, ws=FAKE + 8))[0] == rb.RP_ERR_INVALID_ARG
+        args = list(_prefix_args(h))
+        args[6] = 5  # n_visual > 0 with no visual pointer
+        assert status_of(rb.rp_prefix_forward, *args)[0] == rb.RP_ERR_INVALID_ARG
+    finally:
+        rb.rp_destroy(h)
+
+
+def test_empty_suffix_is_a_no_op(lib):
+    h, keep = make()
+    try:
+        m = configs.TINY
+        kv = rb.make_kv(FAKE, FAKE + (1 << 30), 8 * m.n_kv_heads * m.head_dim)
+        need = rb.rp_suffix_workspace_bytes(h, 2, [0, 4, 8], [0, 0, 0])
+        rb.rp_suffix_logprob(h, None, 2, [0, 4, 8], [0, 0, 0], kv, FAKE + (1 << 31), None, None,
+                             FAKE + (1 << 32), need)
+    finally:
+        rb.rp_destroy(h)
+
+
+def test_launch_fault_injection_reports_hip_error():
+    """RP_FAULT_INJECT makes the first launch fail before any HIP call is made."""
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "from tests.test_abi_cpu import make, _prefix_args, status_of\n"
+        "from paper_2608_14498_amd import binding as rb\n"
+        "h, keep = make()\n"
+        "st, msg = status_of(rb.rp_prefix_forward, *_prefix_args(h))\n"
+        "print(st, msg)\n"
+        "assert st == rb.RP_ERR_HIP and 'injected' in msg\n" % ROOT)
+    env = dict(os.environ, RP_FAULT_INJECT="1")
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
