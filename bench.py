@@ -148,14 +148,14 @@ def main():
     sf = perf.suffix_flops(m, bt.prefix_lens, bt.suffix_lens)
     peak = perf.PEAK_BF16_FLOPS if m.dtype == "bf16" else perf.PEAK_FP32_FLOPS
     gu_flops = perf.gemm_flops(T, 2 * m.ffn_dim, m.d_model)
-    gu = kernels.get("gemm_gate_up")
+    gu = kernels.get("prefix.gemm_gate_up")
     roofline = None
     if gu:
         ach = gu_flops / (gu["avg_ms"] * 1e-3) / 1e12
         roofline = {"kernel": "gemm_gate_up (prefix)", "bound": "mfma", "achieved": ach,
                     "peak": peak / 1e12, "unit": "TFLOP/s", "frac": ach / (peak / 1e12),
                     "traffic": None, "algorithmic_per_launch": gu_flops}
-    ls = kernels.get("logsoftmax_gather")
+    ls = kernels.get("suffix.logsoftmax_gather")
     k12 = None
     if ls:
         gbs = perf.logsoftmax_bytes(R, m.vocab) / (ls["avg_ms"] * 1e-3) / 1e9

@@ -107,14 +107,17 @@ struct LayerWS {
   void* ACT;  // [M, F]
 };
 
-void carve_layer(Carver& c, const rp_config& cfg, int64_t M, bool need_x, LayerWS* w) {
+// bf16 prefix/suffix layers fuse SwiGLU into the gate/up GEMM and need no [M, 2F] buffer.
+bool fused_swiglu(const rp_config& cfg, bool split_gemms) { return cfg.dtype == RP_BF16 && !split_gemms; }
+
+void carve_layer(Carver& c, const rp_config& cfg, int64_t M, bool need_x, bool need_gu, LayerWS* w) {
   const size_t es = elem_size(cfg);
   const int64_t d = cfg.d_model, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
   w->X = need_x ? (float*)c.take(M * d * 4) : nullptr;
   w->N = c.take(M * d * es);
   w->QKV = c.take(M * qkv * es);
   w->O = c.take(M * (int64_t)cfg.n_q_heads * cfg.head_dim * es);
-  w->GU = c.take(M * 2 * (int64_t)cfg.ffn_dim * es);
+  w->GU = need_gu ? c.take(M * 2 * (int64_t)cfg.ffn_dim * es) : nullptr;
   w->ACT = c.take(M * (int64_t)cfg.ffn_dim * es);
 }
 
@@ -187,7 +190,7 @@ size_t prefix_ws(const rp_model* m, int64_t T, void* base, bool need_x, LayerWS*
   int32_t* vi = (int32_t*)c.take(T * 4);
   if (vis_idx) *vis_idx = vi;
   LayerWS tmp;
-  carve_layer(c, m->cfg, T, need_x, w ? w : &tmp);
+  carve_layer(c, m->cfg, T, need_x, !fused_swiglu(m->cfg, false), w ? w : &tmp);
   return c.off + 256;
 }
 
@@ -202,7 +205,7 @@ size_t suffix_ws(const rp_model* m, int64_t R, void* base, SuffixWS* w) {
   Carver c(base);
   SuffixWS tmp;
   SuffixWS* s = w ? w : &tmp;
-  carve_layer(c, m->cfg, R, true, &s->L);
+  carve_layer(c, m->cfg, R, true, !fused_swiglu(m->cfg, false), &s->L);
   const int64_t kvrow = (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim;
   s->Ks = c.take(R * kvrow * elem_size(m->cfg));
   s->Vs = c.take(R * kvrow * elem_size(m->cfg));
@@ -233,7 +236,7 @@ size_t decode_ws(const rp_model* m, int32_t B, int32_t cap, void* base, DecodeWS
   DecodeWS tmp;
   DecodeWS* s = w ? w : &tmp;
   const rp_config& cfg = m->cfg;
-  carve_layer(c, cfg, B, true, &s->L);
+  carve_layer(c, cfg, B, true, true, &s->L);
   s->logits = (float*)c.take((int64_t)B * cfg.vocab * 4);
   s->attn_part = (float*)c.take(rp::decode_attn_partial_floats(B, cfg.n_q_heads, cfg.head_dim, cap) * 4);
   const int64_t d = cfg.d_model, F = cfg.ffn_dim, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
@@ -271,18 +274,29 @@ void* layer_ptr(const rp_model* m, void* base, int64_t stride, int l) {
 
 // One decoder layer over M rows; keys/values go to k_out/v_out (rows aligned with
 // the query rows); attention reads segment 0 from k0/v0 as described by st.
+// Kernel names reported by the per-launch timer, per pass.
+struct LayerNames {
+  const char *norm1, *qkv, *rope, *attn, *oproj, *norm2, *gate_up, *swiglu, *down;
+};
+const LayerNames kPrefixNames = {"prefix.rmsnorm", "prefix.gemm_qkv", "prefix.rope_kv", "prefix.attention",
+                                 "prefix.gemm_o_proj", "prefix.rmsnorm", "prefix.gemm_gate_up", "prefix.swiglu",
+                                 "prefix.gemm_down"};
+const LayerNames kSuffixNames = {"suffix.rmsnorm", "suffix.gemm_qkv", "suffix.rope_kv", "suffix.attention",
+                                 "suffix.gemm_o_proj", "suffix.rmsnorm", "suffix.gemm_gate_up", "suffix.swiglu",
+                                 "suffix.gemm_down"};
+
 rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, const rp::SeqTable& st,
                     int32_t M, const LayerWS& w, void* k_out, void* v_out, const void* k0, const void* v0,
-                    int splitk_ok, float* gemm_part) {
+                    int splitk_ok, float* gemm_part, const LayerNames& nm) {
   const rp_config& c = m->cfg;
   const bool bf = c.dtype == RP_BF16;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
   auto sk = [&](int N, int K) { return splitk_ok ? decode_splitk(c, M, N, K) : 1; };
-  RP_TRY_LAUNCH_N("rmsnorm", rp::launch_rmsnorm(s, bf, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
+  RP_TRY_LAUNCH_N(nm.norm1, rp::launch_rmsnorm(s, bf, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
-  RP_TRY_LAUNCH_N("gemm_qkv", rp::launch_gemm(s, bf, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE, sk(qkv, d), gemm_part));
-  RP_TRY_LAUNCH_N("rope_kv", rp::launch_rope_kv(s, bf, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position,
+  RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, bf, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE, sk(qkv, d), gemm_part));
+  RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv(s, bf, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position,
                                    k_out, v_out));
   rp::AttnArgs a;
   a.q = w.QKV;
@@ -296,16 +310,20 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   a.Hkv = Hkv;
   a.D = D;
   a.scale = (float)(1.0 / sqrt((double)D));
-  RP_TRY_LAUNCH_N("attention", rp::launch_attention(s, bf, st, a, M));
+  RP_TRY_LAUNCH_N(nm.attn, rp::launch_attention(s, bf, st, a, M));
   rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
-  RP_TRY_LAUNCH_N("gemm_o_proj", rp::launch_gemm(s, bf, M, d, hq, w.O, hq, bo, hq, w.X, d, rp::EPI_ADD_F32, sk(d, hq), gemm_part));
-  RP_TRY_LAUNCH_N("rmsnorm", rp::launch_rmsnorm(s, bf, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
+  RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, bf, M, d, hq, w.O, hq, bo, hq, w.X, d, rp::EPI_ADD_F32, sk(d, hq), gemm_part));
+  RP_TRY_LAUNCH_N(nm.norm2, rp::launch_rmsnorm(s, bf, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
-  RP_TRY_LAUNCH_N("gemm_gate_up", rp::launch_gemm(s, bf, M, 2 * F, d, w.N, d, bgu, d, w.GU, 2 * F, rp::EPI_STORE, sk(2 * F, d),
-                                gemm_part));
-  RP_TRY_LAUNCH_N("swiglu", rp::launch_swiglu(s, bf, w.GU, M, F, w.ACT));
+  if (fused_swiglu(c, splitk_ok)) {
+    RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, bf, M, F, d, w.N, d, bgu, d, w.ACT, F, rp::EPI_SWIGLU, 1, nullptr));
+  } else {
+    RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, bf, M, 2 * F, d, w.N, d, bgu, d, w.GU, 2 * F, rp::EPI_STORE,
+                                                sk(2 * F, d), gemm_part));
+    RP_TRY_LAUNCH_N(nm.swiglu, rp::launch_swiglu(s, bf, w.GU, M, F, w.ACT));
+  }
   rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
-  RP_TRY_LAUNCH_N("gemm_down", rp::launch_gemm(s, bf, M, d, F, w.ACT, F, bd, F, w.X, d, rp::EPI_ADD_F32, sk(d, F), gemm_part));
+  RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, bf, M, d, F, w.ACT, F, bd, F, w.X, d, rp::EPI_ADD_F32, sk(d, F), gemm_part));
   return RP_OK;
 }
 
@@ -397,16 +415,16 @@ rp_status rp_prefix_forward(const rp_model* m, void* stream, int32_t B, const in
   if (hidden_out) w.X = hidden_out;
   const rp::SeqTable tab = make_table(B, cu, nullptr);
 
-  RP_TRY_LAUNCH_N("visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
-  RP_TRY_LAUNCH_N("embed", rp::launch_embed(s, bf, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
+  RP_TRY_LAUNCH_N("prefix.visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
+  RP_TRY_LAUNCH_N("prefix.embed", rp::launch_embed(s, bf, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
                                  c.d_model, w.X));
   for (int l = 0; l < c.n_layers; ++l) {
     void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
     void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, 0, nullptr);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, 0, nullptr, kPrefixNames);
     if (st != RP_OK) return st;
   }
-  RP_TRY_LAUNCH_N("gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
+  RP_TRY_LAUNCH_N("prefix.gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
   return RP_OK;
 }
 
@@ -440,19 +458,19 @@ rp_status rp_suffix_logprob(const rp_model* m, void* stream, int32_t B, const in
   SuffixWS w;
   suffix_ws(m, R, ws, &w);
   const rp::SeqTable tab = make_table(B, scu, pcu);
-  RP_TRY_LAUNCH_N("embed", rp::launch_decode_embed(s, bf, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
+  RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, bf, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
   for (int l = 0; l < c.n_layers; ++l) {
     const void* kl = layer_ptr(m, kv.k, kv.layer_stride, l);
     const void* vl = layer_ptr(m, kv.v, kv.layer_stride, l);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, 0, nullptr);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, 0, nullptr, kSuffixNames);
     if (st != RP_OK) return st;
   }
-  RP_TRY_LAUNCH_N("final_norm", rp::launch_final_norm_rows(s, bf, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
+  RP_TRY_LAUNCH_N("suffix.final_norm", rp::launch_final_norm_rows(s, bf, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
                                            c.d_model, w.L.N));
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
-  RP_TRY_LAUNCH_N("gemm_lm_head", rp::launch_gemm(s, bf, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
+  RP_TRY_LAUNCH_N("suffix.gemm_lm_head", rp::launch_gemm(s, bf, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
                                 c.vocab, rp::EPI_STORE_F32, 1, nullptr));
-  RP_TRY_LAUNCH_N("logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
+  RP_TRY_LAUNCH_N("suffix.logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
   return RP_OK;
 }
 
@@ -483,36 +501,36 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
   const float scale = (float)(1.0 / sqrt((double)D));
-  RP_TRY_LAUNCH_N("decode_embed", rp::launch_decode_embed(s, bf, token_ids, m->embed, c.vocab, B, d, w.L.X));
+  RP_TRY_LAUNCH_N("decode.embed", rp::launch_decode_embed(s, bf, token_ids, m->embed, c.vocab, B, d, w.L.X));
   for (int l = 0; l < c.n_layers; ++l) {
     const rp_layer_weights& lw = m->layers[l];
     void* kl = layer_ptr(m, cache.k, cache.layer_stride, l);
     void* vl = layer_ptr(m, cache.v, cache.layer_stride, l);
-    RP_TRY_LAUNCH_N("decode_rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.attn_norm, c.rms_eps, B, d, w.L.N));
+    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.attn_norm, c.rms_eps, B, d, w.L.N));
     rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
-    RP_TRY_LAUNCH_N("decode_gemm_qkv", rp::launch_gemm(s, bf, B, qkv, d, w.L.N, d, bqkv, d, w.L.QKV, qkv, rp::EPI_STORE,
+    RP_TRY_LAUNCH_N("decode.gemm_qkv", rp::launch_gemm(s, bf, B, qkv, d, w.L.N, d, bqkv, d, w.L.QKV, qkv, rp::EPI_STORE,
                                   decode_splitk(c, B, qkv, d), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode_rope_kv", rp::launch_decode_rope_kv(s, bf, w.L.QKV, B, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, kv_len, cap,
+    RP_TRY_LAUNCH_N("decode.rope_kv", rp::launch_decode_rope_kv(s, bf, w.L.QKV, B, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, kv_len, cap,
                                             c.max_position, kl, vl));
-    RP_TRY_LAUNCH_N("decode_attention", rp::launch_decode_attention(s, bf, w.L.QKV, qkv, kl, vl, kv_len, cap, c.max_position, B, Hq, Hkv,
+    RP_TRY_LAUNCH_N("decode.attention", rp::launch_decode_attention(s, bf, w.L.QKV, qkv, kl, vl, kv_len, cap, c.max_position, B, Hq, Hkv,
                                               D, scale, w.attn_part, w.L.O));
     rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
-    RP_TRY_LAUNCH_N("decode_gemm_o_proj", rp::launch_gemm(s, bf, B, d, hq, w.L.O, hq, bo, hq, w.L.X, d, rp::EPI_ADD_F32,
+    RP_TRY_LAUNCH_N("decode.gemm_o_proj", rp::launch_gemm(s, bf, B, d, hq, w.L.O, hq, bo, hq, w.L.X, d, rp::EPI_ADD_F32,
                                   decode_splitk(c, B, d, hq), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode_rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.mlp_norm, c.rms_eps, B, d, w.L.N));
+    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.mlp_norm, c.rms_eps, B, d, w.L.N));
     rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
-    RP_TRY_LAUNCH_N("decode_gemm_gate_up", rp::launch_gemm(s, bf, B, 2 * F, d, w.L.N, d, bgu, d, w.L.GU, 2 * F, rp::EPI_STORE,
+    RP_TRY_LAUNCH_N("decode.gemm_gate_up", rp::launch_gemm(s, bf, B, 2 * F, d, w.L.N, d, bgu, d, w.L.GU, 2 * F, rp::EPI_STORE,
                                   decode_splitk(c, B, 2 * F, d), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode_swiglu", rp::launch_swiglu(s, bf, w.L.GU, B, F, w.L.ACT));
+    RP_TRY_LAUNCH_N("decode.swiglu", rp::launch_swiglu(s, bf, w.L.GU, B, F, w.L.ACT));
     rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
-    RP_TRY_LAUNCH_N("decode_gemm_down", rp::launch_gemm(s, bf, B, d, F, w.L.ACT, F, bd, F, w.L.X, d, rp::EPI_ADD_F32,
+    RP_TRY_LAUNCH_N("decode.gemm_down", rp::launch_gemm(s, bf, B, d, F, w.L.ACT, F, bd, F, w.L.X, d, rp::EPI_ADD_F32,
                                   decode_splitk(c, B, d, F), w.gemm_part));
   }
-  RP_TRY_LAUNCH_N("decode_final_norm", rp::launch_rmsnorm(s, bf, w.L.X, m->final_norm, c.rms_eps, B, d, w.L.N));
+  RP_TRY_LAUNCH_N("decode.final_norm", rp::launch_rmsnorm(s, bf, w.L.X, m->final_norm, c.rms_eps, B, d, w.L.N));
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
-  RP_TRY_LAUNCH_N("decode_gemm_lm_head", rp::launch_gemm(s, bf, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
+  RP_TRY_LAUNCH_N("decode.gemm_lm_head", rp::launch_gemm(s, bf, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
                                 decode_splitk(c, B, c.vocab, d), w.gemm_part));
-  RP_TRY_LAUNCH_N("argmax", rp::launch_argmax(s, lg, B, c.vocab, next_ids));
+  RP_TRY_LAUNCH_N("decode.argmax", rp::launch_argmax(s, lg, B, c.vocab, next_ids));
   return RP_OK;
 }
 

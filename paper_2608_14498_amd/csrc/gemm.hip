@@ -1,13 +1,22 @@
 // GEMMs of the backbone: C[M,N] (epi)= A[M,K] . B[N,K]^T with fp32 accumulation.
-// A is row-major activations, B is nn.Linear weights [out, in] given as up to three
-// row segments (fused q/k/v or gate/up projections without a concatenated copy).
+// A is row-major activations, B is nn.Linear weights [out, in] given as up to three row
+// segments (q/k/v or gate/up projections without a concatenated copy).
 //
-// bf16: 256x256x64 macro-tile, 4 waves (2x2), each wave owns 128x128 of C as 4x4
-// blocks of v_mfma_f32_32x32x16_bf16.  A/B tiles are staged through LDS, double
-// buffered (2 x 64 KiB), with a 16-byte-chunk XOR swizzle so that the 32 rows read
-// by one MFMA operand fetch hit distinct banks.  Tiles are visited in groups of 8
-// tile-rows and the block index is remapped so each XCD walks a contiguous range of
-// tiles (its L2 then holds the shared A rows / B columns).
+// bf16 (v_mfma_f32_32x32x16_bf16): a 256x256 C tile per workgroup, K in 64-deep slabs.
+//   * 4 waves (2x2, 128x128 each, one wave per SIMD) or 8 waves (4x2, 64x128 each, two
+//     waves per SIMD); accumulators live in the accumulation registers.
+//   * A/B slabs are staged through LDS, double buffered (2 x 64 KiB), each row of 8
+//     16-byte chunks XOR-swizzled so that any 8 (32-bank) or 16 (64-bank) consecutive
+//     rows read by one MFMA operand fetch hit distinct banks: no LDS bank conflicts.
+//   * In-tile pipeline: the LDS reads of k-step s+1 are issued before the MFMAs of step
+//     s.  A wave issues in order, so the next slab's global loads are interleaved with
+//     the MFMAs of k-steps 0-1 and its LDS stores with those of steps 2-3 (a burst of
+//     loads at the top of the tile would block the MFMAs behind it).
+//   * Tiles are visited in groups of 8 tile-rows and the block index is remapped so each
+//     XCD walks a contiguous range of tiles (its L2 holds the shared A/B slabs).
+//   * Epilogues: bf16 store, fp32 store, fp32 accumulate (residual), fused SwiGLU (each
+//     wave's 128 B rows are 64 gate + the matching 64 up rows, so gate and up of one
+//     output feature land in the same lane), and fp32 split-K partials.
 //
 // fp32: a plain 64x64 SIMT tile (exact fp32 FMAs) for the fp32 model.
 #include "device_common.h"
@@ -24,7 +33,7 @@ struct GemmArgs {
   void* C;
   int ldc;
   int tiles_m, tiles_n;
-  int k_chunk;       // K range per split (multiple of BK)
+  int k_chunk;       // K range per split (multiple of the k slab)
   float* partials;   // split-K: [splitk][M][N] fp32
 };
 
@@ -46,104 +55,179 @@ __device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int
   *tn = in / gsize;
 }
 
+// Physical 16-byte chunk of logical chunk c in LDS row r is c ^ swz(r).
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+constexpr int GB_M = 256, GB_N = 256, GB_K = 64;
+
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + expf(-g)) * u; }
+
 // ------------------------------------------------------------------------------------
 // bf16 MFMA GEMM
 // ------------------------------------------------------------------------------------
-constexpr int GB_M = 256, GB_N = 256, GB_K = 64, G_THREADS = 256;
-
-template <int EPI>
-__global__ __launch_bounds__(G_THREADS) void k_gemm_bf16(GemmArgs g) {
-  __shared__ uint4 As[2][GB_M * 8];  // [row][8 chunks of 8 bf16], swizzled
+template <int EPI, int WGM>
+__global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
+  constexpr int NT = WGM * 2 * 64;
+  constexpr int TM = GB_M / WGM, TN = GB_N / 2;
+  constexpr int MI = TM / 32, NJ = TN / 32;
+  constexpr int LOADS = (GB_M * 8) / NT;  // 16-byte chunks per matrix per thread: 8 or 4
+  constexpr int MM = MI * NJ;              // MFMAs per k-step
+  __shared__ uint4 As[2][GB_M * 8];
   __shared__ uint4 Bs[2][GB_N * 8];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
   tile_coords(xcd_remap(blockIdx.x, gridDim.x), g.tiles_m, g.tiles_n, &tm, &tn);
-  const int m0 = tm * GB_M, n0 = tn * GB_N;
+  const int m0 = tm * GB_M;
   const int kbeg = blockIdx.y * g.k_chunk;
   const int kend = min(g.K, kbeg + g.k_chunk);
   const int KT = (kend - kbeg) / GB_K;
 
-  // global->LDS mapping: thread loads chunk (tid & 7) of rows (tid >> 3) + 32 i
   const int lc = tid & 7, lr = tid >> 3;
   const bf16_t* Ab = (const bf16_t*)g.A + kbeg + lc * 8;
+  // logical B row staged in local B row r of this tile
+  auto b_logical = [&](int r) -> int {
+    if (EPI == EPI_SWIGLU) {  // per 128-row half: 64 gate rows then the matching 64 up rows
+      const int w = r >> 7, c = r & 127;
+      const int f = min(tn * 128 + w * 64 + (c & 63), g.N - 1);
+      return (c >= 64 ? g.B.n1 : 0) + f;
+    }
+    return min(tn * GB_N + r, g.N - 1);
+  };
   uint4 ra0, ra1, ra2, ra3, ra4, ra5, ra6, ra7, rb0, rb1, rb2, rb3, rb4, rb5, rb6, rb7;
-#define RP_LD1(i_, kt_)                                                                   \
-  ra##i_ = *reinterpret_cast<const uint4*>(                                               \
-      Ab + (int64_t)min(m0 + lr + 32 * i_, g.M - 1) * g.lda + (kt_) * GB_K);              \
-  rb##i_ = *reinterpret_cast<const uint4*>(                                               \
-      brow<bf16_t>(g.B, min(n0 + lr + 32 * i_, g.N - 1), g.ldb) + kbeg + lc * 8 + (kt_) * GB_K);
-#define RP_GLOAD(kt_)                                                                     \
-  RP_LD1(0, kt_) RP_LD1(1, kt_) RP_LD1(2, kt_) RP_LD1(3, kt_) RP_LD1(4, kt_) RP_LD1(5, kt_) \
-  RP_LD1(6, kt_) RP_LD1(7, kt_)
-#define RP_ST1(i_, buf_)                                                                  \
-  {                                                                                       \
-    const int r_ = lr + 32 * i_;                                                          \
-    As[(buf_)][r_ * 8 + (lc ^ (r_ & 7))] = ra##i_;                                        \
-    Bs[(buf_)][r_ * 8 + (lc ^ (r_ & 7))] = rb##i_;                                        \
+#define G_LDA(i_, kt_)                                                                                    \
+  if (i_ < LOADS) {                                                                                       \
+    const int r_ = lr + (NT / 8) * i_;                                                                    \
+    ra##i_ = *reinterpret_cast<const uint4*>(Ab + (int64_t)min(m0 + r_, g.M - 1) * g.lda + (kt_) * GB_K); \
   }
-#define RP_LSTORE(buf_)                                                                   \
-  RP_ST1(0, buf_) RP_ST1(1, buf_) RP_ST1(2, buf_) RP_ST1(3, buf_) RP_ST1(4, buf_)          \
-  RP_ST1(5, buf_) RP_ST1(6, buf_) RP_ST1(7, buf_)
+#define G_LDB(i_, kt_)                                                                                 \
+  if (i_ < LOADS) {                                                                                    \
+    const int r_ = lr + (NT / 8) * i_;                                                                 \
+    rb##i_ = *reinterpret_cast<const uint4*>(brow<bf16_t>(g.B, b_logical(r_), g.ldb) + kbeg + lc * 8 + \
+                                             (kt_) * GB_K);                                            \
+  }
+#define G_STA(i_, buf_)                                    \
+  if (i_ < LOADS) {                                        \
+    const int r_ = lr + (NT / 8) * i_;                     \
+    As[(buf_)][r_ * 8 + (lc ^ swz(r_))] = ra##i_;          \
+  }
+#define G_STB(i_, buf_)                                    \
+  if (i_ < LOADS) {                                        \
+    const int r_ = lr + (NT / 8) * i_;                     \
+    Bs[(buf_)][r_ * 8 + (lc ^ swz(r_))] = rb##i_;          \
+  }
+#define G_LOAD_A(kt_) G_LDA(0, kt_) G_LDA(1, kt_) G_LDA(2, kt_) G_LDA(3, kt_) G_LDA(4, kt_) G_LDA(5, kt_) G_LDA(6, kt_) G_LDA(7, kt_)
+#define G_LOAD_B(kt_) G_LDB(0, kt_) G_LDB(1, kt_) G_LDB(2, kt_) G_LDB(3, kt_) G_LDB(4, kt_) G_LDB(5, kt_) G_LDB(6, kt_) G_LDB(7, kt_)
+#define G_STORE_A(b_) G_STA(0, b_) G_STA(1, b_) G_STA(2, b_) G_STA(3, b_) G_STA(4, b_) G_STA(5, b_) G_STA(6, b_) G_STA(7, b_)
+#define G_STORE_B(b_) G_STB(0, b_) G_STB(1, b_) G_STB(2, b_) G_STB(3, b_) G_STB(4, b_) G_STB(5, b_) G_STB(6, b_) G_STB(7, b_)
+#define G_FRAGS(AF, BF, ks_)                                                   \
+  _Pragma("unroll") for (int i = 0; i < MI; ++i) {                             \
+    const int r_ = wm * TM + i * 32 + fr;                                      \
+    AF[i] = as_bf16x8(As[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]);        \
+  }                                                                            \
+  _Pragma("unroll") for (int j = 0; j < NJ; ++j) {                             \
+    const int r_ = wn * TN + j * 32 + fr;                                      \
+    BF[j] = as_bf16x8(Bs[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]);        \
+  }
+#define G_MMA(AF, BF)                                                           \
+  _Pragma("unroll") for (int i = 0; i < MI; ++i)                                \
+  _Pragma("unroll") for (int j = 0; j < NJ; ++j)                                \
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(AF[i], BF[j], acc[i][j], 0, 0, 0);
+// spread n_other_ instructions of class mask_ evenly over the MM MFMAs of this region
+#define G_INTERLEAVE(mask_, n_other_)                                           \
+  _Pragma("unroll") for (int q = 0; q < (n_other_); ++q) {                      \
+    __builtin_amdgcn_sched_group_barrier(0x008, MM / (n_other_), 0);            \
+    __builtin_amdgcn_sched_group_barrier((mask_), 1, 0);                        \
+  }
 
-  f32x16_t acc[4][4];
+  f32x16_t acc[MI][NJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   if (KT > 0) {
-    RP_GLOAD(0);
-    RP_LSTORE(0);
+    G_LOAD_A(0);
+    G_LOAD_B(0);
+    G_STORE_A(0);
+    G_STORE_B(0);
   }
   __syncthreads();
 
   const int fr = lane & 31, fk = lane >> 5;
   for (int kt = 0; kt < KT; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < KT) { RP_GLOAD(kt + 1); }
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int ch = ks * 2 + fk;
-      bf16x8_t af[4], bfr[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = wm * 128 + i * 32 + fr;
-        af[i] = as_bf16x8(As[buf][r * 8 + (ch ^ (r & 7))]);
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = wn * 128 + j * 32 + fr;
-        bfr[j] = as_bf16x8(Bs[buf][r * 8 + (ch ^ (r & 7))]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < KT) { RP_LSTORE(buf ^ 1); }
+    const int ktn = kt + 1 < KT ? kt + 1 : kt;  // the last tile re-loads itself into the idle buffer
+    bf16x8_t af0[MI], bf0[NJ], af1[MI], bf1[NJ];
+    G_FRAGS(af0, bf0, 0);
+    G_FRAGS(af1, bf1, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    G_MMA(af0, bf0);
+    G_LOAD_A(ktn);
+    G_INTERLEAVE(0x020, LOADS);
+    __builtin_amdgcn_sched_barrier(0);
+    G_FRAGS(af0, bf0, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    G_MMA(af1, bf1);
+    G_LOAD_B(ktn);
+    G_INTERLEAVE(0x020, LOADS);
+    __builtin_amdgcn_sched_barrier(0);
+    G_FRAGS(af1, bf1, 3);
+    __builtin_amdgcn_sched_barrier(0);
+    // buffer buf^1 was last read before the previous barrier, so it can be refilled now
+    G_MMA(af0, bf0);
+    G_STORE_A(buf ^ 1);
+    G_INTERLEAVE(0x200, LOADS);
+    __builtin_amdgcn_sched_barrier(0);
+    G_MMA(af1, bf1);
+    G_STORE_B(buf ^ 1);
+    G_INTERLEAVE(0x200, LOADS);
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
   }
+#undef G_LDA
+#undef G_LDB
+#undef G_STA
+#undef G_STB
+#undef G_LOAD_A
+#undef G_LOAD_B
+#undef G_STORE_A
+#undef G_STORE_B
+#undef G_FRAGS
+#undef G_MMA
+#undef G_INTERLEAVE
 
-#undef RP_LD1
-#undef RP_GLOAD
-#undef RP_ST1
-#undef RP_LSTORE
-
-  // epilogue: acc[i][j][e] -> row 8*(e/4) + 4*(lane/32) + e%4, col lane%32 of block (i, j)
+  // epilogue: acc[i][j][e] = C(row i*32 + 8(e/4) + 4 fk + e%4, col j*32 + fr) of the wave tile
+  if (EPI == EPI_SWIGLU) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MI; ++i) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = n0 + wn * 128 + j * 32 + fr;
+      for (int j = 0; j < 2; ++j) {
+        const int f = tn * 128 + wn * 64 + j * 32 + fr;
+        if (f >= g.N) continue;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + wm * TM + i * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
+          if (m >= g.M) continue;
+          ((bf16_t*)g.C)[(int64_t)m * g.ldc + f] = f2bf(silu_mul(acc[i][j][e], acc[i][j + 2][e]));
+        }
+      }
+    }
+    return;
+  }
+  const int n0 = tn * GB_N;
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int n = n0 + wn * TN + j * 32 + fr;
       if (n >= g.N) continue;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int m = m0 + wm * 128 + i * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
+        const int m = m0 + wm * TM + i * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
         if (m >= g.M) continue;
         const float v = acc[i][j][e];
         if (EPI == -1) {
@@ -247,10 +331,23 @@ size_t gemm_partial_floats(int32_t M, int32_t N, int32_t splitk) {
   return splitk > 1 ? (size_t)splitk * M * N : 0;
 }
 
+// Workgroup shape of a bf16 GEMM: 8 waves (two per SIMD), except for very wide outputs,
+// where one 128x128 tile per wave measured faster.
+static bool four_waves_for(int32_t N, Epi epi) { return epi == EPI_SWIGLU || N >= 16384; }
+
+template <int EPI>
+static void launch_bf16(hipStream_t s, const GemmArgs& g, dim3 grid, bool four_waves) {
+  if (four_waves)
+    k_gemm_bf16<EPI, 2><<<grid, 256, 0, s>>>(g);
+  else
+    k_gemm_bf16<EPI, 4><<<grid, 512, 0, s>>>(g);
+}
+
 hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
                        int32_t splitk, float* partials) {
   if (M <= 0 || N <= 0) return hipSuccess;
+  if (epi == EPI_SWIGLU && (!bf16 || splitk > 1)) return hipErrorInvalidValue;
   GemmArgs g;
   g.M = M;
   g.N = N;
@@ -271,16 +368,19 @@ hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K
   const bool split = splitk > 1;
   if (bf16) {
     g.tiles_m = (M + GB_M - 1) / GB_M;
-    g.tiles_n = (N + GB_N - 1) / GB_N;
+    g.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB_N - 1) / GB_N;
     dim3 grid(g.tiles_m * g.tiles_n, splitk);
+    const bool four = four_waves_for(N, epi);
     if (split)
-      k_gemm_bf16<-1><<<grid, G_THREADS, 0, s>>>(g);
+      launch_bf16<-1>(s, g, grid, four);
     else if (epi == EPI_STORE)
-      k_gemm_bf16<EPI_STORE><<<grid, G_THREADS, 0, s>>>(g);
+      launch_bf16<EPI_STORE>(s, g, grid, four);
     else if (epi == EPI_STORE_F32)
-      k_gemm_bf16<EPI_STORE_F32><<<grid, G_THREADS, 0, s>>>(g);
+      launch_bf16<EPI_STORE_F32>(s, g, grid, four);
+    else if (epi == EPI_SWIGLU)
+      launch_bf16<EPI_SWIGLU>(s, g, grid, four);
     else
-      k_gemm_bf16<EPI_ADD_F32><<<grid, G_THREADS, 0, s>>>(g);
+      launch_bf16<EPI_ADD_F32>(s, g, grid, four);
   } else {
     g.tiles_m = (M + GF_M - 1) / GF_M;
     g.tiles_n = (N + GF_N - 1) / GF_N;
@@ -302,6 +402,29 @@ hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K
     k_splitk_reduce<EPI_STORE_F32, float><<<blocks, 256, 0, s>>>(partials, splitk, M, N, C, ldc);
   else
     k_splitk_reduce<EPI_ADD_F32, float><<<blocks, 256, 0, s>>>(partials, splitk, M, N, C, ldc);
+  return hipGetLastError();
+}
+
+// Timing-harness hook: plain bf16 store epilogue with a forced workgroup shape
+// (variant 0: 4 waves, otherwise 8 waves).
+hipError_t launch_gemm_variant(hipStream_t s, int variant, int32_t M, int32_t N, int32_t K, const void* A,
+                               const void* B, void* C) {
+  GemmArgs g;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = A;
+  g.lda = K;
+  g.B = BSeg{B, B, B, N, N};
+  g.ldb = K;
+  g.C = C;
+  g.ldc = N;
+  g.partials = nullptr;
+  g.k_chunk = K;
+  g.tiles_m = (M + GB_M - 1) / GB_M;
+  g.tiles_n = (N + GB_N - 1) / GB_N;
+  dim3 grid(g.tiles_m * g.tiles_n, 1);
+  launch_bf16<EPI_STORE>(s, g, grid, variant == 0);
   return hipGetLastError();
 }
 

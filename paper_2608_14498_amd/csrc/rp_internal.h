@@ -37,6 +37,7 @@ enum Epi : int {
   EPI_STORE = 0,      // C[T] = acc
   EPI_STORE_F32 = 1,  // C[f32] = acc
   EPI_ADD_F32 = 2,    // C[f32] += acc  (residual stream)
+  EPI_SWIGLU = 3,     // C[T][m, f] = silu(gate) * up; B = {gate rows, up rows}, N = ffn features
 };
 
 // B operand of a GEMM given as up to three row segments of nn.Linear weights:
@@ -69,7 +70,9 @@ hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const in
                                     int32_t V, float* lp);
 hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t V, int32_t* out);
 
-// GEMM: C[M,N] (epi)= A[M,K] . B[N,K]^T, fp32 accumulation.
+// GEMM: C[M,N] (epi)= A[M,K] . B[N,K]^T, fp32 accumulation.  For EPI_SWIGLU, N is the
+// number of output features f and B = {b0 = gate [N,K], b1 = up [N,K]} (n1 = N); the fused
+// epilogue writes silu(A.gate_f) * (A.up_f).  splitk > 1 needs EPI != EPI_SWIGLU.
 hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
                        int32_t splitk, float* partials);
