@@ -52,20 +52,34 @@ __device__ __forceinline__ QBlock find_qblock(const SeqTable& st, int qbl, int B
 
 // ------------------------------------------------------------------------------------
 // bf16 MFMA flash attention
+//
+// K and V tiles are both staged row-major ([key][Dh], 16-byte chunks, per-operand XOR
+// swizzle).  S^T = K Q^T reads K fragments with ds_read_b128.  The V^T operand of
+// O^T += V^T P^T is read with ds_read_b64_tr_b16: within a 16-lane group, lane i receives
+// column i%4 of the 8-byte chunks addressed by lanes i/4, i/4+4, i/4+8, i/4+12, so lane
+// p addressing V[k0 + p/4][d0 + 4(p%4)] hands lane i the four keys k0..k0+3 of head
+// dimension d0+i -- the MFMA operand, with no transposed copy of V.
 // ------------------------------------------------------------------------------------
-constexpr int FA_KT = 64;        // keys per tile
 constexpr float kMaskVal = -1e30f;
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 
-template <int D, int QW>
-__global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
+template <int D>
+__device__ __forceinline__ int kswz(int key) { return D == 128 ? (key & 15) : (key & 7); }
+__device__ __forceinline__ int vswz(int key) { return (key & 3) << 1; }
+
+template <int D, int QW, int KT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QW == 1 ? 2 : 1, QW == 1 ? 2 : 1)))
+void k_attn_bf16(SeqTable st, AttnArgs a) {
   constexpr int BQ = 4 * 32 * QW;
-  constexpr int CH = D / 8;              // 16-byte chunks per K row
-  constexpr int VT_LD = FA_KT + 4;       // V^T row stride (bf16): 136 bytes
-  constexpr int KSTEPS = D / 16;         // MFMA k-steps of S^T
+  constexpr int CH = D / 8;              // 16-byte chunks per K/V row
+  constexpr int KSTEPS = D / 16;         // MFMA k-steps of S^T (over Dh)
   constexpr int DB = D / 32;             // 32-row blocks of O^T
-  constexpr int LOADS = (FA_KT * CH) / 256;
-  __shared__ uint4 Ks[2][FA_KT * CH];
-  __shared__ __align__(16) bf16_t Vt[2][D * VT_LD];
+  constexpr int KB = KT / 32;            // 32-key blocks per tile
+  constexpr int LOADS = (KT * CH) / 256;  // 16-byte chunks per thread per matrix
+  static_assert(LOADS == 1 || LOADS == 2 || LOADS == 4, "tile loader");
+  __shared__ uint4 Ks[2][KT * CH];
+  __shared__ uint4 Vs[2][KT * CH];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = blockIdx.x % a.Hq;
@@ -74,18 +88,16 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
   const int b = qb.b;
   const int G = a.Hq / a.Hkv, g = h / G;
   const int n0 = st.pos0(b);
-  const int nq_seq = st.q_cu[b + 1] - st.q_cu[b];
   const int qpos_first = n0 + (qb.q_begin - st.q_cu[b]);
   const int qpos_last = n0 + (qb.q_end - 1 - st.q_cu[b]);
-  const int nk = qpos_last + 1;                       // keys needed by this block
-  const int ntiles = (nk + FA_KT - 1) / FA_KT;
+  const int nk = qpos_last + 1;  // keys needed by this block
+  const int ntiles = (nk + KT - 1) / KT;
   const int64_t kv_ld = (int64_t)a.Hkv * D;
   const bf16_t* k0 = (const bf16_t*)a.k0 + (int64_t)g * D;
   const bf16_t* v0 = (const bf16_t*)a.v0 + (int64_t)g * D;
   const bf16_t* k1 = (const bf16_t*)a.k1 + (int64_t)g * D;
   const bf16_t* v1 = (const bf16_t*)a.v1 + (int64_t)g * D;
   const int krow0 = st.k_cu[b], qrow0 = st.q_cu[b];
-  (void)nq_seq;
 
   // ---- queries of this lane: column (lane & 31) of each 32-query block ----
   const int fr = lane & 31, fk = lane >> 5;
@@ -98,38 +110,27 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
     qpos[qi] = n0 + (qrow_raw - qrow0);
     const bf16_t* qp = (const bf16_t*)a.q + (int64_t)qrow * a.q_ld + h * D + fk * 8;
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-      qf[qi][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + ks * 16));
-    }
+    for (int ks = 0; ks < KSTEPS; ++ks) qf[qi][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + ks * 16));
   }
 
-  // ---- tile loader: thread handles chunks (key = id / CH, c = id % CH) ----
-  static_assert(LOADS == 2 || LOADS == 4, "tile loader covers D = 64 or 128");
+  // ---- tile loader: chunk id = i*256 + tid -> (key = id / CH, c = id % CH) ----
   uint4 rk0, rk1, rk2, rk3, rv0, rv1, rv2, rv3;
-#define RP_FA_LD1(i_, t_)                                                                  \
-  if (i_ < LOADS) {                                                                        \
-    const int id = i_ * 256 + tid, key = id / CH, c = id % CH;                             \
-    const int kv = min((t_) * FA_KT + key, nk - 1);                                        \
-    const int64_t roff = kv < n0 ? (int64_t)(krow0 + kv) * kv_ld : (int64_t)(qrow0 + kv - n0) * kv_ld; \
-    rk##i_ = *reinterpret_cast<const uint4*>((kv < n0 ? k0 : k1) + roff + c * 8);          \
-    rv##i_ = *reinterpret_cast<const uint4*>((kv < n0 ? v0 : v1) + roff + c * 8);          \
+#define FA_LD1(i_, t_)                                                                                   \
+  if (i_ < LOADS) {                                                                                      \
+    const int id = i_ * 256 + tid, key = id / CH, c = id % CH;                                           \
+    const int kv = min((t_) * KT + key, nk - 1);                                                         \
+    const int64_t roff = kv < n0 ? (int64_t)(krow0 + kv) * kv_ld : (int64_t)(qrow0 + kv - n0) * kv_ld;   \
+    rk##i_ = *reinterpret_cast<const uint4*>((kv < n0 ? k0 : k1) + roff + c * 8);                        \
+    rv##i_ = *reinterpret_cast<const uint4*>((kv < n0 ? v0 : v1) + roff + c * 8);                        \
   }
-#define RP_FA_GLOAD(t_) RP_FA_LD1(0, t_) RP_FA_LD1(1, t_) RP_FA_LD1(2, t_) RP_FA_LD1(3, t_)
-#define RP_FA_ST1(i_, buf_)                                                                \
-  if (i_ < LOADS) {                                                                        \
-    const int id = i_ * 256 + tid, key = id / CH, c = id % CH;                             \
-    Ks[(buf_)][key * CH + (c ^ (key & 7))] = rk##i_;                                       \
-    bf16_t* vt_ = &Vt[(buf_)][(c * 8) * VT_LD + (key ^ ((c << 2) & (FA_KT - 1)))];         \
-    vt_[0 * VT_LD] = (bf16_t)(rv##i_.x & 0xffffu);                                         \
-    vt_[1 * VT_LD] = (bf16_t)(rv##i_.x >> 16);                                             \
-    vt_[2 * VT_LD] = (bf16_t)(rv##i_.y & 0xffffu);                                         \
-    vt_[3 * VT_LD] = (bf16_t)(rv##i_.y >> 16);                                             \
-    vt_[4 * VT_LD] = (bf16_t)(rv##i_.z & 0xffffu);                                         \
-    vt_[5 * VT_LD] = (bf16_t)(rv##i_.z >> 16);                                             \
-    vt_[6 * VT_LD] = (bf16_t)(rv##i_.w & 0xffffu);                                         \
-    vt_[7 * VT_LD] = (bf16_t)(rv##i_.w >> 16);                                             \
+#define FA_GLOAD(t_) FA_LD1(0, t_) FA_LD1(1, t_) FA_LD1(2, t_) FA_LD1(3, t_)
+#define FA_ST1(i_, buf_)                                                  \
+  if (i_ < LOADS) {                                                       \
+    const int id = i_ * 256 + tid, key = id / CH, c = id % CH;            \
+    Ks[(buf_)][key * CH + (c ^ kswz<D>(key))] = rk##i_;                   \
+    Vs[(buf_)][key * CH + (c ^ vswz(key))] = rv##i_;                      \
   }
-#define RP_FA_LSTORE(buf_) RP_FA_ST1(0, buf_) RP_FA_ST1(1, buf_) RP_FA_ST1(2, buf_) RP_FA_ST1(3, buf_)
+#define FA_LSTORE(buf_) FA_ST1(0, buf_) FA_ST1(1, buf_) FA_ST1(2, buf_) FA_ST1(3, buf_)
 
   f32x16_t o[QW][DB];
   float m_run[QW], l_run[QW];
@@ -143,29 +144,33 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
       for (int e = 0; e < 16; ++e) o[qi][db][e] = 0.f;
   }
   const float c2 = a.scale * 1.4426950408889634f;  // scores in log2 units
+  // V^T fragment addressing (see header): 16-lane group -> d0, lane p = lane % 16
+  const int tr_p = lane & 15;
+  const int tr_key = fk * 4 + (tr_p >> 2);                 // + kb*32 + hh*16 (+8 for the second read)
+  const int tr_col = ((lane & 16) ? 16 : 0) + 4 * (tr_p & 3);  // + db*32
 
-  RP_FA_GLOAD(0);
-  RP_FA_LSTORE(0);
+  FA_GLOAD(0);
+  FA_LSTORE(0);
   __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntiles) { RP_FA_GLOAD(t + 1); }
+    if (t + 1 < ntiles) { FA_GLOAD(t + 1); }
 
-    // ---- S^T = K Q^T: s[qi][kb][e] = score(key t*64 + kb*32 + 8(e/4) + 4 fk + e%4, query fr) ----
-    f32x16_t s[QW][2];
+    // ---- S^T = K Q^T: s[qi][kb][e] = score(key t*KT + kb*32 + 8(e/4) + 4 fk + e%4, query fr) ----
+    f32x16_t s[QW][KB];
 #pragma unroll
     for (int qi = 0; qi < QW; ++qi)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) s[qi][kb][e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < KB; ++kb) {
         const int key = kb * 32 + fr;
-        const bf16x8_t kf = as_bf16x8(Ks[buf][key * CH + ((ks * 2 + fk) ^ (key & 7))]);
+        const bf16x8_t kf = as_bf16x8(Ks[buf][key * CH + ((ks * 2 + fk) ^ kswz<D>(key))]);
 #pragma unroll
         for (int qi = 0; qi < QW; ++qi)
           s[qi][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qi][ks], s[qi][kb], 0, 0, 0);
@@ -173,15 +178,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
     }
 
     // ---- mask, online softmax (per lane = per query) ----
-    const bool need_mask = (t * FA_KT + FA_KT - 1) > qpos_first;
+    const bool need_mask = (t * KT + KT - 1) > qpos_first;
 #pragma unroll
     for (int qi = 0; qi < QW; ++qi) {
       float mx = kMaskVal;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int key = t * FA_KT + kb * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
+          const int key = t * KT + kb * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
           float v = s[qi][kb][e] * c2;
           if (need_mask && key > qpos[qi]) v = kMaskVal;
           s[qi][kb][e] = v;
@@ -193,7 +198,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
       m_run[qi] = m_new;
       float ls = 0.f;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const float p = exp2f(s[qi][kb][e] - m_new);
@@ -207,9 +212,10 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
         for (int e = 0; e < 16; ++e) o[qi][db][e] *= alpha;
     }
 
-    // ---- O^T += V^T P^T over the 4 sixteen-key steps (kb, hh) ----
+    // ---- O^T += V^T P^T over the sixteen-key steps (kb, hh) ----
+    const bf16_t* vbase = reinterpret_cast<const bf16_t*>(&Vs[buf][0]);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         bf16x8_t pf[QW];
@@ -221,15 +227,16 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
                                         pack_bf2(sv[hh * 8 + 4], sv[hh * 8 + 5]),
                                         pack_bf2(sv[hh * 8 + 6], sv[hh * 8 + 7])));
         }
-        const int key_lo = kb * 32 + hh * 16 + 4 * fk;  // keys key_lo..+3 and key_lo+8..+11
+        const int ka = kb * 32 + hh * 16 + tr_key, kc = ka + 8;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const int dh = db * 32 + fr;
-          const int sw = ((dh >> 3) << 2) & (FA_KT - 1);
-          const bf16_t* row = &Vt[buf][dh * VT_LD];
-          uint2 lo = *reinterpret_cast<const uint2*>(row + (key_lo ^ sw));
-          uint2 hi = *reinterpret_cast<const uint2*>(row + ((key_lo + 8) ^ sw));
-          const bf16x8_t vf = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+          const int col = db * 32 + tr_col;
+          const int ca = ((col >> 3) ^ vswz(ka)) * 8 + (col & 7);
+          const int cc = ((col >> 3) ^ vswz(kc)) * 8 + (col & 7);
+          const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + ka * D + ca));
+          const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + kc * D + cc));
+          const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+          const bf16x8_t vf = as_bf16x8(make_uint4(l2.x, l2.y, h2.x, h2.y));
 #pragma unroll
           for (int qi = 0; qi < QW; ++qi)
             o[qi][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qi], o[qi][db], 0, 0, 0);
@@ -237,13 +244,13 @@ __global__ __launch_bounds__(256) void k_attn_bf16(SeqTable st, AttnArgs a) {
       }
     }
 
-    if (t + 1 < ntiles) { RP_FA_LSTORE(buf ^ 1); }
+    if (t + 1 < ntiles) { FA_LSTORE(buf ^ 1); }
     __syncthreads();
   }
-#undef RP_FA_LD1
-#undef RP_FA_GLOAD
-#undef RP_FA_ST1
-#undef RP_FA_LSTORE
+#undef FA_LD1
+#undef FA_GLOAD
+#undef FA_ST1
+#undef FA_LSTORE
 
   // ---- normalise and store: o[qi][db][e] = O^T(dh = db*32 + 8(e/4) + 4 fk + e%4, query fr) ----
 #pragma unroll
@@ -327,25 +334,29 @@ __global__ __launch_bounds__(64) void k_attn_f32(SeqTable st, AttnArgs a) {
   }
 }
 
-static int count_qblocks(const SeqTable& st, int BQ) {
+int count_qblocks(const SeqTable& st, int BQ) {
   int n = 0;
   for (int b = 0; b < st.n; ++b) n += (st.q_cu[b + 1] - st.q_cu[b] + BQ - 1) / BQ;
   return n;
 }
 
+// Timing-harness hook: forced tile shape (0: 32 queries/wave x 64-key tiles,
+// 1: 64 queries/wave x 32-key tiles).
+hipError_t launch_attention_variant(hipStream_t s, int variant, const SeqTable& st, const AttnArgs& a) {
+  if (variant == 0)
+    k_attn_bf16<128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+  else
+    k_attn_bf16<128, 2, 32><<<count_qblocks(st, 256) * a.Hq, 256, 0, s>>>(st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(hipStream_t s, bool bf16, const SeqTable& st, const AttnArgs& a, int32_t total_q) {
   if (total_q <= 0) return hipSuccess;
   if (bf16) {
-    // D = 128 keeps one 32-query block per wave (two would spill the accumulators).
-    if (a.D == 128) {
-      k_attn_bf16<128, 1><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
-    } else {
-      const int nqb2 = count_qblocks(st, 256);
-      if ((int64_t)nqb2 * a.Hq >= 512)
-        k_attn_bf16<64, 2><<<nqb2 * a.Hq, 256, 0, s>>>(st, a);
-      else
-        k_attn_bf16<64, 1><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
-    }
+    if (a.D == 128)
+      k_attn_bf16<128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+    else
+      k_attn_bf16<64, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
   } else {
     const int nqb = count_qblocks(st, 64);
     if (a.D == 128)
