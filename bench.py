@@ -54,6 +54,156 @@ def cpu_baseline(w, hw, bt, prefix_len: int):
                       f"suffix {t2 - t1:.1f} s"}
 
 
+def colocation(args, w):
+    """Prefix pass on one stream beside repeated decode steps on another (one GPU).
+
+    Arms: each alone on all CUs; co-run on two unmasked streams (the analog of the
+    paper's MPS-Default, Section "Resource Sharing Policy"); co-run with disjoint CU
+    masks giving decode k CUs (the analog of its static SM partitions).  Reports the
+    decode slowdown delta_D and the critical-path saving S of Eq. (1).
+    """
+    import torch
+
+    from paper_2608_14498_amd import binding as rb
+    from paper_2608_14498_amd import inputs, perf
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+
+    m = w.model
+    spec = w.decode
+    log(f"workload {w.name}: generating seeded inputs")
+    hw = inputs.make_weights(w)
+    bt = inputs.make_batch(w)
+    Bd, cap, kvl = spec["batch"], spec["cap"], spec["kv_len"]
+    maxp = max(max(bt.prefix_lens), cap) + 1
+    dm = DeviceModel(hw, maxp)
+    dev = dm.device
+    ids = to_device(bt.token_ids, dev)
+    vis = to_device(bt.visual, dev)
+    cu_p = [int(x) for x in bt.cu_prefix]
+    B, T = bt.batch, bt.T
+    K, V = dm.alloc_kv(T)
+    h_last = torch.empty((B, m.d_model), dtype=torch.float32, device=dev)
+    ws_p = dm.workspace(rb.rp_prefix_workspace_bytes(dm.handle, B, cu_p))
+    # decode state: the KV cache (N(0,1), drawn on the device with a seeded generator),
+    # constant context: every step writes slot kv_len and attends to kv_len + 1 keys
+    gen = torch.Generator(device=dev).manual_seed(w.index * 1000 + 20)
+    shape = (m.n_layers, Bd, cap, m.n_kv_heads, m.head_dim)
+    ck = torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    cv = torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    kv_len = torch.full((Bd,), kvl, dtype=torch.int32, device=dev)
+    tok = torch.randint(0, m.vocab, (Bd,), generator=gen, device=dev, dtype=torch.int32)
+    nxt = torch.empty(Bd, dtype=torch.int32, device=dev)
+    ws_d = dm.workspace(rb.rp_decode_workspace_bytes(dm.handle, Bd, cap))
+    kv_d = rb.make_kv(ck, cv, ck[0].numel())
+
+    def prefix_on(stream):
+        dm.prefix(cu_p, ids, vis, kv=(K, V), h_last=h_last, workspace=ws_p, stream=stream)
+
+    def decode_on(stream, n):
+        for _ in range(n):
+            rb.rp_decode_step(dm.handle, stream.cuda_stream, Bd, kv_d, cap, kv_len, tok, None, nxt, ws_d,
+                              ws_d.numel())
+
+    def timed(fn, stream):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    main = torch.cuda.current_stream()
+    for _ in range(2):
+        prefix_on(main)
+        decode_on(main, 3)
+    torch.cuda.synchronize()
+    T_P = min(timed(lambda: prefix_on(main), main) for _ in range(3))
+    step_ms = min(timed(lambda: decode_on(main, 10), main) for _ in range(3)) / 10
+    n_steps = max(1, int(round(T_P / step_ms)))
+    log(f"prefix alone {T_P:.2f} ms, decode step alone {step_ms:.3f} ms -> {n_steps} steps per window")
+    rb.rp_profile_reset()
+    rb.rp_profile_enable(True, 4096)
+    for _ in range(3):
+        decode_on(main, 1)
+        torch.cuda.synchronize()
+        rb.rp_profile_collect()
+    decode_kernels = {k: {"launches": n, "avg_ms": ms / max(n, 1), "ms_per_step": ms / 3}
+                      for k, (n, ms) in sorted(rb.rp_profile_read_all().items(), key=lambda kv: -kv[1][1])}
+    rb.rp_profile_enable(False)
+    for k, v in decode_kernels.items():
+        log(f"  decode kernel {k:24s} {v['ms_per_step']:.3f} ms/step")
+
+    ncu = rb.rp_device_cu_count(0)
+    words = (ncu + 31) // 32
+
+    def mask(lo, hi):
+        wv = [0] * words
+        for i in range(lo, hi):
+            wv[i // 32] |= 1 << (i % 32)
+        return wv
+
+    def corun(sa, sd, steps):
+        """Returns (prefix ms, decode ms, makespan ms) with both enqueued together."""
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        torch.cuda.synchronize()
+        ev[0].record(sa)
+        ev[2].record(sd)
+        prefix_on(sa)
+        decode_on(sd, steps)
+        ev[1].record(sa)
+        ev[3].record(sd)
+        torch.cuda.synchronize()
+        t_p, t_d = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+        start_gap = ev[0].elapsed_time(ev[2])
+        makespan = max(t_p, start_gap + t_d) - min(0.0, start_gap)
+        return t_p, t_d, makespan
+
+    arms = []
+    for regime, steps in (("balanced", n_steps), ("prefix-bounded", max(1, n_steps // 2)),
+                          ("decode-bounded", 2 * n_steps)):
+        T_D = step_ms * steps
+        streams = [("unmasked (MPS-Default analog)", torch.cuda.Stream(), torch.cuda.Stream(), None)]
+        if regime == "balanced":
+            for k in (32, 64, 96, 128):
+                sd = rb.rp_stream_create_cu_masked(0, mask(0, k))
+                sa = rb.rp_stream_create_cu_masked(0, mask(k, ncu))
+                streams.append((f"decode {k} CUs / prefix {ncu - k} CUs", torch.cuda.ExternalStream(sa),
+                                torch.cuda.ExternalStream(sd), (sa, sd)))
+        for name, sa, sd, raw in streams:
+            corun(sa, sd, steps)  # warm
+            t_p, t_d, mk = min((corun(sa, sd, steps) for _ in range(3)), key=lambda r: r[2])
+            model = perf.overlap_model(T_D, T_P, t_d - T_D)
+            arms.append({"regime": regime, "arm": name, "decode_steps": steps, "T_P_alone_ms": T_P,
+                         "T_D_alone_ms": T_D, "prefix_corun_ms": t_p, "decode_corun_ms": t_d,
+                         "makespan_ms": mk, "delta_D_ms": t_d - T_D, "serial_ms": T_P + T_D,
+                         "saving_measured_ms": T_P + T_D - mk, "saving_eq1_ms": model["saving"],
+                         "eq1_regime": model["regime"],
+                         "prefix_tokens_per_s": T / (t_p * 1e-3),
+                         "decode_tokens_per_s": Bd * steps / (t_d * 1e-3)})
+            log(f"{regime:15s} {name:36s} prefix {t_p:7.2f} ms decode {t_d:7.2f} ms makespan {mk:7.2f} "
+                f"(serial {T_P + T_D:7.2f})")
+            if raw:
+                rb.rp_stream_destroy(raw[0])
+                rb.rp_stream_destroy(raw[1])
+    best = min((a for a in arms if a["regime"] == "balanced"), key=lambda a: a["makespan_ms"])
+    out = {
+        "metric": "co-location: prefix tokens/s and decode tokens/s co-running vs alone; Eq. (1) saving",
+        "value": T / (best["makespan_ms"] * 1e-3),
+        "unit": "prefix tokens/s over the co-run makespan",
+        "n_gpus": 1, "steps": n_steps, "warmup": 2, "ms_per_step": best["makespan_ms"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": m.dtype,
+        "data": "synthetic (seeded)",
+        "config": {"workload": w.name, "prefix_batch": B, "prefix_len": bt.prefix_lens[0],
+                   "decode_batch": Bd, "decode_kv": kvl, "cus": ncu},
+        "prefix_alone_ms": T_P, "prefix_alone_tokens_per_s": T / (T_P * 1e-3),
+        "decode_step_alone_ms": step_ms, "decode_alone_tokens_per_s": Bd / (step_ms * 1e-3),
+        "decode_kernels": decode_kernels, "best_balanced_arm": best["arm"], "arms": arms,
+    }
+    dm.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -78,6 +228,8 @@ def main():
     from paper_2608_14498_amd.runtime import DeviceModel, to_device
 
     w = configs.get(args.workload)
+    if w.decode is not None:
+        return colocation(args, w)
     m = w.model
     log(f"workload {w.name}: generating seeded inputs")
     t0 = time.time()

@@ -63,7 +63,8 @@ typedef enum {
 typedef enum { RP_F32 = 0, RP_BF16 = 1 } rp_dtype;
 
 /* Backbone hyper-parameters.  head_dim must be 64 or 128; n_q_heads a
- * multiple of n_kv_heads (q head h reads kv head h / (n_q_heads/n_kv_heads)).
+ * multiple of n_kv_heads, at most 8 q heads per kv head (q head h reads kv head
+ * h / (n_q_heads/n_kv_heads)).
  * For bf16, d_model, ffn_dim and n_q_heads*head_dim must be multiples of 64.
  * rms_eps is the RMSNorm epsilon (1e-6 for the Qwen2 family); rope_theta the
  * RoPE base (1e6).  max_position bounds every position a call may use. */

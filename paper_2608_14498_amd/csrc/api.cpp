@@ -129,8 +129,8 @@ rp_status check_config(const rp_config* c) {
     return fail(RP_ERR_SHAPE, "config sizes must be positive");
   if (c->n_q_heads % c->n_kv_heads != 0)
     return fail(RP_ERR_SHAPE, "n_q_heads %d not a multiple of n_kv_heads %d", c->n_q_heads, c->n_kv_heads);
-  if (c->n_q_heads / c->n_kv_heads > 16)
-    return fail(RP_ERR_UNSUPPORTED, "query group size %d > 16", c->n_q_heads / c->n_kv_heads);
+  if (c->n_q_heads / c->n_kv_heads > 8)
+    return fail(RP_ERR_UNSUPPORTED, "query group size %d > 8", c->n_q_heads / c->n_kv_heads);
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(RP_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
   if (c->d_model % 8 || c->ffn_dim % 8) return fail(RP_ERR_UNSUPPORTED, "d_model and ffn_dim must be multiples of 8");

@@ -371,7 +371,7 @@ hipError_t launch_attention(hipStream_t s, bool bf16, const SeqTable& st, const 
 // Decode attention: split-KV partials + merge.
 // ------------------------------------------------------------------------------------
 constexpr int DC_KEYS = 256;  // keys per chunk
-constexpr int DC_MAXG = 16;
+constexpr int DC_MAXG = 8;   // q heads per kv head (validated on the host)
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_decode_attn_part(const T* __restrict__ q, int q_ld,
@@ -379,11 +379,12 @@ __global__ __launch_bounds__(256) void k_decode_attn_part(const T* __restrict__ 
                                                           const int32_t* __restrict__ kv_len, int cap,
                                                           int max_pos, int Hq, int Hkv, float scale,
                                                           int nchunks, float* __restrict__ part) {
-  constexpr int NPARTS = 256 / D;  // threads per output column
+  constexpr int LPK = D / 8;        // lanes per key row (8 head dims each, 16-byte loads)
+  constexpr int KPW = kWave / LPK;  // keys per wave pass
   __shared__ float qs[DC_MAXG][D];
   __shared__ float ps[DC_MAXG][DC_KEYS];
   __shared__ float red[DC_MAXG][4];
-  __shared__ float osum[NPARTS][DC_MAXG][D];
+  __shared__ float osum[4][DC_MAXG][D];
   const int c = blockIdx.x % nchunks;
   const int bg = blockIdx.x / nchunks;
   const int g = bg % Hkv, b = bg / Hkv;
@@ -407,66 +408,116 @@ __global__ __launch_bounds__(256) void k_decode_attn_part(const T* __restrict__ 
   const int64_t row_ld = (int64_t)Hkv * D;
   const T* kbase = ck + ((int64_t)b * cap) * row_ld + g * D;
   const T* vbase = cv + ((int64_t)b * cap) * row_ld + g * D;
-  // scores: one thread per key
-  if (tid < nkeys) {
-    const T* kr = kbase + (int64_t)(k_begin + tid) * row_ld;
-    float acc[DC_MAXG];
-#pragma unroll
-    for (int hg = 0; hg < DC_MAXG; ++hg) acc[hg] = 0.f;
-    for (int i = 0; i < D; i += 8) {
-      float kv8[8];
-      load8(kr + i, kv8);
-#pragma unroll
-      for (int hg = 0; hg < DC_MAXG; ++hg)
-        if (hg < G) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[hg] = fmaf(qs[hg][i + e], kv8[e], acc[hg]);
-        }
-    }
+  const int sub = lane % LPK, kk = lane / LPK;
+
+  // ---- scores: LPK lanes per key row, partial dots reduced across them.  All of this
+  // lane's K loads for the chunk are issued before any is consumed (memory-level
+  // parallelism: a decode step is bound by HBM bandwidth) ----
+  constexpr int NP = DC_KEYS / (4 * KPW);  // passes over the chunk
+  {
+    float qreg[DC_MAXG][8];
 #pragma unroll
     for (int hg = 0; hg < DC_MAXG; ++hg)
-      if (hg < G) ps[hg][tid] = acc[hg] * scale;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qreg[hg][e] = hg < G ? qs[hg][sub * 8 + e] : 0.f;
+    typename Raw8<T>::type kr[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int key = w * KPW + kk + p * 4 * KPW;
+      kr[p] = key < nkeys ? ld_raw8(kbase + (int64_t)(k_begin + key) * row_ld + sub * 8)
+                          : typename Raw8<T>::type{};
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int key = w * KPW + kk + p * 4 * KPW;
+      float kv8[8];
+      unpack8(kr[p], kv8);
+#pragma unroll
+      for (int hg = 0; hg < DC_MAXG; ++hg) {
+        if (hg < G) {
+          float a = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) a = fmaf(qreg[hg][e], kv8[e], a);
+          a = LPK == 16 ? row16_sum(a) : oct8_sum(a);
+          if (sub == 0 && key < nkeys) ps[hg][key] = a * scale;
+        }
+      }
+    }
+  }
+  // V loads for the chunk go out now, to land while the softmax runs
+  typename Raw8<T>::type vr[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int key = w * KPW + kk + p * 4 * KPW;
+    vr[p] = key < nkeys ? ld_raw8(vbase + (int64_t)(k_begin + key) * row_ld + sub * 8)
+                        : typename Raw8<T>::type{};
   }
   __syncthreads();
+  // ---- per-head max, exp, sum over the chunk (thread = key) ----
   for (int hg = 0; hg < G; ++hg) {
     const float mx = wave_max(tid < nkeys ? ps[hg][tid] : -INFINITY);
     if (lane == 0) red[hg][w] = mx;
   }
   __syncthreads();
-  for (int hg = 0; hg < G; ++hg) {
-    const float mx = fmaxf(fmaxf(red[hg][0], red[hg][1]), fmaxf(red[hg][2], red[hg][3]));
-    if (tid < nkeys) ps[hg][tid] = expf(ps[hg][tid] - mx);
-  }
-  __syncthreads();
-  // o[hg][d]: thread (d = tid % D, part = tid / D) sums keys k = part, part + NPARTS, ...
-  const int d = tid % D, pi = tid / D;
-  float acc[DC_MAXG];
-#pragma unroll
-  for (int hg = 0; hg < DC_MAXG; ++hg) acc[hg] = 0.f;
-  for (int k = pi; k < nkeys; k += NPARTS) {
-    const float vv = ldf(vbase + (int64_t)(k_begin + k) * row_ld + d);
-#pragma unroll
-    for (int hg = 0; hg < DC_MAXG; ++hg)
-      if (hg < G) acc[hg] = fmaf(ps[hg][k], vv, acc[hg]);
-  }
+  float mxs[DC_MAXG];
 #pragma unroll
   for (int hg = 0; hg < DC_MAXG; ++hg)
-    if (hg < G) osum[pi][hg][d] = acc[hg];
+    mxs[hg] = hg < G ? fmaxf(fmaxf(red[hg][0], red[hg][1]), fmaxf(red[hg][2], red[hg][3])) : 0.f;
+  __syncthreads();  // everyone has read red[] before it is reused for the sums
+  for (int hg = 0; hg < G; ++hg) {
+    float p = 0.f;
+    if (tid < nkeys) {
+      p = expf(ps[hg][tid] - mxs[hg]);
+      ps[hg][tid] = p;
+    }
+    p = wave_sum(p);
+    if (lane == 0) red[hg][w] = p;
+  }
+  __syncthreads();
+  // ---- o[hg][d] = sum_k p[hg][k] v[k][d]: LPK lanes per V row, KPW key groups per wave ----
+  {
+    float acc[DC_MAXG][8];
+#pragma unroll
+    for (int hg = 0; hg < DC_MAXG; ++hg)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[hg][e] = 0.f;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int k = w * KPW + kk + p * 4 * KPW;
+      float v8[8];
+      unpack8(vr[p], v8);
+      const int kc = min(k, DC_KEYS - 1);  // rows beyond nkeys hold zeros
+#pragma unroll
+      for (int hg = 0; hg < DC_MAXG; ++hg) {
+        if (hg < G) {
+          const float pk = k < nkeys ? ps[hg][kc] : 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[hg][e] = fmaf(pk, v8[e], acc[hg][e]);
+        }
+      }
+    }
+    // reduce the KPW key groups of the wave (lanes with equal sub), then the 4 waves
+#pragma unroll
+    for (int hg = 0; hg < DC_MAXG; ++hg) {
+      if (hg < G) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float a = acc[hg][e];
+#pragma unroll
+          for (int o = LPK; o < kWave; o <<= 1) a += __shfl_xor(a, o, kWave);
+          if (kk == 0) osum[w][hg][sub * 8 + e] = a;
+        }
+      }
+    }
+  }
   __syncthreads();
   for (int hg = 0; hg < G; ++hg) {
     float* o = out + hg * head_stride;
     if (tid == 0) {
-      o[0] = fmaxf(fmaxf(red[hg][0], red[hg][1]), fmaxf(red[hg][2], red[hg][3]));
-      float l = 0.f;
-      for (int k = 0; k < nkeys; ++k) l += ps[hg][k];
-      o[1] = l;
+      o[0] = mxs[hg];
+      o[1] = red[hg][0] + red[hg][1] + red[hg][2] + red[hg][3];
     }
-    if (tid < D) {
-      float sum = 0.f;
-#pragma unroll
-      for (int p2 = 0; p2 < NPARTS; ++p2) sum += osum[p2][hg][tid];
-      o[2 + tid] = sum;
-    }
+    if (tid < D) o[2 + tid] = osum[0][hg][tid] + osum[1][hg][tid] + osum[2][hg][tid] + osum[3][hg][tid];
   }
 }
 

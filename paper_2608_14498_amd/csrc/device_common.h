@@ -51,6 +51,23 @@ __device__ __forceinline__ T wave_max(T v) {
   return v;
 }
 
+// Sum over the 16 lanes of a DPP row (lanes 16r .. 16r+15), every lane gets the total;
+// in-register lane moves (quad_perm for xor 1 and 2, row_ror 4 and 8), no LDS traffic.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false));  // quad_perm 1,0,3,2
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xf, 0xf, false));  // quad_perm 2,3,0,1
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xf, 0xf, false)); // row_ror 4
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xf, 0xf, false)); // row_ror 8
+  return v;
+}
+// Sum over aligned groups of 8 lanes (row_ror 4 wraps within 16, so use a half-row mask).
+__device__ __forceinline__ float oct8_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xf, 0xf, false));
+  v += __shfl_xor(v, 4, 64);
+  return v;
+}
+
 // Block-wide sum for blockDim.x a multiple of 64 (<= 1024). `red` holds >= 16 floats.
 __device__ __forceinline__ float block_sum(float v, float* red) {
   v = wave_sum(v);
@@ -82,6 +99,30 @@ __device__ __forceinline__ void load8(const bf16_t* p, float* v) {
     v[2 * i] = __uint_as_float(w[i] << 16);
     v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
+}
+// Raw 8-element chunks (bf16: one 16-byte load; fp32: two), loaded first and widened later.
+struct Raw8b { uint4 a; };
+struct Raw8f { uint4 a, b; };
+template <typename T> struct Raw8;
+template <> struct Raw8<bf16_t> { typedef Raw8b type; };
+template <> struct Raw8<float> { typedef Raw8f type; };
+__device__ __forceinline__ Raw8b ld_raw8(const bf16_t* p) { return Raw8b{*reinterpret_cast<const uint4*>(p)}; }
+__device__ __forceinline__ Raw8f ld_raw8(const float* p) {
+  return Raw8f{*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 4)};
+}
+__device__ __forceinline__ void unpack8(const Raw8b& c, float* v) {
+  const uint32_t w[4] = {c.a.x, c.a.y, c.a.z, c.a.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void unpack8(const Raw8f& c, float* v) {
+  v[0] = __uint_as_float(c.a.x); v[1] = __uint_as_float(c.a.y);
+  v[2] = __uint_as_float(c.a.z); v[3] = __uint_as_float(c.a.w);
+  v[4] = __uint_as_float(c.b.x); v[5] = __uint_as_float(c.b.y);
+  v[6] = __uint_as_float(c.b.z); v[7] = __uint_as_float(c.b.w);
 }
 __device__ __forceinline__ void load8(const float* p, float* v) {
   float4 a = *reinterpret_cast<const float4*>(p);

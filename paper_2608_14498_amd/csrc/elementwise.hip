@@ -405,30 +405,39 @@ hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const in
 // ------------------------------------------------------------------------------------
 // Greedy argmax per row (lowest index on ties).
 // ------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_argmax(const float* __restrict__ logits, int V,
-                                                int32_t* __restrict__ out) {
+__device__ __forceinline__ void argmax_merge(float& best, int& bi, float vb, int ib) {
+  if (vb > best || (vb == best && ib < bi)) {
+    best = vb;
+    bi = ib;
+  }
+}
+
+__global__ __launch_bounds__(1024) void k_argmax(const float* __restrict__ logits, int V,
+                                                 int32_t* __restrict__ out) {
   const int b = blockIdx.x;
   const float* row = logits + (int64_t)b * V;
   float best = -INFINITY;
   int bi = 0x7fffffff;
-  for (int i = threadIdx.x; i < V; i += blockDim.x) {
-    const float x = row[i];
-    if (x > best) {  // i increases per thread: strict > keeps the lowest index
-      best = x;
-      bi = i;
+  if ((V & 3) == 0) {
+    const f32x4_t* row4 = reinterpret_cast<const f32x4_t*>(row);
+    for (int i = threadIdx.x; i < V / 4; i += blockDim.x) {  // i increases: strict > keeps the lowest index
+      const f32x4_t x = row4[i];
+      argmax_merge(best, bi, x[0], 4 * i);
+      argmax_merge(best, bi, x[1], 4 * i + 1);
+      argmax_merge(best, bi, x[2], 4 * i + 2);
+      argmax_merge(best, bi, x[3], 4 * i + 3);
     }
+  } else {
+    for (int i = threadIdx.x; i < V; i += blockDim.x) argmax_merge(best, bi, row[i], i);
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float vb = __shfl_xor(best, o, kWave);
     const int ib = __shfl_xor(bi, o, kWave);
-    if (vb > best || (vb == best && ib < bi)) {
-      best = vb;
-      bi = ib;
-    }
+    argmax_merge(best, bi, vb, ib);
   }
-  __shared__ float sv[4];
-  __shared__ int si[4];
+  __shared__ float sv[16];
+  __shared__ int si[16];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   if (lane == 0) {
     sv[w] = best;
@@ -436,17 +445,13 @@ __global__ __launch_bounds__(256) void k_argmax(const float* __restrict__ logits
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int k = 1; k < 4; ++k)
-      if (sv[k] > best || (sv[k] == best && si[k] < bi)) {
-        best = sv[k];
-        bi = si[k];
-      }
+    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) argmax_merge(best, bi, sv[k], si[k]);
     out[b] = bi == 0x7fffffff ? -1 : bi;
   }
 }
 
 hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t V, int32_t* out) {
-  k_argmax<<<B, 256, 0, s>>>(logits, V, out);
+  k_argmax<<<B, 1024, 0, s>>>(logits, V, out);
   return hipGetLastError();
 }
 
