@@ -204,6 +204,19 @@ def colocation(args, w):
     print(json.dumps(out), flush=True)
 
 
+def measured_traffic(kernel_src: str, path: str):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter runs,
+    or None when the kernel source has changed since those counters were taken."""
+    import hashlib
+
+    try:
+        rec = json.load(open(os.path.join(ROOT, path)))
+        cur = hashlib.sha1(open(os.path.join(ROOT, kernel_src), "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    return rec["traffic_bytes_per_launch"] if rec.get("gemm_source_sha1") == cur else None
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -214,7 +227,20 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-prefix-len", type=int, default=0,
                     help="truncate the CPU-baseline sample prefix (0 = full)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+
+        n = args.calibrate_copy << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the path shards by "
               f"sequence and is measured on one GPU's share.", file=sys.stderr)
@@ -304,9 +330,15 @@ def main():
     roofline = None
     if gu:
         ach = gu_flops / (gu["avg_ms"] * 1e-3) / 1e12
-        roofline = {"kernel": "gemm_gate_up (prefix)", "bound": "mfma", "achieved": ach,
+        traffic = None
+        if w.name == "qwen7b_b4_p4096_s256":
+            traffic = measured_traffic("paper_2608_14498_amd/csrc/gemm.hip",
+                                       "profiles/gemm_gate_up_qwen7b_p4096_traffic.json")
+        roofline = {"kernel": "prefix.gemm_gate_up (fused SwiGLU)", "bound": "mfma", "achieved": ach,
                     "peak": peak / 1e12, "unit": "TFLOP/s", "frac": ach / (peak / 1e12),
-                    "traffic": None, "algorithmic_per_launch": gu_flops}
+                    "traffic": traffic, "algorithmic_per_launch": gu_flops,
+                    "algorithmic_bytes_per_launch": 2 * (T * m.d_model + 2 * m.ffn_dim * m.d_model
+                                                         + T * m.ffn_dim)}
     ls = kernels.get("suffix.logsoftmax_gather")
     k12 = None
     if ls:
