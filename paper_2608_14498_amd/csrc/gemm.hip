@@ -2,16 +2,18 @@
 // A is row-major activations, B is nn.Linear weights [out, in] given as up to three row
 // segments (q/k/v or gate/up projections without a concatenated copy).
 //
-// bf16 (v_mfma_f32_32x32x16_bf16): a 256x256 C tile per workgroup, K in 64-deep slabs.
-//   * 4 waves (2x2, 128x128 each, one wave per SIMD) or 8 waves (4x2, 64x128 each, two
-//     waves per SIMD); accumulators live in the accumulation registers.
+// bf16 (v_mfma_f32_32x32x16_bf16): a 256x256 C tile per workgroup of 8 waves (4x2, each
+// 64x128, two waves per SIMD), K in 64-deep slabs, fp32 accumulators in registers.
 //   * A/B slabs are staged through LDS, double buffered (2 x 64 KiB), each row of 8
 //     16-byte chunks XOR-swizzled so that any 8 (32-bank) or 16 (64-bank) consecutive
 //     rows read by one MFMA operand fetch hit distinct banks: no LDS bank conflicts.
-//   * In-tile pipeline: the LDS reads of k-step s+1 are issued before the MFMAs of step
-//     s.  A wave issues in order, so the next slab's global loads are interleaved with
-//     the MFMAs of k-steps 0-1 and its LDS stores with those of steps 2-3 (a burst of
-//     loads at the top of the tile would block the MFMAs behind it).
+//   * Main kernel: the load unit copies the next slab straight into the idle LDS buffer
+//     (buffer_load ... lds), issued at the top of the current slab and interleaved with
+//     its MFMAs; the tile barrier sits before the last k-step so the next slab's first
+//     fragments are read under that step's MFMAs.  A register-staged variant (global ->
+//     VGPR -> LDS) serves operands that do not fit one 2 GiB buffer window.
+//   * The MFMAs take the B fragment as first operand, so each lane ends with 4
+//     consecutive columns of one output row: 8-byte bf16 / 16-byte fp32 stores.
 //   * Tiles are visited in groups of 8 tile-rows and the block index is remapped so each
 //     XCD walks a contiguous range of tiles (its L2 holds the shared A/B slabs).
 //   * Epilogues: bf16 store, fp32 store, fp32 accumulate (residual), fused SwiGLU (each
@@ -35,6 +37,9 @@ struct GemmArgs {
   int tiles_m, tiles_n;
   int k_chunk;       // K range per split (multiple of the k slab)
   float* partials;   // split-K: [splitk][M][N] fp32
+  // LDS-DMA kernel only: the B segments as byte offsets from one base
+  const void* Bbase;
+  uint32_t boff[3];
 };
 
 template <typename T>
@@ -61,6 +66,90 @@ __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 constexpr int GB_M = 256, GB_N = 256, GB_K = 64;
 
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + expf(-g)) * u; }
+
+// Four consecutive outputs n0..n0+3 of one row: one 8-byte (bf16) or 16-byte (fp32)
+// access when the row is aligned for it and the four columns are all inside [0, N).
+__device__ __forceinline__ void store4(bf16_t* row, int n0, int N, const float (&v)[4], bool vec) {
+  if (vec && n0 + 3 < N) {
+    *reinterpret_cast<uint2*>(row + n0) = make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+  } else {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (n0 + t < N) row[n0 + t] = f2bf(v[t]);
+  }
+}
+template <bool ADD>
+__device__ __forceinline__ void store4(float* row, int n0, int N, const float (&v)[4], bool vec) {
+  if (vec && n0 + 3 < N) {
+    float4* p = reinterpret_cast<float4*>(row + n0);
+    float4 o = ADD ? *p : make_float4(0.f, 0.f, 0.f, 0.f);
+    o.x += v[0];
+    o.y += v[1];
+    o.z += v[2];
+    o.w += v[3];
+    *p = o;
+  } else {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (n0 + t < N) row[n0 + t] = ADD ? row[n0 + t] + v[t] : v[t];
+  }
+}
+
+// Epilogue of the bf16 kernels.  The MFMAs take the B fragment as their first operand,
+// so a lane holds rows of C^T: acc[i][j][e] = C(row i*32 + fr, col j*32 + 8(e/4) + 4 fk
+// + e%4) of the wave tile, i.e. four consecutive columns of one row per e/4.
+template <int EPI, int MI, int NJ, int TM, int TN>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)[MI][NJ], int tm, int tn, int wm,
+                                              int wn, int fr, int fk) {
+  const int mb = tm * GB_M + wm * TM + fr;
+  if (EPI == EPI_SWIGLU) {  // gate in acc[i][j], up in acc[i][j + 2]
+    const bool vec = (g.ldc & 3) == 0 && ((uintptr_t)g.C & 7) == 0;
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int m = mb + i * 32;
+      if (m >= g.M) continue;
+      bf16_t* row = (bf16_t*)g.C + (int64_t)m * g.ldc;
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = silu_mul(acc[i][j][4 * q + t], acc[i][j + 2][4 * q + t]);
+          store4(row, tn * 128 + wn * 64 + j * 32 + 8 * q + 4 * fk, g.N, v, vec);
+        }
+    }
+    return;
+  }
+  bool vec;
+  if (EPI == -1)
+    vec = (g.N & 3) == 0 && ((uintptr_t)g.partials & 15) == 0;
+  else if (EPI == EPI_STORE)
+    vec = (g.ldc & 3) == 0 && ((uintptr_t)g.C & 7) == 0;
+  else
+    vec = (g.ldc & 3) == 0 && ((uintptr_t)g.C & 15) == 0;
+  const int nb = tn * GB_N + wn * TN + 4 * fk;
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    const int m = mb + i * 32;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n0 = nb + j * 32 + 8 * q;
+        const float v[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if (EPI == -1)
+          store4<false>(g.partials + ((int64_t)blockIdx.y * g.M + m) * g.N, n0, g.N, v, vec);
+        else if (EPI == EPI_STORE)
+          store4((bf16_t*)g.C + (int64_t)m * g.ldc, n0, g.N, v, vec);
+        else if (EPI == EPI_STORE_F32)
+          store4<false>((float*)g.C + (int64_t)m * g.ldc, n0, g.N, v, vec);
+        else
+          store4<true>((float*)g.C + (int64_t)m * g.ldc, n0, g.N, v, vec);
+      }
+  }
+}
 
 // ------------------------------------------------------------------------------------
 // bf16 MFMA GEMM
@@ -133,7 +222,7 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 #define G_MMA(AF, BF)                                                           \
   _Pragma("unroll") for (int i = 0; i < MI; ++i)                                \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j)                                \
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(AF[i], BF[j], acc[i][j], 0, 0, 0);
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(BF[j], AF[i], acc[i][j], 0, 0, 0);
 // spread n_other_ instructions of class mask_ evenly over the MM MFMAs of this region
 #define G_INTERLEAVE(mask_, n_other_)                                           \
   _Pragma("unroll") for (int q = 0; q < (n_other_); ++q) {                      \
@@ -200,48 +289,151 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 #undef G_MMA
 #undef G_INTERLEAVE
 
-  // epilogue: acc[i][j][e] = C(row i*32 + 8(e/4) + 4 fk + e%4, col j*32 + fr) of the wave tile
-  if (EPI == EPI_SWIGLU) {
+  gemm_epilogue<EPI, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
+}
+
+// ------------------------------------------------------------------------------------
+// bf16 MFMA GEMM fed by direct global->LDS loads (global_load_lds_dwordx4).
+// Same tile, wave layout, swizzle and epilogues as k_gemm_bf16, but the next slab is
+// copied straight into the idle LDS buffer by the load unit: the loads of slab kt+1 are
+// issued at the start of slab kt and have the whole slab's MFMA time to land (the
+// register-staged pipeline gives them about half of it), and no VGPRs or LDS store
+// instructions are spent on staging.  One load instruction writes 64 consecutive 16-byte
+// LDS chunks (8 rows of one slab); the swizzle is applied by choosing which global
+// chunk each lane fetches.  The two LDS buffers are separate arrays and the k loop is
+// unrolled by two, so every LDS access names its buffer at compile time.
+// ------------------------------------------------------------------------------------
+template <int EPI, int WGM>
+__global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16_dma(GemmArgs g) {
+#if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
+  constexpr int NT = WGM * 2 * 64;
+  constexpr int NW = NT / 64;
+  constexpr int TM = GB_M / WGM, TN = GB_N / 2;
+  constexpr int MI = TM / 32, NJ = TN / 32;
+  constexpr int LOADS = (GB_M * 8) / NT;  // load instructions per matrix per wave: 8 or 4
+  constexpr int MM = MI * NJ;
+  typedef __attribute__((address_space(3))) void lds_void;
+  // native vector element type: each fragment read is one 16-byte LDS load in the IR
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  __shared__ u32x4_t As0[GB_M * 8], As1[GB_M * 8];
+  __shared__ u32x4_t Bs0[GB_N * 8], Bs1[GB_N * 8];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  int tm, tn;
+  tile_coords(xcd_remap(blockIdx.x, gridDim.x), g.tiles_m, g.tiles_n, &tm, &tn);
+  const int m0 = tm * GB_M;
+  const int kbeg = blockIdx.y * g.k_chunk;
+  const int kend = min(g.K, kbeg + g.k_chunk);
+  const int KT = (kend - kbeg) / GB_K;
+
+  // Load instruction i of this wave fills LDS rows wave*8*LOADS + 8i .. +8; lane l writes
+  // physical chunk l%8 of row +l/8, which holds logical chunk (l%8) ^ swz(row).  Sources
+  // are byte offsets into one buffer resource per operand (the host guarantees every
+  // operand byte lies within 2 GiB of the resource base); the slab offset is uniform.
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc((void*)g.Bbase, 0, 0x7fffffff, 0x00020000);
+  uint32_t aoff[LOADS], boff[LOADS];
 #pragma unroll
-    for (int i = 0; i < MI; ++i) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int f = tn * 128 + wn * 64 + j * 32 + fr;
-        if (f >= g.N) continue;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = m0 + wm * TM + i * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
-          if (m >= g.M) continue;
-          ((bf16_t*)g.C)[(int64_t)m * g.ldc + f] = f2bf(silu_mul(acc[i][j][e], acc[i][j + 2][e]));
-        }
-      }
+  for (int i = 0; i < LOADS; ++i) {
+    const int r = wave * 8 * LOADS + 8 * i + (lane >> 3);
+    const int c = (lane & 7) ^ swz(r);
+    aoff[i] = 2u * ((uint32_t)min(m0 + r, g.M - 1) * (uint32_t)g.lda + (uint32_t)(kbeg + c * 8));
+    int br;
+    if (EPI == EPI_SWIGLU) {  // per 128-row half: 64 gate rows then the matching 64 up rows
+      const int w = r >> 7, cc = r & 127;
+      br = (cc >= 64 ? g.B.n1 : 0) + min(tn * 128 + w * 64 + (cc & 63), g.N - 1);
+    } else {
+      br = min(tn * GB_N + r, g.N - 1);
     }
-    return;
+    const uint32_t seg = br < g.B.n1 ? g.boff[0] : br < g.B.n2 ? g.boff[1] : g.boff[2];
+    const int rin = br < g.B.n1 ? br : br < g.B.n2 ? br - g.B.n1 : br - g.B.n2;
+    boff[i] = seg + 2u * ((uint32_t)rin * (uint32_t)g.ldb + (uint32_t)(kbeg + c * 8));
   }
-  const int n0 = tn * GB_N;
+#define D_LOAD(DA, DB, kt_)                                                                            \
+  _Pragma("unroll") for (int i = 0; i < LOADS; ++i) {                                                 \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)(DA + (wave * LOADS + i) * 64), 16, aoff[i], \
+                                             (kt_) * (GB_K * 2), 0, 0);                                \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void*)(DB + (wave * LOADS + i) * 64), 16, boff[i], \
+                                             (kt_) * (GB_K * 2), 0, 0);                                \
+  }
+#define D_FRAGS(AF, BF, SA, SB, ks_)                                          \
+  _Pragma("unroll") for (int i = 0; i < MI; ++i) {                            \
+    const int r_ = wm * TM + i * 32 + fr;                                     \
+    AF[i] = __builtin_bit_cast(bf16x8_t, SA[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+  }                                                                           \
+  _Pragma("unroll") for (int j = 0; j < NJ; ++j) {                            \
+    const int r_ = wn * TN + j * 32 + fr;                                     \
+    BF[j] = __builtin_bit_cast(bf16x8_t, SB[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+  }
+#define D_MMA(AF, BF)                                                         \
+  _Pragma("unroll") for (int i = 0; i < MI; ++i)                              \
+  _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(BF[j], AF[i], acc[i][j], 0, 0, 0);
+  // One 64-deep slab read from (SA, SB) while slab kt_+1 streams into (DA, DB).  The
+  // barrier sits before the last k-step: the fragments of k-step 0 of the next slab are
+  // read (from DA, DB) under the MFMAs of k-step 3, so no slab starts with a wait on
+  // LDS.  DA/DB are free at the top of the slab: their last reads (k-step 3 fragments of
+  // the previous slab) were issued before the previous barrier.
+#define D_REGION(n_mem_, mem_mask_)                                                        \
+  __builtin_amdgcn_sched_group_barrier(0x100, MI + NJ, 0);                                 \
+  _Pragma("unroll") for (int q = 0; q < MM; ++q) {                                         \
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                     \
+    if (q < (n_mem_)) __builtin_amdgcn_sched_group_barrier((mem_mask_), 1, 0);             \
+  }
+#define D_TILE(SA, SB, DA, DB, kt_)                                           \
+  {                                                                           \
+    const int ktn_ = (kt_) + 1 < KT ? (kt_) + 1 : (kt_);                      \
+    D_FRAGS(af1, bf1, SA, SB, 1);                                             \
+    D_MMA(af0, bf0);                                                          \
+    D_LOAD(DA, DB, ktn_);                                                     \
+    D_REGION(2 * LOADS, 0x010);                                               \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+    D_FRAGS(af0, bf0, SA, SB, 2);                                             \
+    D_MMA(af1, bf1);                                                          \
+    D_REGION(0, 0x000);                                                       \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+    D_FRAGS(af1, bf1, SA, SB, 3);                                             \
+    D_MMA(af0, bf0);                                                          \
+    D_REGION(0, 0x000);                                                       \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+    __syncthreads();                                                          \
+    D_FRAGS(af0, bf0, DA, DB, 0);                                             \
+    D_MMA(af1, bf1);                                                          \
+    D_REGION(0, 0x000);                                                       \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+  }
+
+  f32x16_t acc[MI][NJ];
 #pragma unroll
-  for (int i = 0; i < MI; ++i) {
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int n = n0 + wn * TN + j * 32 + fr;
-      if (n >= g.N) continue;
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int m = m0 + wm * TM + i * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
-        if (m >= g.M) continue;
-        const float v = acc[i][j][e];
-        if (EPI == -1) {
-          g.partials[((int64_t)blockIdx.y * g.M + m) * g.N + n] = v;
-        } else if (EPI == EPI_STORE) {
-          ((bf16_t*)g.C)[(int64_t)m * g.ldc + n] = f2bf(v);
-        } else if (EPI == EPI_STORE_F32) {
-          ((float*)g.C)[(int64_t)m * g.ldc + n] = v;
-        } else {
-          ((float*)g.C)[(int64_t)m * g.ldc + n] += v;
-        }
-      }
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int fr = lane & 31, fk = lane >> 5;
+  bf16x8_t af0[MI], bf0[NJ], af1[MI], bf1[NJ];
+  if (KT > 0) {
+    D_LOAD(As0, Bs0, 0);
+    __syncthreads();
+    D_FRAGS(af0, bf0, As0, Bs0, 0);
+    int kt = 0;
+    for (; kt + 2 <= KT; kt += 2) {
+      D_TILE(As0, Bs0, As1, Bs1, kt);
+      D_TILE(As1, Bs1, As0, Bs0, kt + 1);
     }
+    if (kt < KT) D_TILE(As0, Bs0, As1, Bs1, kt);
   }
+#undef D_LOAD
+#undef D_FRAGS
+#undef D_MMA
+#undef D_TILE
+#undef D_REGION
+  (void)NW;
+  gemm_epilogue<EPI, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
+#endif
 }
 
 // ------------------------------------------------------------------------------------
@@ -331,14 +523,38 @@ size_t gemm_partial_floats(int32_t M, int32_t N, int32_t splitk) {
   return splitk > 1 ? (size_t)splitk * M * N : 0;
 }
 
-// Workgroup shape of a bf16 GEMM: 8 waves (two per SIMD), except for very wide outputs,
-// where one 128x128 tile per wave measured faster.
-static bool four_waves_for(int32_t N, Epi epi) { return epi == EPI_SWIGLU || N >= 16384; }
+// The LDS-DMA kernel addresses each operand through a buffer resource with 32-bit byte
+// offsets: it is usable when A, and all used B segments together, span less than 2 GiB.
+// b_rows is the number of logical B rows (N, or n1 + N for the fused SwiGLU layout).
+static bool dma_setup(GemmArgs& g, int64_t b_rows) {
+  constexpr uint64_t kLim = 0x7FFFFF00ull;  // the resources cover 2 GiB
+  if (g.M <= 0 || g.K <= 0) return false;
+  const uint64_t a_ext = ((uint64_t)(g.M - 1) * (uint64_t)g.lda + (uint64_t)g.K) * 2u;
+  if (a_ext > kLim) return false;
+  const void* base[3] = {g.B.b0, g.B.b1, g.B.b2};
+  const int64_t start[3] = {0, g.B.n1, g.B.n2};
+  const int64_t end[3] = {g.B.n1, g.B.n2, b_rows};
+  uintptr_t lo = UINTPTR_MAX, hi = 0;
+  int64_t rows[3];
+  for (int k = 0; k < 3; ++k) {
+    rows[k] = std::min(end[k], b_rows) - start[k];
+    if (rows[k] <= 0) continue;
+    const uintptr_t p = (uintptr_t)base[k];
+    lo = std::min(lo, p);
+    hi = std::max(hi, p + (uintptr_t)(((uint64_t)(rows[k] - 1) * (uint64_t)g.ldb + (uint64_t)g.K) * 2u));
+  }
+  if (hi <= lo || hi - lo > kLim) return false;
+  g.Bbase = (const void*)lo;
+  for (int k = 0; k < 3; ++k) g.boff[k] = rows[k] > 0 ? (uint32_t)((uintptr_t)base[k] - lo) : 0u;
+  return true;
+}
 
+// bf16 GEMMs run 8 waves per workgroup (two per SIMD, 64x128 per wave); operands are
+// streamed by the LDS-DMA kernel unless they span more than its 2 GiB buffer window.
 template <int EPI>
-static void launch_bf16(hipStream_t s, const GemmArgs& g, dim3 grid, bool four_waves) {
-  if (four_waves)
-    k_gemm_bf16<EPI, 2><<<grid, 256, 0, s>>>(g);
+static void launch_bf16(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, bool allow_dma = true) {
+  if (allow_dma && dma_setup(g, b_rows))
+    k_gemm_bf16_dma<EPI, 4><<<grid, 512, 0, s>>>(g);
   else
     k_gemm_bf16<EPI, 4><<<grid, 512, 0, s>>>(g);
 }
@@ -370,17 +586,17 @@ hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K
     g.tiles_m = (M + GB_M - 1) / GB_M;
     g.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB_N - 1) / GB_N;
     dim3 grid(g.tiles_m * g.tiles_n, splitk);
-    const bool four = four_waves_for(N, epi);
+    const int64_t b_rows = epi == EPI_SWIGLU ? (int64_t)B.n1 + N : N;
     if (split)
-      launch_bf16<-1>(s, g, grid, four);
+      launch_bf16<-1>(s, g, grid, b_rows);
     else if (epi == EPI_STORE)
-      launch_bf16<EPI_STORE>(s, g, grid, four);
+      launch_bf16<EPI_STORE>(s, g, grid, b_rows);
     else if (epi == EPI_STORE_F32)
-      launch_bf16<EPI_STORE_F32>(s, g, grid, four);
+      launch_bf16<EPI_STORE_F32>(s, g, grid, b_rows);
     else if (epi == EPI_SWIGLU)
-      launch_bf16<EPI_SWIGLU>(s, g, grid, four);
+      launch_bf16<EPI_SWIGLU>(s, g, grid, b_rows);
     else
-      launch_bf16<EPI_ADD_F32>(s, g, grid, four);
+      launch_bf16<EPI_ADD_F32>(s, g, grid, b_rows);
   } else {
     g.tiles_m = (M + GF_M - 1) / GF_M;
     g.tiles_n = (N + GF_N - 1) / GF_N;
@@ -405,8 +621,8 @@ hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K
   return hipGetLastError();
 }
 
-// Timing-harness hook: plain bf16 store epilogue with a forced workgroup shape
-// (variant 0: 4 waves, otherwise 8 waves).
+// Timing-harness hook: plain bf16 store epilogue; variant 0 forces the register-staged
+// kernel, any other value the LDS-DMA kernel.
 hipError_t launch_gemm_variant(hipStream_t s, int variant, int32_t M, int32_t N, int32_t K, const void* A,
                                const void* B, void* C) {
   GemmArgs g;
@@ -424,7 +640,7 @@ hipError_t launch_gemm_variant(hipStream_t s, int variant, int32_t M, int32_t N,
   g.tiles_m = (M + GB_M - 1) / GB_M;
   g.tiles_n = (N + GB_N - 1) / GB_N;
   dim3 grid(g.tiles_m * g.tiles_n, 1);
-  launch_bf16<EPI_STORE>(s, g, grid, variant == 0);
+  launch_bf16<EPI_STORE>(s, g, grid, N, variant != 0);
   return hipGetLastError();
 }
 
