@@ -2,7 +2,7 @@
 // A is row-major activations, B is nn.Linear weights [out, in] given as up to three row
 // segments (q/k/v or gate/up projections without a concatenated copy).
 //
-// bf16 (v_mfma_f32_32x32x16_bf16): a 256x256 C tile per workgroup of 8 waves (4x2, each
+// 16-bit (v_mfma_f32_32x32x16_bf16 / _f16): a 256x256 C tile per workgroup of 8 waves (4x2, each
 // 64x128, two waves per SIMD), K in 64-deep slabs, fp32 accumulators in registers.
 //   * A/B slabs are staged through LDS, double buffered (2 x 64 KiB), each row of 8
 //     16-byte chunks XOR-swizzled so that any 8 (32-bank) or 16 (64-bank) consecutive
@@ -69,13 +69,15 @@ __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f +
 
 // Four consecutive outputs n0..n0+3 of one row: one 8-byte (bf16) or 16-byte (fp32)
 // access when the row is aligned for it and the four columns are all inside [0, N).
-__device__ __forceinline__ void store4(bf16_t* row, int n0, int N, const float (&v)[4], bool vec) {
+template <typename T16>
+__device__ __forceinline__ void store4h(T16* row, int n0, int N, const float (&v)[4], bool vec) {
   if (vec && n0 + 3 < N) {
-    *reinterpret_cast<uint2*>(row + n0) = make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+    *reinterpret_cast<uint2*>(row + n0) =
+        make_uint2(Half16<T16>::pack2(v[0], v[1]), Half16<T16>::pack2(v[2], v[3]));
   } else {
 #pragma unroll
     for (int t = 0; t < 4; ++t)
-      if (n0 + t < N) row[n0 + t] = f2bf(v[t]);
+      if (n0 + t < N) stf(row + n0 + t, v[t]);
   }
 }
 template <bool ADD>
@@ -98,7 +100,7 @@ __device__ __forceinline__ void store4(float* row, int n0, int N, const float (&
 // Epilogue of the bf16 kernels.  The MFMAs take the B fragment as their first operand,
 // so a lane holds rows of C^T: acc[i][j][e] = C(row i*32 + fr, col j*32 + 8(e/4) + 4 fk
 // + e%4) of the wave tile, i.e. four consecutive columns of one row per e/4.
-template <int EPI, int MI, int NJ, int TM, int TN>
+template <int EPI, typename T16, int MI, int NJ, int TM, int TN>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)[MI][NJ], int tm, int tn, int wm,
                                               int wn, int fr, int fk) {
   const int mb = tm * GB_M + wm * TM + fr;
@@ -108,7 +110,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)
     for (int i = 0; i < MI; ++i) {
       const int m = mb + i * 32;
       if (m >= g.M) continue;
-      bf16_t* row = (bf16_t*)g.C + (int64_t)m * g.ldc;
+      T16* row = (T16*)g.C + (int64_t)m * g.ldc;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -116,7 +118,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)
           float v[4];
 #pragma unroll
           for (int t = 0; t < 4; ++t) v[t] = silu_mul(acc[i][j][4 * q + t], acc[i][j + 2][4 * q + t]);
-          store4(row, tn * 128 + wn * 64 + j * 32 + 8 * q + 4 * fk, g.N, v, vec);
+          store4h(row, tn * 128 + wn * 64 + j * 32 + 8 * q + 4 * fk, g.N, v, vec);
         }
     }
     return;
@@ -142,7 +144,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)
         if (EPI == -1)
           store4<false>(g.partials + ((int64_t)blockIdx.y * g.M + m) * g.N, n0, g.N, v, vec);
         else if (EPI == EPI_STORE)
-          store4((bf16_t*)g.C + (int64_t)m * g.ldc, n0, g.N, v, vec);
+          store4h((T16*)g.C + (int64_t)m * g.ldc, n0, g.N, v, vec);
         else if (EPI == EPI_STORE_F32)
           store4<false>((float*)g.C + (int64_t)m * g.ldc, n0, g.N, v, vec);
         else
@@ -151,11 +153,128 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)
   }
 }
 
+// Epilogue through LDS for the 8-wave kernels (wave tile 64 x 128).  After the main
+// loop the LDS is free: each wave stages its sub-tile in a private 16 KiB region and
+// writes it back as whole row segments (256 B of bf16 or 512 B of fp32 per row), one
+// 16-byte access per lane, instead of 4 columns x 32 rows per store instruction.
+// Staging layout: row-major, 8-byte (bf16) or 16-byte (fp32) chunks XOR-swizzled with
+// the row so that the 32 rows written by one instruction fall in distinct banks.
+template <int EPI, typename T16, int MI, int NJ, int TM, int TN>
+__device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&acc)[MI][NJ], uint8_t* stage,
+                                                  int tm, int tn, int wm, int wn, int lane) {
+  static_assert(MI == 2 && NJ == 4 && TM == 64 && TN == 128, "8-wave tile only");
+  const int fr = lane & 31, fk = lane >> 5;
+  const int mw = tm * GB_M + wm * TM;  // first row of the wave tile
+  if (EPI == EPI_SWIGLU || EPI == EPI_STORE) {
+    // bf16 output: SwiGLU gives 64 features per row (rows of 128 B), plain 128 (256 B)
+    constexpr int W8 = EPI == EPI_SWIGLU ? 16 : 32;  // 8-byte chunks per staged row
+    constexpr int XM = W8 - 1;
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int r = i * 32 + fr;
+#pragma unroll
+      for (int j = 0; j < (EPI == EPI_SWIGLU ? 2 : NJ); ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+            v[t] = EPI == EPI_SWIGLU ? silu_mul(acc[i][j][4 * q + t], acc[i][j + 2][4 * q + t]) : acc[i][j][4 * q + t];
+          const int c8 = j * 8 + 2 * q + fk;
+          *reinterpret_cast<uint2*>(stage + r * (W8 * 8) + ((c8 ^ (r & XM)) << 3)) =
+              make_uint2(Half16<T16>::pack2(v[0], v[1]), Half16<T16>::pack2(v[2], v[3]));
+        }
+    }
+    constexpr int LPR = W8 / 2;  // lanes per row (16 bytes each)
+    constexpr int RPI = 64 / LPR;  // rows per instruction
+    const int ncol0 = EPI == EPI_SWIGLU ? tn * 128 + wn * 64 : tn * GB_N + wn * TN;
+    const bool vec = (g.ldc & 7) == 0 && ((uintptr_t)g.C & 15) == 0;
+    const int k = lane % LPR;
+#pragma unroll
+    for (int s = 0; s < 64 / RPI; ++s) {
+      const int r = s * RPI + lane / LPR;
+      uint4 v = *reinterpret_cast<const uint4*>(stage + r * (W8 * 8) + ((k ^ ((r & XM) >> 1)) << 4));
+      if (r & 1) {  // the two 8-byte halves were stored swapped
+        const uint32_t x = v.x, y = v.y;
+        v.x = v.z;
+        v.y = v.w;
+        v.z = x;
+        v.w = y;
+      }
+      const int m = mw + r, n = ncol0 + k * 8;
+      if (m >= g.M) continue;
+      T16* dst = (T16*)g.C + (int64_t)m * g.ldc + n;
+      if (vec && n + 7 < g.N) {
+        *reinterpret_cast<uint4*>(dst) = v;
+      } else {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (n + e < g.N) reinterpret_cast<uint16_t*>(dst)[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+      }
+    }
+    return;
+  }
+  // fp32 outputs (store, residual accumulate, split-K partials): two passes of 32 rows,
+  // staged rows of 128 floats (32 chunks of 16 bytes)
+  float* out;
+  int64_t ld;
+  bool vec;
+  if (EPI == -1) {
+    out = g.partials + (int64_t)blockIdx.y * g.M * g.N;
+    ld = g.N;
+    vec = (g.N & 3) == 0 && ((uintptr_t)g.partials & 15) == 0;
+  } else {
+    out = (float*)g.C;
+    ld = g.ldc;
+    vec = (g.ldc & 3) == 0 && ((uintptr_t)g.C & 15) == 0;
+  }
+  const int ncol0 = tn * GB_N + wn * TN;
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    if (i > 0) __builtin_amdgcn_s_waitcnt(0xc07f);  // previous pass's LDS reads are done (lgkmcnt(0))
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c16 = j * 8 + 2 * q + fk;
+        *reinterpret_cast<float4*>(stage + fr * 512 + ((c16 ^ (fr & 15)) << 4)) =
+            make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+      }
+    const int k = lane & 31;
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      const int r = 2 * s + (lane >> 5);
+      const float4 v = *reinterpret_cast<const float4*>(stage + r * 512 + ((k ^ (r & 15)) << 4));
+      const int m = mw + i * 32 + r, n = ncol0 + k * 4;
+      if (m >= g.M) continue;
+      float* dst = out + (int64_t)m * ld + n;
+      if (vec && n + 3 < g.N) {
+        float4 o = v;
+        if (EPI == EPI_ADD_F32) {
+          const float4 c = *reinterpret_cast<const float4*>(dst);
+          o.x += c.x;
+          o.y += c.y;
+          o.z += c.z;
+          o.w += c.w;
+        }
+        *reinterpret_cast<float4*>(dst) = o;
+      } else {
+        const float w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < g.N) dst[e] = EPI == EPI_ADD_F32 ? dst[e] + w[e] : w[e];
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------------------------
 // bf16 MFMA GEMM
 // ------------------------------------------------------------------------------------
-template <int EPI, int WGM>
+template <int EPI, typename T16, int WGM>
 __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
+  typedef typename Half16<T16>::V8 V8;
   constexpr int NT = WGM * 2 * 64;
   constexpr int TM = GB_M / WGM, TN = GB_N / 2;
   constexpr int MI = TM / 32, NJ = TN / 32;
@@ -174,7 +293,7 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
   const int KT = (kend - kbeg) / GB_K;
 
   const int lc = tid & 7, lr = tid >> 3;
-  const bf16_t* Ab = (const bf16_t*)g.A + kbeg + lc * 8;
+  const T16* Ab = (const T16*)g.A + kbeg + lc * 8;
   // logical B row staged in local B row r of this tile
   auto b_logical = [&](int r) -> int {
     if (EPI == EPI_SWIGLU) {  // per 128-row half: 64 gate rows then the matching 64 up rows
@@ -193,7 +312,7 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 #define G_LDB(i_, kt_)                                                                                 \
   if (i_ < LOADS) {                                                                                    \
     const int r_ = lr + (NT / 8) * i_;                                                                 \
-    rb##i_ = *reinterpret_cast<const uint4*>(brow<bf16_t>(g.B, b_logical(r_), g.ldb) + kbeg + lc * 8 + \
+    rb##i_ = *reinterpret_cast<const uint4*>(brow<T16>(g.B, b_logical(r_), g.ldb) + kbeg + lc * 8 + \
                                              (kt_) * GB_K);                                            \
   }
 #define G_STA(i_, buf_)                                    \
@@ -213,16 +332,16 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 #define G_FRAGS(AF, BF, ks_)                                                   \
   _Pragma("unroll") for (int i = 0; i < MI; ++i) {                             \
     const int r_ = wm * TM + i * 32 + fr;                                      \
-    AF[i] = as_bf16x8(As[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]);        \
+    AF[i] = Half16<T16>::as_v8(As[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
   }                                                                            \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j) {                             \
     const int r_ = wn * TN + j * 32 + fr;                                      \
-    BF[j] = as_bf16x8(Bs[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]);        \
+    BF[j] = Half16<T16>::as_v8(Bs[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
   }
 #define G_MMA(AF, BF)                                                           \
   _Pragma("unroll") for (int i = 0; i < MI; ++i)                                \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j)                                \
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(BF[j], AF[i], acc[i][j], 0, 0, 0);
+    acc[i][j] = Half16<T16>::mma(BF[j], AF[i], acc[i][j]);
 // spread n_other_ instructions of class mask_ evenly over the MM MFMAs of this region
 #define G_INTERLEAVE(mask_, n_other_)                                           \
   _Pragma("unroll") for (int q = 0; q < (n_other_); ++q) {                      \
@@ -250,7 +369,7 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
   for (int kt = 0; kt < KT; ++kt) {
     const int buf = kt & 1;
     const int ktn = kt + 1 < KT ? kt + 1 : kt;  // the last tile re-loads itself into the idle buffer
-    bf16x8_t af0[MI], bf0[NJ], af1[MI], bf1[NJ];
+    V8 af0[MI], bf0[NJ], af1[MI], bf1[NJ];
     G_FRAGS(af0, bf0, 0);
     G_FRAGS(af1, bf1, 1);
     __builtin_amdgcn_sched_barrier(0);
@@ -289,7 +408,7 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 #undef G_MMA
 #undef G_INTERLEAVE
 
-  gemm_epilogue<EPI, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
+  gemm_epilogue<EPI, T16, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
 }
 
 // ------------------------------------------------------------------------------------
@@ -303,16 +422,17 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 // chunk each lane fetches.  The two LDS buffers are separate arrays and the k loop is
 // unrolled by two, so every LDS access names its buffer at compile time.
 // ------------------------------------------------------------------------------------
-template <int EPI, int WGM>
-__global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16_dma(GemmArgs g) {
+template <int EPI, typename T16>
+__global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
 #if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
+  constexpr int WGM = 4;  // 4 x 2 waves of 64 x 128
   constexpr int NT = WGM * 2 * 64;
-  constexpr int NW = NT / 64;
   constexpr int TM = GB_M / WGM, TN = GB_N / 2;
   constexpr int MI = TM / 32, NJ = TN / 32;
-  constexpr int LOADS = (GB_M * 8) / NT;  // load instructions per matrix per wave: 8 or 4
+  constexpr int LOADS = (GB_M * 8) / NT;  // load instructions per matrix per wave: 4
   constexpr int MM = MI * NJ;
   typedef __attribute__((address_space(3))) void lds_void;
+  typedef typename Half16<T16>::V8 V8;
   // native vector element type: each fragment read is one 16-byte LDS load in the IR
   typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
   __shared__ u32x4_t As0[GB_M * 8], As1[GB_M * 8];
@@ -361,16 +481,16 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16_dma(GemmArgs g) {
 #define D_FRAGS(AF, BF, SA, SB, ks_)                                          \
   _Pragma("unroll") for (int i = 0; i < MI; ++i) {                            \
     const int r_ = wm * TM + i * 32 + fr;                                     \
-    AF[i] = __builtin_bit_cast(bf16x8_t, SA[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+    AF[i] = __builtin_bit_cast(V8, SA[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
   }                                                                           \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j) {                            \
     const int r_ = wn * TN + j * 32 + fr;                                     \
-    BF[j] = __builtin_bit_cast(bf16x8_t, SB[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+    BF[j] = __builtin_bit_cast(V8, SB[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
   }
 #define D_MMA(AF, BF)                                                         \
   _Pragma("unroll") for (int i = 0; i < MI; ++i)                              \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(BF[j], AF[i], acc[i][j], 0, 0, 0);
+    acc[i][j] = Half16<T16>::mma(BF[j], AF[i], acc[i][j]);
   // One 64-deep slab read from (SA, SB) while slab kt_+1 streams into (DA, DB).  The
   // barrier sits before the last k-step: the fragments of k-step 0 of the next slab are
   // read (from DA, DB) under the MFMAs of k-step 3, so no slab starts with a wait on
@@ -414,7 +534,7 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16_dma(GemmArgs g) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   const int fr = lane & 31, fk = lane >> 5;
-  bf16x8_t af0[MI], bf0[NJ], af1[MI], bf1[NJ];
+  V8 af0[MI], bf0[NJ], af1[MI], bf1[NJ];
   if (KT > 0) {
     D_LOAD(As0, Bs0, 0);
     __syncthreads();
@@ -431,8 +551,9 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16_dma(GemmArgs g) {
 #undef D_MMA
 #undef D_TILE
 #undef D_REGION
-  (void)NW;
-  gemm_epilogue<EPI, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
+  __syncthreads();  // every wave is done with the slab buffers
+  uint8_t* stage = (uint8_t*)(wave < 2 ? As0 : wave < 4 ? As1 : wave < 6 ? Bs0 : Bs1) + (wave & 1) * 16384;
+  gemm_epilogue_lds<EPI, T16, MI, NJ, TM, TN>(g, acc, stage, tm, tn, wm, wn, lane);
 #endif
 }
 
@@ -551,19 +672,20 @@ static bool dma_setup(GemmArgs& g, int64_t b_rows) {
 
 // bf16 GEMMs run 8 waves per workgroup (two per SIMD, 64x128 per wave); operands are
 // streamed by the LDS-DMA kernel unless they span more than its 2 GiB buffer window.
-template <int EPI>
-static void launch_bf16(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, bool allow_dma = true) {
+template <int EPI, typename T16>
+static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, bool allow_dma = true) {
   if (allow_dma && dma_setup(g, b_rows))
-    k_gemm_bf16_dma<EPI, 4><<<grid, 512, 0, s>>>(g);
+    k_gemm_bf16_dma<EPI, T16><<<grid, 512, 0, s>>>(g);
   else
-    k_gemm_bf16<EPI, 4><<<grid, 512, 0, s>>>(g);
+    k_gemm_bf16<EPI, T16, 4><<<grid, 512, 0, s>>>(g);
 }
 
-hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K, const void* A,
+hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
                        int32_t splitk, float* partials) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  if (epi == EPI_SWIGLU && (!bf16 || splitk > 1)) return hipErrorInvalidValue;
+  const bool half = dt != RP_F32;
+  if (epi == EPI_SWIGLU && (!half || splitk > 1)) return hipErrorInvalidValue;
   GemmArgs g;
   g.M = M;
   g.N = N;
@@ -576,27 +698,30 @@ hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K
   g.ldc = ldc;
   g.partials = partials;
   if (splitk < 1) splitk = 1;
-  const int bk = bf16 ? GB_K : GF_K;
+  const int bk = half ? GB_K : GF_K;
   const int kblocks = (K + bk - 1) / bk;
   if (splitk > kblocks) splitk = kblocks;
   g.k_chunk = ((kblocks + splitk - 1) / splitk) * bk;
   splitk = (K + g.k_chunk - 1) / g.k_chunk;
   const bool split = splitk > 1;
-  if (bf16) {
+  if (half) {
     g.tiles_m = (M + GB_M - 1) / GB_M;
     g.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB_N - 1) / GB_N;
     dim3 grid(g.tiles_m * g.tiles_n, splitk);
     const int64_t b_rows = epi == EPI_SWIGLU ? (int64_t)B.n1 + N : N;
-    if (split)
-      launch_bf16<-1>(s, g, grid, b_rows);
-    else if (epi == EPI_STORE)
-      launch_bf16<EPI_STORE>(s, g, grid, b_rows);
-    else if (epi == EPI_STORE_F32)
-      launch_bf16<EPI_STORE_F32>(s, g, grid, b_rows);
-    else if (epi == EPI_SWIGLU)
-      launch_bf16<EPI_SWIGLU>(s, g, grid, b_rows);
-    else
-      launch_bf16<EPI_ADD_F32>(s, g, grid, b_rows);
+    with_half16(dt, [&](auto tag_) {
+      using H = decltype(tag_);
+      if (split)
+        launch_half<-1, H>(s, g, grid, b_rows);
+      else if (epi == EPI_STORE)
+        launch_half<EPI_STORE, H>(s, g, grid, b_rows);
+      else if (epi == EPI_STORE_F32)
+        launch_half<EPI_STORE_F32, H>(s, g, grid, b_rows);
+      else if (epi == EPI_SWIGLU)
+        launch_half<EPI_SWIGLU, H>(s, g, grid, b_rows);
+      else
+        launch_half<EPI_ADD_F32, H>(s, g, grid, b_rows);
+    });
   } else {
     g.tiles_m = (M + GF_M - 1) / GF_M;
     g.tiles_n = (N + GF_N - 1) / GF_N;
@@ -612,8 +737,10 @@ hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K
   if (e != hipSuccess || !split) return e;
   const int64_t total = (int64_t)M * N;
   const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
-  if (epi == EPI_STORE && bf16)
+  if (epi == EPI_STORE && dt == RP_BF16)
     k_splitk_reduce<EPI_STORE, bf16_t><<<blocks, 256, 0, s>>>(partials, splitk, M, N, C, ldc);
+  else if (epi == EPI_STORE && dt == RP_F16)
+    k_splitk_reduce<EPI_STORE, f16_t><<<blocks, 256, 0, s>>>(partials, splitk, M, N, C, ldc);
   else if (epi == EPI_STORE || epi == EPI_STORE_F32)
     k_splitk_reduce<EPI_STORE_F32, float><<<blocks, 256, 0, s>>>(partials, splitk, M, N, C, ldc);
   else
@@ -640,7 +767,7 @@ hipError_t launch_gemm_variant(hipStream_t s, int variant, int32_t M, int32_t N,
   g.tiles_m = (M + GB_M - 1) / GB_M;
   g.tiles_n = (N + GB_N - 1) / GB_N;
   dim3 grid(g.tiles_m * g.tiles_n, 1);
-  launch_bf16<EPI_STORE>(s, g, grid, N, variant != 0);
+  launch_half<EPI_STORE, bf16_t>(s, g, grid, N, variant != 0);
   return hipGetLastError();
 }
 
