@@ -30,8 +30,14 @@
  *     (shape outside what the kernels implement) or RP_ERR_WORKSPACE
  *     (workspace too small).  A failed launch returns RP_ERR_HIP.  The text
  *     of the last non-OK status of the calling thread is rp_last_error().
- *   - Dtypes: weights, visual embeddings and KV share rp_config.dtype (fp32
- *     or bf16, row-major, nn.Linear layout [out, in] for projections).
+ *   - Dtypes: weights, visual embeddings and KV share rp_config.dtype (fp32,
+ *     bf16 or fp16; row-major, nn.Linear layout [out, in] for projections).
+ *     The 16-bit dtypes run the same kernels (MFMA with fp32 accumulation,
+ *     fp32 residual stream) and differ only in the storage rounding of
+ *     activations, K/V and weights: fp16 carries 3 more mantissa bits, so a
+ *     bf16-trained model whose weights convert to fp16 exactly (|w| within
+ *     fp16's normal range) computes its log-probabilities about 8x closer to
+ *     exact arithmetic at the same speed.
  *     h_last, hidden_out, logprobs and logits are always fp32.  Token ids are
  *     int32.  Length tables (cu_seqlens) are HOST int32 arrays.
  *   - Device-side data the host cannot see (token ids, kv_len) is clamped to
@@ -60,12 +66,13 @@ typedef enum {
   RP_ERR_HIP = 5
 } rp_status;
 
-typedef enum { RP_F32 = 0, RP_BF16 = 1 } rp_dtype;
+typedef enum { RP_F32 = 0, RP_BF16 = 1, RP_F16 = 2 } rp_dtype;
 
 /* Backbone hyper-parameters.  head_dim must be 64 or 128; n_q_heads a
  * multiple of n_kv_heads, at most 8 q heads per kv head (q head h reads kv head
  * h / (n_q_heads/n_kv_heads)).
- * For bf16, d_model, ffn_dim and n_q_heads*head_dim must be multiples of 64.
+ * For bf16 and fp16, d_model, ffn_dim and n_q_heads*head_dim must be
+ * multiples of 64.
  * rms_eps is the RMSNorm epsilon (1e-6 for the Qwen2 family); rope_theta the
  * RoPE base (1e6).  max_position bounds every position a call may use. */
 typedef struct {

@@ -17,7 +17,8 @@ from typing import Optional, Sequence
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "librollplex.so")
 
 RP_OK, RP_ERR_INVALID_ARG, RP_ERR_SHAPE, RP_ERR_UNSUPPORTED, RP_ERR_WORKSPACE, RP_ERR_HIP = range(6)
-RP_F32, RP_BF16 = 0, 1
+RP_F32, RP_BF16, RP_F16 = 0, 1, 2
+_DTYPES = {"f32": RP_F32, "bf16": RP_BF16, "f16": RP_F16}
 RP_MAX_SEQS = 256
 SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_forward",
            "rp_suffix_workspace_bytes", "rp_suffix_logprob", "rp_decode_workspace_bytes",
@@ -127,7 +128,7 @@ def _i32(seq: Optional[Sequence[int]]):
 def make_config(model, max_position: int) -> RpConfig:
     return RpConfig(model.n_layers, model.d_model, model.n_q_heads, model.n_kv_heads, model.head_dim,
                     model.ffn_dim, model.vocab, int(max_position), float(model.rms_eps),
-                    float(model.rope_theta), RP_BF16 if model.dtype == "bf16" else RP_F32)
+                    float(model.rope_theta), _DTYPES[model.dtype])
 
 
 def make_kv(k, v, layer_stride: int) -> RpKV:

@@ -23,7 +23,7 @@ class ModelShape:
     head_dim: int
     ffn_dim: int
     vocab: int
-    dtype: str                      # "f32" or "bf16": storage + compute type of weights/KV
+    dtype: str                      # "f32", "bf16" or "f16": storage type of weights/activations/KV
     rms_eps: float = 1e-6
     rope_theta: float = 1e6
 

@@ -83,7 +83,8 @@ bool prof_end(hipStream_t s, int slot) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-size_t elem_size(const rp_config& c) { return c.dtype == RP_BF16 ? 2 : 4; }
+size_t elem_size(const rp_config& c) { return c.dtype == RP_F32 ? 4 : 2; }
+bool half_dtype(const rp_config& c) { return c.dtype == RP_BF16 || c.dtype == RP_F16; }
 
 // Bump allocator over the caller's workspace (sizing pass when base == nullptr).
 struct Carver {
@@ -101,21 +102,22 @@ struct Carver {
 struct LayerWS {
   float* X;   // fp32 residual [M, d]
   void* N;    // normed activations [M, d]
-  void* QKV;  // [M, qkv]
+  float* QKV;  // fp32 projections [M, qkv]
+  void* Q;     // rotated queries [M, Hq*D]
   void* O;    // attention output [M, Hq*D]
   void* GU;   // [M, 2F]
   void* ACT;  // [M, F]
 };
 
 // bf16 prefix/suffix layers fuse SwiGLU into the gate/up GEMM and need no [M, 2F] buffer.
-bool fused_swiglu(const rp_config& cfg, bool split_gemms) { return cfg.dtype == RP_BF16 && !split_gemms; }
 
 void carve_layer(Carver& c, const rp_config& cfg, int64_t M, bool need_x, bool need_gu, LayerWS* w) {
   const size_t es = elem_size(cfg);
   const int64_t d = cfg.d_model, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
   w->X = need_x ? (float*)c.take(M * d * 4) : nullptr;
   w->N = c.take(M * d * es);
-  w->QKV = c.take(M * qkv * es);
+  w->QKV = (float*)c.take(M * qkv * 4);
+  w->Q = c.take(M * (int64_t)cfg.n_q_heads * cfg.head_dim * es);
   w->O = c.take(M * (int64_t)cfg.n_q_heads * cfg.head_dim * es);
   w->GU = need_gu ? c.take(M * 2 * (int64_t)cfg.ffn_dim * es) : nullptr;
   w->ACT = c.take(M * (int64_t)cfg.ffn_dim * es);
@@ -123,7 +125,8 @@ void carve_layer(Carver& c, const rp_config& cfg, int64_t M, bool need_x, bool n
 
 rp_status check_config(const rp_config* c) {
   if (!c) return fail(RP_ERR_INVALID_ARG, "config is NULL");
-  if (c->dtype != RP_F32 && c->dtype != RP_BF16) return fail(RP_ERR_INVALID_ARG, "bad dtype %d", (int)c->dtype);
+  if (c->dtype != RP_F32 && c->dtype != RP_BF16 && c->dtype != RP_F16)
+    return fail(RP_ERR_INVALID_ARG, "bad dtype %d", (int)c->dtype);
   if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn_dim < 1 ||
       c->vocab < 1 || c->max_position < 1)
     return fail(RP_ERR_SHAPE, "config sizes must be positive");
@@ -134,9 +137,8 @@ rp_status check_config(const rp_config* c) {
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(RP_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", c->head_dim);
   if (c->d_model % 8 || c->ffn_dim % 8) return fail(RP_ERR_UNSUPPORTED, "d_model and ffn_dim must be multiples of 8");
-  if (c->dtype == RP_BF16 &&
-      (c->d_model % 64 || c->ffn_dim % 64 || (c->n_q_heads * c->head_dim) % 64))
-    return fail(RP_ERR_UNSUPPORTED, "bf16 needs d_model, ffn_dim and n_q_heads*head_dim multiples of 64");
+  if (c->dtype != RP_F32 && (c->d_model % 64 || c->ffn_dim % 64 || (c->n_q_heads * c->head_dim) % 64))
+    return fail(RP_ERR_UNSUPPORTED, "16-bit dtypes need d_model, ffn_dim and n_q_heads*head_dim multiples of 64");
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.0)) return fail(RP_ERR_SHAPE, "rms_eps and rope_theta must be > 0");
   const int64_t qkv = (int64_t)(c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
   if (qkv > (1 << 30) || (int64_t)c->ffn_dim * 2 > (1 << 30)) return fail(RP_ERR_UNSUPPORTED, "dimension too large");
@@ -185,12 +187,62 @@ rp::SeqTable make_table(int32_t B, const int32_t* q_cu, const int32_t* k_cu) {
   return t;
 }
 
+// split-K factor for small-M GEMMs (decode): aim for >= 2 workgroups per CU.
+int decode_splitk(const rp_config& cfg, int32_t M, int32_t N, int32_t K) {
+  if (!half_dtype(cfg)) return 1;
+  const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  int s = (512 + tiles - 1) / tiles;
+  s = s < 1 ? 1 : s;
+  s = s > 8 ? 8 : s;
+  const int kb = K / 64;
+  return s > kb ? kb : s;
+}
+
+// Split-K plan of one decoder layer's GEMMs.
+//   prefix: no split (the prefix holds many rows; results are bitwise independent of how
+//           sequences are packed);
+//   suffix: GEMMs with fewer than 16384 output columns split K into min(8, K/1024) chunks,
+//           a factor that depends on the shapes of the weights only, so a row's result
+//           does not depend on how many other rows share the launch;
+//   decode: split to fill the chip for the batch at hand (decode_splitk).
+// Split GEMMs cannot fuse SwiGLU into their epilogue.
+enum class Pass { kPrefix, kSuffix, kDecode };
+struct LayerPlan {
+  int qkv = 1, o = 1, gu = 1, down = 1;
+  bool fused = false;
+  size_t part_floats = 0;
+};
+int suffix_splitk(const rp_config& cfg, int32_t N, int32_t K) {
+  if (!half_dtype(cfg) || N >= 16384) return 1;
+  int s = K / 1024;
+  return s < 1 ? 1 : s > 8 ? 8 : s;
+}
+LayerPlan plan_layer(const rp_config& c, int32_t M, Pass pass) {
+  const int d = c.d_model, F = c.ffn_dim, qkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const int hq = c.n_q_heads * c.head_dim;
+  auto f = [&](int N, int K) {
+    return pass == Pass::kPrefix ? 1 : pass == Pass::kSuffix ? suffix_splitk(c, N, K) : decode_splitk(c, M, N, K);
+  };
+  LayerPlan p;
+  p.qkv = f(qkv, d);
+  p.o = f(d, hq);
+  p.gu = f(2 * F, d);
+  p.down = f(d, F);
+  p.fused = half_dtype(c) && p.gu == 1;
+  const int64_t shapes[4][3] = {{qkv, p.qkv, 0}, {d, p.o, 0}, {2 * F, p.gu, 0}, {d, p.down, 0}};
+  for (auto& sh : shapes) {
+    const size_t fl = rp::gemm_partial_floats(M, (int32_t)sh[0], (int32_t)sh[1]);
+    p.part_floats = fl > p.part_floats ? fl : p.part_floats;
+  }
+  return p;
+}
+
 size_t prefix_ws(const rp_model* m, int64_t T, void* base, bool need_x, LayerWS* w, int32_t** vis_idx) {
   Carver c(base);
   int32_t* vi = (int32_t*)c.take(T * 4);
   if (vis_idx) *vis_idx = vi;
   LayerWS tmp;
-  carve_layer(c, m->cfg, T, need_x, !fused_swiglu(m->cfg, false), w ? w : &tmp);
+  carve_layer(c, m->cfg, T, need_x, !plan_layer(m->cfg, (int32_t)T, Pass::kPrefix).fused, w ? w : &tmp);
   return c.off + 256;
 }
 
@@ -199,29 +251,22 @@ struct SuffixWS {
   void* Ks;
   void* Vs;
   float* logits;
+  float* gemm_part;
+  LayerPlan plan;
 };
 
 size_t suffix_ws(const rp_model* m, int64_t R, void* base, SuffixWS* w) {
   Carver c(base);
   SuffixWS tmp;
   SuffixWS* s = w ? w : &tmp;
-  carve_layer(c, m->cfg, R, true, !fused_swiglu(m->cfg, false), &s->L);
+  s->plan = plan_layer(m->cfg, (int32_t)R, Pass::kSuffix);
+  carve_layer(c, m->cfg, R, true, !s->plan.fused, &s->L);
   const int64_t kvrow = (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim;
   s->Ks = c.take(R * kvrow * elem_size(m->cfg));
   s->Vs = c.take(R * kvrow * elem_size(m->cfg));
   s->logits = (float*)c.take(R * (int64_t)m->cfg.vocab * 4);
+  s->gemm_part = (float*)c.take(s->plan.part_floats * 4);
   return c.off + 256;
-}
-
-// split-K factor for small-M GEMMs (decode): aim for >= 2 workgroups per CU.
-int decode_splitk(const rp_config& cfg, int32_t M, int32_t N, int32_t K) {
-  if (cfg.dtype != RP_BF16) return 1;
-  const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
-  int s = (512 + tiles - 1) / tiles;
-  s = s < 1 ? 1 : s;
-  s = s > 8 ? 8 : s;
-  const int kb = K / 64;
-  return s > kb ? kb : s;
 }
 
 struct DecodeWS {
@@ -287,20 +332,19 @@ const LayerNames kSuffixNames = {"suffix.rmsnorm", "suffix.gemm_qkv", "suffix.ro
 
 rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, const rp::SeqTable& st,
                     int32_t M, const LayerWS& w, void* k_out, void* v_out, const void* k0, const void* v0,
-                    int splitk_ok, float* gemm_part, const LayerNames& nm) {
+                    const LayerPlan& plan, float* gemm_part, const LayerNames& nm) {
   const rp_config& c = m->cfg;
-  const bool bf = c.dtype == RP_BF16;
+  const rp_dtype dt = c.dtype;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
-  auto sk = [&](int N, int K) { return splitk_ok ? decode_splitk(c, M, N, K) : 1; };
-  RP_TRY_LAUNCH_N(nm.norm1, rp::launch_rmsnorm(s, bf, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
+  RP_TRY_LAUNCH_N(nm.norm1, rp::launch_rmsnorm(s, dt, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
-  RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, bf, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE, sk(qkv, d), gemm_part));
-  RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv(s, bf, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position,
+  RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE_F32, plan.qkv, gemm_part));
+  RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv(s, dt, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position, w.Q,
                                    k_out, v_out));
   rp::AttnArgs a;
-  a.q = w.QKV;
-  a.q_ld = qkv;
+  a.q = w.Q;
+  a.q_ld = hq;
   a.k0 = k0;
   a.v0 = v0;
   a.k1 = k_out;
@@ -310,20 +354,20 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   a.Hkv = Hkv;
   a.D = D;
   a.scale = (float)(1.0 / sqrt((double)D));
-  RP_TRY_LAUNCH_N(nm.attn, rp::launch_attention(s, bf, st, a, M));
+  RP_TRY_LAUNCH_N(nm.attn, rp::launch_attention(s, dt, st, a, M));
   rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
-  RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, bf, M, d, hq, w.O, hq, bo, hq, w.X, d, rp::EPI_ADD_F32, sk(d, hq), gemm_part));
-  RP_TRY_LAUNCH_N(nm.norm2, rp::launch_rmsnorm(s, bf, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
+  RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, dt, M, d, hq, w.O, hq, bo, hq, w.X, d, rp::EPI_ADD_F32, plan.o, gemm_part));
+  RP_TRY_LAUNCH_N(nm.norm2, rp::launch_rmsnorm(s, dt, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
-  if (fused_swiglu(c, splitk_ok)) {
-    RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, bf, M, F, d, w.N, d, bgu, d, w.ACT, F, rp::EPI_SWIGLU, 1, nullptr));
+  if (plan.fused) {
+    RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, dt, M, F, d, w.N, d, bgu, d, w.ACT, F, rp::EPI_SWIGLU, 1, nullptr));
   } else {
-    RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, bf, M, 2 * F, d, w.N, d, bgu, d, w.GU, 2 * F, rp::EPI_STORE,
-                                                sk(2 * F, d), gemm_part));
-    RP_TRY_LAUNCH_N(nm.swiglu, rp::launch_swiglu(s, bf, w.GU, M, F, w.ACT));
+    RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, dt, M, 2 * F, d, w.N, d, bgu, d, w.GU, 2 * F, rp::EPI_STORE,
+                                                plan.gu, gemm_part));
+    RP_TRY_LAUNCH_N(nm.swiglu, rp::launch_swiglu(s, dt, w.GU, M, F, w.ACT));
   }
   rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
-  RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, bf, M, d, F, w.ACT, F, bd, F, w.X, d, rp::EPI_ADD_F32, sk(d, F), gemm_part));
+  RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, dt, M, d, F, w.ACT, F, bd, F, w.X, d, rp::EPI_ADD_F32, plan.down, gemm_part));
   return RP_OK;
 }
 
@@ -354,7 +398,6 @@ rp_status rp_create(const rp_config* cfg, const rp_weights* w, rp_model** out) {
   if (st != RP_OK) return st;
   if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers)
     return fail(RP_ERR_INVALID_ARG, "weights: embed, final_norm, lm_head and layers are required");
-  const bool bf = cfg->dtype == RP_BF16;
   for (int l = 0; l < cfg->n_layers; ++l) {
     const rp_layer_weights& lw = w->layers[l];
     const void* req[] = {lw.attn_norm, lw.wq, lw.wk, lw.wv, lw.wo, lw.mlp_norm, lw.w_gate, lw.w_up, lw.w_down};
@@ -365,7 +408,6 @@ rp_status rp_create(const rp_config* cfg, const rp_weights* w, rp_model** out) {
   }
   if (!aligned16(w->embed) || !aligned16(w->lm_head) || !aligned16(w->final_norm))
     return fail(RP_ERR_INVALID_ARG, "embed/lm_head/final_norm must be 16-byte aligned");
-  (void)bf;
   rp_model* m = new rp_model;
   m->cfg = *cfg;
   m->embed = w->embed;
@@ -408,20 +450,21 @@ rp_status rp_prefix_forward(const rp_model* m, void* stream, int32_t B, const in
 
   hipStream_t s = (hipStream_t)stream;
   const rp_config& c = m->cfg;
-  const bool bf = c.dtype == RP_BF16;
+  const rp_dtype dt = c.dtype;
   LayerWS w;
   int32_t* vis_idx = nullptr;
   prefix_ws(m, T, ws, hidden_out == nullptr, &w, &vis_idx);
   if (hidden_out) w.X = hidden_out;
   const rp::SeqTable tab = make_table(B, cu, nullptr);
+  const LayerPlan plan = plan_layer(c, (int32_t)T, Pass::kPrefix);
 
   RP_TRY_LAUNCH_N("prefix.visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
-  RP_TRY_LAUNCH_N("prefix.embed", rp::launch_embed(s, bf, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
+  RP_TRY_LAUNCH_N("prefix.embed", rp::launch_embed(s, dt, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
                                  c.d_model, w.X));
   for (int l = 0; l < c.n_layers; ++l) {
     void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
     void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, 0, nullptr, kPrefixNames);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames);
     if (st != RP_OK) return st;
   }
   RP_TRY_LAUNCH_N("prefix.gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
@@ -454,21 +497,21 @@ rp_status rp_suffix_logprob(const rp_model* m, void* stream, int32_t B, const in
 
   hipStream_t s = (hipStream_t)stream;
   const rp_config& c = m->cfg;
-  const bool bf = c.dtype == RP_BF16;
+  const rp_dtype dt = c.dtype;
   SuffixWS w;
   suffix_ws(m, R, ws, &w);
   const rp::SeqTable tab = make_table(B, scu, pcu);
-  RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, bf, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
+  RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, dt, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
   for (int l = 0; l < c.n_layers; ++l) {
     const void* kl = layer_ptr(m, kv.k, kv.layer_stride, l);
     const void* vl = layer_ptr(m, kv.v, kv.layer_stride, l);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, 0, nullptr, kSuffixNames);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, w.plan, w.gemm_part, kSuffixNames);
     if (st != RP_OK) return st;
   }
-  RP_TRY_LAUNCH_N("suffix.final_norm", rp::launch_final_norm_rows(s, bf, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
+  RP_TRY_LAUNCH_N("suffix.final_norm", rp::launch_final_norm_rows(s, dt, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
                                            c.d_model, w.L.N));
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
-  RP_TRY_LAUNCH_N("suffix.gemm_lm_head", rp::launch_gemm(s, bf, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
+  RP_TRY_LAUNCH_N("suffix.gemm_lm_head", rp::launch_gemm(s, dt, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
                                 c.vocab, rp::EPI_STORE_F32, 1, nullptr));
   RP_TRY_LAUNCH_N("suffix.logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
   return RP_OK;
@@ -494,41 +537,41 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
 
   hipStream_t s = (hipStream_t)stream;
   const rp_config& c = m->cfg;
-  const bool bf = c.dtype == RP_BF16;
+  const rp_dtype dt = c.dtype;
   DecodeWS w;
   decode_ws(m, B, cap, ws, &w);
   float* lg = logits ? logits : w.logits;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
   const float scale = (float)(1.0 / sqrt((double)D));
-  RP_TRY_LAUNCH_N("decode.embed", rp::launch_decode_embed(s, bf, token_ids, m->embed, c.vocab, B, d, w.L.X));
+  RP_TRY_LAUNCH_N("decode.embed", rp::launch_decode_embed(s, dt, token_ids, m->embed, c.vocab, B, d, w.L.X));
   for (int l = 0; l < c.n_layers; ++l) {
     const rp_layer_weights& lw = m->layers[l];
     void* kl = layer_ptr(m, cache.k, cache.layer_stride, l);
     void* vl = layer_ptr(m, cache.v, cache.layer_stride, l);
-    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.attn_norm, c.rms_eps, B, d, w.L.N));
+    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, dt, w.L.X, lw.attn_norm, c.rms_eps, B, d, w.L.N));
     rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
-    RP_TRY_LAUNCH_N("decode.gemm_qkv", rp::launch_gemm(s, bf, B, qkv, d, w.L.N, d, bqkv, d, w.L.QKV, qkv, rp::EPI_STORE,
+    RP_TRY_LAUNCH_N("decode.gemm_qkv", rp::launch_gemm(s, dt, B, qkv, d, w.L.N, d, bqkv, d, w.L.QKV, qkv, rp::EPI_STORE_F32,
                                   decode_splitk(c, B, qkv, d), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode.rope_kv", rp::launch_decode_rope_kv(s, bf, w.L.QKV, B, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, kv_len, cap,
-                                            c.max_position, kl, vl));
-    RP_TRY_LAUNCH_N("decode.attention", rp::launch_decode_attention(s, bf, w.L.QKV, qkv, kl, vl, kv_len, cap, c.max_position, B, Hq, Hkv,
+    RP_TRY_LAUNCH_N("decode.rope_kv", rp::launch_decode_rope_kv(s, dt, w.L.QKV, B, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, kv_len, cap,
+                                            c.max_position, w.L.Q, kl, vl));
+    RP_TRY_LAUNCH_N("decode.attention", rp::launch_decode_attention(s, dt, w.L.Q, hq, kl, vl, kv_len, cap, c.max_position, B, Hq, Hkv,
                                               D, scale, w.attn_part, w.L.O));
     rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
-    RP_TRY_LAUNCH_N("decode.gemm_o_proj", rp::launch_gemm(s, bf, B, d, hq, w.L.O, hq, bo, hq, w.L.X, d, rp::EPI_ADD_F32,
+    RP_TRY_LAUNCH_N("decode.gemm_o_proj", rp::launch_gemm(s, dt, B, d, hq, w.L.O, hq, bo, hq, w.L.X, d, rp::EPI_ADD_F32,
                                   decode_splitk(c, B, d, hq), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, bf, w.L.X, lw.mlp_norm, c.rms_eps, B, d, w.L.N));
+    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, dt, w.L.X, lw.mlp_norm, c.rms_eps, B, d, w.L.N));
     rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
-    RP_TRY_LAUNCH_N("decode.gemm_gate_up", rp::launch_gemm(s, bf, B, 2 * F, d, w.L.N, d, bgu, d, w.L.GU, 2 * F, rp::EPI_STORE,
+    RP_TRY_LAUNCH_N("decode.gemm_gate_up", rp::launch_gemm(s, dt, B, 2 * F, d, w.L.N, d, bgu, d, w.L.GU, 2 * F, rp::EPI_STORE,
                                   decode_splitk(c, B, 2 * F, d), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode.swiglu", rp::launch_swiglu(s, bf, w.L.GU, B, F, w.L.ACT));
+    RP_TRY_LAUNCH_N("decode.swiglu", rp::launch_swiglu(s, dt, w.L.GU, B, F, w.L.ACT));
     rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
-    RP_TRY_LAUNCH_N("decode.gemm_down", rp::launch_gemm(s, bf, B, d, F, w.L.ACT, F, bd, F, w.L.X, d, rp::EPI_ADD_F32,
+    RP_TRY_LAUNCH_N("decode.gemm_down", rp::launch_gemm(s, dt, B, d, F, w.L.ACT, F, bd, F, w.L.X, d, rp::EPI_ADD_F32,
                                   decode_splitk(c, B, d, F), w.gemm_part));
   }
-  RP_TRY_LAUNCH_N("decode.final_norm", rp::launch_rmsnorm(s, bf, w.L.X, m->final_norm, c.rms_eps, B, d, w.L.N));
+  RP_TRY_LAUNCH_N("decode.final_norm", rp::launch_rmsnorm(s, dt, w.L.X, m->final_norm, c.rms_eps, B, d, w.L.N));
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
-  RP_TRY_LAUNCH_N("decode.gemm_lm_head", rp::launch_gemm(s, bf, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
+  RP_TRY_LAUNCH_N("decode.gemm_lm_head", rp::launch_gemm(s, dt, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
                                 decode_splitk(c, B, c.vocab, d), w.gemm_part));
   RP_TRY_LAUNCH_N("decode.argmax", rp::launch_argmax(s, lg, B, c.vocab, next_ids));
   return RP_OK;

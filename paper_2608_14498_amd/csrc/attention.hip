@@ -68,9 +68,11 @@ template <int D>
 __device__ __forceinline__ int kswz(int key) { return D == 128 ? (key & 15) : (key & 7); }
 __device__ __forceinline__ int vswz(int key) { return (key & 3) << 1; }
 
-template <int D, int QW, int KT>
+template <typename T16, int D, int QW, int KT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QW == 1 ? 2 : 1, QW == 1 ? 2 : 1)))
 void k_attn_bf16(SeqTable st, AttnArgs a) {
+  typedef Half16<T16> H;
+  typedef typename H::V8 V8;
   constexpr int BQ = 4 * 32 * QW;
   constexpr int CH = D / 8;              // 16-byte chunks per K/V row
   constexpr int KSTEPS = D / 16;         // MFMA k-steps of S^T (over Dh)
@@ -93,24 +95,24 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   const int nk = qpos_last + 1;  // keys needed by this block
   const int ntiles = (nk + KT - 1) / KT;
   const int64_t kv_ld = (int64_t)a.Hkv * D;
-  const bf16_t* k0 = (const bf16_t*)a.k0 + (int64_t)g * D;
-  const bf16_t* v0 = (const bf16_t*)a.v0 + (int64_t)g * D;
-  const bf16_t* k1 = (const bf16_t*)a.k1 + (int64_t)g * D;
-  const bf16_t* v1 = (const bf16_t*)a.v1 + (int64_t)g * D;
+  const T16* k0 = (const T16*)a.k0 + (int64_t)g * D;
+  const T16* v0 = (const T16*)a.v0 + (int64_t)g * D;
+  const T16* k1 = (const T16*)a.k1 + (int64_t)g * D;
+  const T16* v1 = (const T16*)a.v1 + (int64_t)g * D;
   const int krow0 = st.k_cu[b], qrow0 = st.q_cu[b];
 
   // ---- queries of this lane: column (lane & 31) of each 32-query block ----
   const int fr = lane & 31, fk = lane >> 5;
-  bf16x8_t qf[QW][KSTEPS];
+  V8 qf[QW][KSTEPS];
   int qpos[QW];
 #pragma unroll
   for (int qi = 0; qi < QW; ++qi) {
     const int qrow_raw = qb.q_begin + (wave * QW + qi) * 32 + fr;
     const int qrow = min(qrow_raw, qb.q_end - 1);
     qpos[qi] = n0 + (qrow_raw - qrow0);
-    const bf16_t* qp = (const bf16_t*)a.q + (int64_t)qrow * a.q_ld + h * D + fk * 8;
+    const T16* qp = (const T16*)a.q + (int64_t)qrow * a.q_ld + h * D + fk * 8;
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) qf[qi][ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + ks * 16));
+    for (int ks = 0; ks < KSTEPS; ++ks) qf[qi][ks] = H::as_v8(*reinterpret_cast<const uint4*>(qp + ks * 16));
   }
 
   // ---- tile loader: chunk id = i*256 + tid -> (key = id / CH, c = id % CH) ----
@@ -170,10 +172,10 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         const int key = kb * 32 + fr;
-        const bf16x8_t kf = as_bf16x8(Ks[buf][key * CH + ((ks * 2 + fk) ^ kswz<D>(key))]);
+        const V8 kf = H::as_v8(Ks[buf][key * CH + ((ks * 2 + fk) ^ kswz<D>(key))]);
 #pragma unroll
         for (int qi = 0; qi < QW; ++qi)
-          s[qi][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qi][ks], s[qi][kb], 0, 0, 0);
+          s[qi][kb] = H::mma(kf, qf[qi][ks], s[qi][kb]);
       }
     }
 
@@ -213,19 +215,17 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
     }
 
     // ---- O^T += V^T P^T over the sixteen-key steps (kb, hh) ----
-    const bf16_t* vbase = reinterpret_cast<const bf16_t*>(&Vs[buf][0]);
+    const T16* vbase = reinterpret_cast<const T16*>(&Vs[buf][0]);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        bf16x8_t pf[QW];
+        V8 pf[QW];
 #pragma unroll
         for (int qi = 0; qi < QW; ++qi) {
           const f32x16_t& sv = s[qi][kb];
-          pf[qi] = as_bf16x8(make_uint4(pack_bf2(sv[hh * 8 + 0], sv[hh * 8 + 1]),
-                                        pack_bf2(sv[hh * 8 + 2], sv[hh * 8 + 3]),
-                                        pack_bf2(sv[hh * 8 + 4], sv[hh * 8 + 5]),
-                                        pack_bf2(sv[hh * 8 + 6], sv[hh * 8 + 7])));
+          pf[qi] = H::as_v8(make_uint4(H::pack2(sv[hh * 8 + 0], sv[hh * 8 + 1]), H::pack2(sv[hh * 8 + 2], sv[hh * 8 + 3]),
+                                       H::pack2(sv[hh * 8 + 4], sv[hh * 8 + 5]), H::pack2(sv[hh * 8 + 6], sv[hh * 8 + 7])));
         }
         const int ka = kb * 32 + hh * 16 + tr_key, kc = ka + 8;
 #pragma unroll
@@ -236,10 +236,9 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
           const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + ka * D + ca));
           const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + kc * D + cc));
           const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
-          const bf16x8_t vf = as_bf16x8(make_uint4(l2.x, l2.y, h2.x, h2.y));
+          const V8 vf = H::as_v8(make_uint4(l2.x, l2.y, h2.x, h2.y));
 #pragma unroll
-          for (int qi = 0; qi < QW; ++qi)
-            o[qi][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qi], o[qi][db], 0, 0, 0);
+          for (int qi = 0; qi < QW; ++qi) o[qi][db] = H::mma(vf, pf[qi], o[qi][db]);
         }
       }
     }
@@ -259,15 +258,15 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
     const float l = l_run[qi] + __shfl_xor(l_run[qi], 32, kWave);
     if (qrow >= qb.q_end) continue;
     const float inv = 1.0f / l;
-    bf16_t* op = (bf16_t*)a.o + (int64_t)qrow * a.Hq * D + h * D;
+    T16* op = (T16*)a.o + (int64_t)qrow * a.Hq * D + h * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int e4 = 0; e4 < 4; ++e4) {
         const int dh = db * 32 + 8 * e4 + 4 * fk;
         uint2 w;
-        w.x = pack_bf2(o[qi][db][4 * e4] * inv, o[qi][db][4 * e4 + 1] * inv);
-        w.y = pack_bf2(o[qi][db][4 * e4 + 2] * inv, o[qi][db][4 * e4 + 3] * inv);
+        w.x = H::pack2(o[qi][db][4 * e4] * inv, o[qi][db][4 * e4 + 1] * inv);
+        w.y = H::pack2(o[qi][db][4 * e4 + 2] * inv, o[qi][db][4 * e4 + 3] * inv);
         *reinterpret_cast<uint2*>(op + dh) = w;
       }
   }
@@ -344,19 +343,22 @@ int count_qblocks(const SeqTable& st, int BQ) {
 // 1: 64 queries/wave x 32-key tiles).
 hipError_t launch_attention_variant(hipStream_t s, int variant, const SeqTable& st, const AttnArgs& a) {
   if (variant == 0)
-    k_attn_bf16<128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+    k_attn_bf16<bf16_t, 128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
   else
-    k_attn_bf16<128, 2, 32><<<count_qblocks(st, 256) * a.Hq, 256, 0, s>>>(st, a);
+    k_attn_bf16<bf16_t, 128, 2, 32><<<count_qblocks(st, 256) * a.Hq, 256, 0, s>>>(st, a);
   return hipGetLastError();
 }
 
-hipError_t launch_attention(hipStream_t s, bool bf16, const SeqTable& st, const AttnArgs& a, int32_t total_q) {
+hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, const AttnArgs& a, int32_t total_q) {
   if (total_q <= 0) return hipSuccess;
-  if (bf16) {
-    if (a.D == 128)
-      k_attn_bf16<128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
-    else
-      k_attn_bf16<64, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+  if (dt != RP_F32) {
+    with_half16(dt, [&](auto tag_) {
+      using H = decltype(tag_);
+      if (a.D == 128)
+        k_attn_bf16<H, 128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+      else
+        k_attn_bf16<H, 64, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+    });
   } else {
     const int nqb = count_qblocks(st, 64);
     if (a.D == 128)
@@ -544,7 +546,7 @@ size_t decode_attn_partial_floats(int32_t B, int32_t Hq, int32_t D, int32_t cap)
   return (size_t)B * Hq * nchunks * (D + 2);
 }
 
-hipError_t launch_decode_attention(hipStream_t s, bool bf16, const void* q, int32_t q_ld,
+hipError_t launch_decode_attention(hipStream_t s, rp_dtype dt, const void* q, int32_t q_ld,
                                    const void* cache_k, const void* cache_v, const int32_t* kv_len,
                                    int32_t cap, int32_t max_pos, int32_t B, int32_t Hq, int32_t Hkv,
                                    int32_t D, float scale, float* partials, void* o) {
@@ -555,11 +557,10 @@ hipError_t launch_decode_attention(hipStream_t s, bool bf16, const void* q, int3
                                                  (const T*)cache_v, kv_len, cap, max_pos, Hq, Hkv, \
                                                  scale, nchunks, partials);                    \
   k_decode_attn_merge<T, DD><<<B * Hq, DD, 0, s>>>(partials, nchunks, Hq, (T*)o);
-  if (bf16) {
-    if (D == 128) { RP_DEC(bf16_t, 128) } else { RP_DEC(bf16_t, 64) }
-  } else {
-    if (D == 128) { RP_DEC(float, 128) } else { RP_DEC(float, 64) }
-  }
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    if (D == 128) { RP_DEC(E, 128) } else { RP_DEC(E, 64) }
+  });
 #undef RP_DEC
   return hipGetLastError();
 }

@@ -1,5 +1,5 @@
-// Device helpers shared by the gfx950 kernels: bf16 storage, vector types,
-// wavefront (64-lane) reductions, XCD-aware block remapping.
+// Device helpers shared by the gfx950 kernels: 16-bit storage types (bf16, fp16),
+// vector types, wavefront (64-lane) reductions, XCD-aware block remapping.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -8,9 +8,31 @@
 namespace rp {
 
 typedef uint16_t bf16_t;  // raw bfloat16 bits
+typedef _Float16 f16_t;   // IEEE binary16
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Host-side dispatch on the storage type of a model: calls f(T()) with T = float,
+// bf16_t or f16_t for RP_F32, RP_BF16 and RP_F16.
+template <class F>
+inline void with_storage(int dtype, F&& f) {
+  if (dtype == 1)
+    f(bf16_t());
+  else if (dtype == 2)
+    f(f16_t());
+  else
+    f(float());
+}
+// The same over the two 16-bit types only (MFMA kernels).
+template <class F>
+inline void with_half16(int dtype, F&& f) {
+  if (dtype == 2)
+    f(f16_t());
+  else
+    f(bf16_t());
+}
 
 constexpr int kWave = 64;
 constexpr int kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin
@@ -32,11 +54,47 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
   return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
 }
 
+// float -> fp16, round to nearest even (the conversion instruction's default mode);
+// pack two into one word (lo in bits 0..15).
+__device__ __forceinline__ f16_t f2h(float f) { return (f16_t)f; }
+__device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, f2h(lo)) | ((uint32_t)__builtin_bit_cast(uint16_t, f2h(hi)) << 16);
+}
+__device__ __forceinline__ float h2f_bits(uint32_t bits16) {
+  return (float)__builtin_bit_cast(f16_t, (uint16_t)bits16);
+}
+
 // Generic scalar load/store of a storage element as float.
 __device__ __forceinline__ float ldf(const float* p) { return *p; }
 __device__ __forceinline__ float ldf(const bf16_t* p) { return bf2f(*p); }
+__device__ __forceinline__ float ldf(const f16_t* p) { return (float)*p; }
 __device__ __forceinline__ void stf(float* p, float v) { *p = v; }
 __device__ __forceinline__ void stf(bf16_t* p, float v) { *p = f2bf(v); }
+__device__ __forceinline__ void stf(f16_t* p, float v) { *p = f2h(v); }
+
+// The two 16-bit storage types of the MFMA paths: operand vector type, the 32x32x16
+// MFMA with fp32 accumulation, and float -> storage packing.
+template <typename T16> struct Half16;
+template <> struct Half16<bf16_t> {
+  typedef bf16x8_t V8;
+  static __device__ __forceinline__ V8 as_v8(uint4 v) { return __builtin_bit_cast(V8, v); }
+  static __device__ __forceinline__ f32x16_t mma(V8 a, V8 b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ uint32_t pack2(float lo, float hi) { return pack_bf2(lo, hi); }
+  static __device__ __forceinline__ float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
+  static __device__ __forceinline__ float hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+};
+template <> struct Half16<f16_t> {
+  typedef f16x8_t V8;
+  static __device__ __forceinline__ V8 as_v8(uint4 v) { return __builtin_bit_cast(V8, v); }
+  static __device__ __forceinline__ f32x16_t mma(V8 a, V8 b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ uint32_t pack2(float lo, float hi) { return pack_h2(lo, hi); }
+  static __device__ __forceinline__ float lo_f(uint32_t w) { return h2f_bits(w & 0xffffu); }
+  static __device__ __forceinline__ float hi_f(uint32_t w) { return h2f_bits(w >> 16); }
+};
 
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
@@ -100,13 +158,34 @@ __device__ __forceinline__ void load8(const bf16_t* p, float* v) {
     v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
 }
-// Raw 8-element chunks (bf16: one 16-byte load; fp32: two), loaded first and widened later.
+__device__ __forceinline__ void load8(const f16_t* p, float* v) {
+  uint4 u = *reinterpret_cast<const uint4*>(p);
+  uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = h2f_bits(w[i] & 0xffffu);
+    v[2 * i + 1] = h2f_bits(w[i] >> 16);
+  }
+}
+// Raw 8-element chunks (16-bit types: one 16-byte load; fp32: two), loaded first and
+// widened later.
 struct Raw8b { uint4 a; };
+struct Raw8h { uint4 a; };
 struct Raw8f { uint4 a, b; };
 template <typename T> struct Raw8;
 template <> struct Raw8<bf16_t> { typedef Raw8b type; };
+template <> struct Raw8<f16_t> { typedef Raw8h type; };
 template <> struct Raw8<float> { typedef Raw8f type; };
 __device__ __forceinline__ Raw8b ld_raw8(const bf16_t* p) { return Raw8b{*reinterpret_cast<const uint4*>(p)}; }
+__device__ __forceinline__ Raw8h ld_raw8(const f16_t* p) { return Raw8h{*reinterpret_cast<const uint4*>(p)}; }
+__device__ __forceinline__ void unpack8(const Raw8h& c, float* v) {
+  const uint32_t w[4] = {c.a.x, c.a.y, c.a.z, c.a.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = h2f_bits(w[i] & 0xffffu);
+    v[2 * i + 1] = h2f_bits(w[i] >> 16);
+  }
+}
 __device__ __forceinline__ Raw8f ld_raw8(const float* p) {
   return Raw8f{*reinterpret_cast<const uint4*>(p), *reinterpret_cast<const uint4*>(p + 4)};
 }
@@ -136,6 +215,14 @@ __device__ __forceinline__ void store8(bf16_t* p, const float* v) {
   u.y = pack_bf2(v[2], v[3]);
   u.z = pack_bf2(v[4], v[5]);
   u.w = pack_bf2(v[6], v[7]);
+  *reinterpret_cast<uint4*>(p) = u;
+}
+__device__ __forceinline__ void store8(f16_t* p, const float* v) {
+  uint4 u;
+  u.x = pack_h2(v[0], v[1]);
+  u.y = pack_h2(v[2], v[3]);
+  u.z = pack_h2(v[4], v[5]);
+  u.w = pack_h2(v[6], v[7]);
   *reinterpret_cast<uint4*>(p) = u;
 }
 __device__ __forceinline__ void store8(float* p, const float* v) {

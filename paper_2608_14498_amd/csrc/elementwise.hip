@@ -62,16 +62,15 @@ __global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ ids,
   }
 }
 
-hipError_t launch_embed(hipStream_t s, bool bf16, const int32_t* ids, const int32_t* vis_idx,
+hipError_t launch_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const int32_t* vis_idx,
                         const void* visual, int64_t n_visual, const void* embed, int32_t vocab,
                         int32_t T, int32_t d, float* X) {
   if (T <= 0) return hipSuccess;
-  if (bf16)
-    k_embed<bf16_t><<<T, 256, 0, s>>>(ids, vis_idx, (const bf16_t*)visual, n_visual,
-                                      (const bf16_t*)embed, vocab, d, X);
-  else
-    k_embed<float><<<T, 256, 0, s>>>(ids, vis_idx, (const float*)visual, n_visual,
-                                     (const float*)embed, vocab, d, X);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_embed<E><<<T, 256, 0, s>>>(ids, vis_idx, (const E*)visual, n_visual,
+                                      (const E*)embed, vocab, d, X);
+  });
   return hipGetLastError();
 }
 
@@ -88,12 +87,12 @@ __global__ __launch_bounds__(256) void k_decode_embed(const int32_t* __restrict_
   }
 }
 
-hipError_t launch_decode_embed(hipStream_t s, bool bf16, const int32_t* ids, const void* embed,
+hipError_t launch_decode_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const void* embed,
                                int32_t vocab, int32_t B, int32_t d, float* X) {
-  if (bf16)
-    k_decode_embed<bf16_t><<<B, 256, 0, s>>>(ids, (const bf16_t*)embed, vocab, d, X);
-  else
-    k_decode_embed<float><<<B, 256, 0, s>>>(ids, (const float*)embed, vocab, d, X);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_decode_embed<E><<<B, 256, 0, s>>>(ids, (const E*)embed, vocab, d, X);
+  });
   return hipGetLastError();
 }
 
@@ -130,13 +129,13 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ X, co
   rmsnorm_row(X + r * d, w, eps, d, out + r * d, red);
 }
 
-hipError_t launch_rmsnorm(hipStream_t s, bool bf16, const float* X, const void* w, float eps, int32_t M,
+hipError_t launch_rmsnorm(hipStream_t s, rp_dtype dt, const float* X, const void* w, float eps, int32_t M,
                           int32_t d, void* out) {
   if (M <= 0) return hipSuccess;
-  if (bf16)
-    k_rmsnorm<bf16_t><<<M, 256, 0, s>>>(X, (const bf16_t*)w, eps, d, (bf16_t*)out);
-  else
-    k_rmsnorm<float><<<M, 256, 0, s>>>(X, (const float*)w, eps, d, (float*)out);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_rmsnorm<E><<<M, 256, 0, s>>>(X, (const E*)w, eps, d, (E*)out);
+  });
   return hipGetLastError();
 }
 
@@ -152,25 +151,27 @@ __global__ __launch_bounds__(256) void k_final_norm_rows(SeqTable st, const floa
   rmsnorm_row(src, w, eps, d, out + (int64_t)r * d, red);
 }
 
-hipError_t launch_final_norm_rows(hipStream_t s, bool bf16, const SeqTable& st, const float* Y,
+hipError_t launch_final_norm_rows(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* Y,
                                   const float* h_last, const void* w, float eps, int32_t R, int32_t d,
                                   void* out) {
   if (R <= 0) return hipSuccess;
-  if (bf16)
-    k_final_norm_rows<bf16_t><<<R, 256, 0, s>>>(st, Y, h_last, (const bf16_t*)w, eps, d, (bf16_t*)out);
-  else
-    k_final_norm_rows<float><<<R, 256, 0, s>>>(st, Y, h_last, (const float*)w, eps, d, (float*)out);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_final_norm_rows<E><<<R, 256, 0, s>>>(st, Y, h_last, (const E*)w, eps, d, (E*)out);
+  });
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------------
-// RoPE (rotate-half pairs (i, i+D/2)) + optional q/k/v bias + KV materialisation.
-// q is rotated in place inside the qkv rows; k (rotated) and v go to k_out/v_out.
+// RoPE (rotate-half pairs (i, i+D/2)) + optional q/k/v bias + Q/K/V materialisation.
+// The projection row arrives in fp32 (the GEMM accumulator); bias, rotation and the
+// single rounding to the storage type happen here.  q (rotated) goes to q_dst, k
+// (rotated) and v to k_dst / v_dst.
 // ------------------------------------------------------------------------------------
 template <typename T>
-__device__ __forceinline__ void rope_row(T* __restrict__ row, int pos, int Hq, int Hkv, int D,
+__device__ __forceinline__ void rope_row(const float* __restrict__ row, int pos, int Hq, int Hkv, int D,
                                          const T* __restrict__ bq, const T* __restrict__ bk,
-                                         const T* __restrict__ bv, const RopeFreq& rf,
+                                         const T* __restrict__ bv, const RopeFreq& rf, T* __restrict__ q_dst,
                                          T* __restrict__ k_dst, T* __restrict__ v_dst, float* cs) {
   const int half = D >> 1;
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
@@ -186,7 +187,7 @@ __device__ __forceinline__ void rope_row(T* __restrict__ row, int pos, int Hq, i
     const int pp = isq ? p : p - nq;
     const int h = pp / half, i = pp - h * half;
     const int col = (isq ? 0 : Hq * D) + h * D + i;
-    float x1 = ldf(row + col), x2 = ldf(row + col + half);
+    float x1 = row[col], x2 = row[col + half];
     const T* b = isq ? bq : bk;
     if (b) {
       x1 += ldf(b + h * D + i);
@@ -195,8 +196,8 @@ __device__ __forceinline__ void rope_row(T* __restrict__ row, int pos, int Hq, i
     const float c = cs[i], s = cs[64 + i];
     const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
     if (isq) {
-      stf(row + col, y1);
-      stf(row + col + half, y2);
+      stf(q_dst + h * D + i, y1);
+      stf(q_dst + h * D + i + half, y2);
     } else {
       stf(k_dst + h * D + i, y1);
       stf(k_dst + h * D + i + half, y2);
@@ -204,69 +205,66 @@ __device__ __forceinline__ void rope_row(T* __restrict__ row, int pos, int Hq, i
   }
   const int vbase = (Hq + Hkv) * D;
   for (int e = threadIdx.x; e < Hkv * D; e += blockDim.x) {
-    float v = ldf(row + vbase + e);
+    float v = row[vbase + e];
     if (bv) v += ldf(bv + e);
     stf(v_dst + e, v);
   }
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_rope_kv(SeqTable st, T* __restrict__ qkv, int Hq, int Hkv, int D,
-                                                 const T* __restrict__ bq, const T* __restrict__ bk,
+__global__ __launch_bounds__(256) void k_rope_kv(SeqTable st, const float* __restrict__ qkv, int Hq, int Hkv,
+                                                 int D, const T* __restrict__ bq, const T* __restrict__ bk,
                                                  const T* __restrict__ bv, RopeFreq rf, int max_pos,
-                                                 T* __restrict__ k_out, T* __restrict__ v_out) {
+                                                 T* __restrict__ q_out, T* __restrict__ k_out,
+                                                 T* __restrict__ v_out) {
   __shared__ float cs[128];
   const int r = blockIdx.x;
   const int b = seq_of_row(st, r);
   const int pos = min(st.pos0(b) + (r - st.q_cu[b]), max_pos - 1);
   const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
-  rope_row<T>(qkv + r * ld, pos, Hq, Hkv, D, bq, bk, bv, rf, k_out + (int64_t)r * Hkv * D,
-              v_out + (int64_t)r * Hkv * D, cs);
+  rope_row<T>(qkv + r * ld, pos, Hq, Hkv, D, bq, bk, bv, rf, q_out + (int64_t)r * Hq * D,
+              k_out + (int64_t)r * Hkv * D, v_out + (int64_t)r * Hkv * D, cs);
 }
 
-hipError_t launch_rope_kv(hipStream_t s, bool bf16, const SeqTable& st, void* qkv, int32_t M,
+hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* qkv, int32_t M,
                           int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
-                          const void* bv, const RopeFreq& rf, int32_t max_pos, void* k_out,
+                          const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
                           void* v_out) {
   if (M <= 0) return hipSuccess;
-  if (bf16)
-    k_rope_kv<bf16_t><<<M, 256, 0, s>>>(st, (bf16_t*)qkv, Hq, Hkv, D, (const bf16_t*)bq,
-                                        (const bf16_t*)bk, (const bf16_t*)bv, rf, max_pos,
-                                        (bf16_t*)k_out, (bf16_t*)v_out);
-  else
-    k_rope_kv<float><<<M, 256, 0, s>>>(st, (float*)qkv, Hq, Hkv, D, (const float*)bq,
-                                       (const float*)bk, (const float*)bv, rf, max_pos,
-                                       (float*)k_out, (float*)v_out);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_rope_kv<E><<<M, 256, 0, s>>>(st, qkv, Hq, Hkv, D, (const E*)bq, (const E*)bk,
+                                        (const E*)bv, rf, max_pos, (E*)q_out, (E*)k_out,
+                                        (E*)v_out);
+  });
   return hipGetLastError();
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_decode_rope_kv(T* __restrict__ qkv, int Hq, int Hkv, int D,
+__global__ __launch_bounds__(256) void k_decode_rope_kv(const float* __restrict__ qkv, int Hq, int Hkv, int D,
                                                         const T* __restrict__ bq, const T* __restrict__ bk,
                                                         const T* __restrict__ bv, RopeFreq rf,
                                                         const int32_t* __restrict__ kv_len, int cap,
-                                                        int max_pos, T* __restrict__ ck,
-                                                        T* __restrict__ cv) {
+                                                        int max_pos, T* __restrict__ q_out,
+                                                        T* __restrict__ ck, T* __restrict__ cv) {
   __shared__ float cs[128];
   const int b = blockIdx.x;
   const int slot = min(max(kv_len[b], 0), min(cap, max_pos) - 1);
   const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
   const int64_t dst = ((int64_t)b * cap + slot) * Hkv * D;
-  rope_row<T>(qkv + b * ld, slot, Hq, Hkv, D, bq, bk, bv, rf, ck + dst, cv + dst, cs);
+  rope_row<T>(qkv + b * ld, slot, Hq, Hkv, D, bq, bk, bv, rf, q_out + (int64_t)b * Hq * D, ck + dst, cv + dst, cs);
 }
 
-hipError_t launch_decode_rope_kv(hipStream_t s, bool bf16, void* qkv, int32_t B, int32_t Hq, int32_t Hkv,
+hipError_t launch_decode_rope_kv(hipStream_t s, rp_dtype dt, const float* qkv, int32_t B, int32_t Hq, int32_t Hkv,
                                  int32_t D, const void* bq, const void* bk, const void* bv,
                                  const RopeFreq& rf, const int32_t* kv_len, int32_t cap, int32_t max_pos,
-                                 void* cache_k, void* cache_v) {
-  if (bf16)
-    k_decode_rope_kv<bf16_t><<<B, 256, 0, s>>>((bf16_t*)qkv, Hq, Hkv, D, (const bf16_t*)bq,
-                                               (const bf16_t*)bk, (const bf16_t*)bv, rf, kv_len, cap,
-                                               max_pos, (bf16_t*)cache_k, (bf16_t*)cache_v);
-  else
-    k_decode_rope_kv<float><<<B, 256, 0, s>>>((float*)qkv, Hq, Hkv, D, (const float*)bq,
-                                              (const float*)bk, (const float*)bv, rf, kv_len, cap,
-                                              max_pos, (float*)cache_k, (float*)cache_v);
+                                 void* q_out, void* cache_k, void* cache_v) {
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_decode_rope_kv<E><<<B, 256, 0, s>>>(qkv, Hq, Hkv, D, (const E*)bq, (const E*)bk,
+                                               (const E*)bv, rf, kv_len, cap, max_pos, (E*)q_out,
+                                               (E*)cache_k, (E*)cache_v);
+  });
   return hipGetLastError();
 }
 
@@ -291,14 +289,14 @@ __global__ __launch_bounds__(256) void k_swiglu(const T* __restrict__ gu, int64_
   }
 }
 
-hipError_t launch_swiglu(hipStream_t s, bool bf16, const void* gu, int32_t M, int32_t F, void* act) {
+hipError_t launch_swiglu(hipStream_t s, rp_dtype dt, const void* gu, int32_t M, int32_t F, void* act) {
   if (M <= 0) return hipSuccess;
   const int64_t n = (int64_t)M * (F / 8);
   const int blocks = (int)std::min<int64_t>((n + 255) / 256, 256 * 64);
-  if (bf16)
-    k_swiglu<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)gu, M, F, (bf16_t*)act);
-  else
-    k_swiglu<float><<<blocks, 256, 0, s>>>((const float*)gu, M, F, (float*)act);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_swiglu<E><<<blocks, 256, 0, s>>>((const E*)gu, M, F, (E*)act);
+  });
   return hipGetLastError();
 }
 

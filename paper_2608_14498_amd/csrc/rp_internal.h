@@ -51,20 +51,22 @@ struct BSeg {
 
 // ---- launchers (return hipGetLastError() of the launch) ----
 hipError_t launch_visual_index(hipStream_t s, const int32_t* ids, int32_t T, int32_t* vis_idx);
-hipError_t launch_embed(hipStream_t s, bool bf16, const int32_t* ids, const int32_t* vis_idx,
+hipError_t launch_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const int32_t* vis_idx,
                         const void* visual, int64_t n_visual, const void* embed, int32_t vocab,
                         int32_t T, int32_t d, float* X);
-hipError_t launch_rmsnorm(hipStream_t s, bool bf16, const float* X, const void* w, float eps, int32_t M,
+hipError_t launch_rmsnorm(hipStream_t s, rp_dtype dt, const float* X, const void* w, float eps, int32_t M,
                           int32_t d, void* out);
 // Final norm of the suffix rows with boundary assembly: row r of sequence b reads
 // h_last[b] if it is the sequence's first response row, else Y[r-1].
-hipError_t launch_final_norm_rows(hipStream_t s, bool bf16, const SeqTable& st, const float* Y,
+hipError_t launch_final_norm_rows(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* Y,
                                   const float* h_last, const void* w, float eps, int32_t R, int32_t d,
                                   void* out);
-hipError_t launch_rope_kv(hipStream_t s, bool bf16, const SeqTable& st, void* qkv, int32_t M,
+// qkv: fp32 projection rows [M, (Hq+2Hkv)*D]; q_out [M, Hq*D], k_out/v_out [M, Hkv*D] in T.
+hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* qkv, int32_t M,
                           int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
-                          const void* bv, const RopeFreq& rf, int32_t max_pos, void* k_out, void* v_out);
-hipError_t launch_swiglu(hipStream_t s, bool bf16, const void* gu, int32_t M, int32_t F, void* act);
+                          const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
+                          void* v_out);
+hipError_t launch_swiglu(hipStream_t s, rp_dtype dt, const void* gu, int32_t M, int32_t F, void* act);
 hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X, int32_t d, float* h_last);
 hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const int32_t* ids, int32_t R,
                                     int32_t V, float* lp);
@@ -73,7 +75,7 @@ hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t 
 // GEMM: C[M,N] (epi)= A[M,K] . B[N,K]^T, fp32 accumulation.  For EPI_SWIGLU, N is the
 // number of output features f and B = {b0 = gate [N,K], b1 = up [N,K]} (n1 = N); the fused
 // epilogue writes silu(A.gate_f) * (A.up_f).  splitk > 1 needs EPI != EPI_SWIGLU.
-hipError_t launch_gemm(hipStream_t s, bool bf16, int32_t M, int32_t N, int32_t K, const void* A,
+hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
                        int32_t splitk, float* partials);
 // Required float count of `partials` for a split-K GEMM.
@@ -95,18 +97,18 @@ struct AttnArgs {
   int32_t Hq, Hkv, D;
   float scale;
 };
-hipError_t launch_attention(hipStream_t s, bool bf16, const SeqTable& st, const AttnArgs& a,
+hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, const AttnArgs& a,
                             int32_t total_q);
 
 // Decode step pieces.
-hipError_t launch_decode_embed(hipStream_t s, bool bf16, const int32_t* ids, const void* embed,
+hipError_t launch_decode_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const void* embed,
                                int32_t vocab, int32_t B, int32_t d, float* X);
-hipError_t launch_decode_rope_kv(hipStream_t s, bool bf16, void* qkv, int32_t B, int32_t Hq, int32_t Hkv,
+hipError_t launch_decode_rope_kv(hipStream_t s, rp_dtype dt, const float* qkv, int32_t B, int32_t Hq, int32_t Hkv,
                                  int32_t D, const void* bq, const void* bk, const void* bv,
                                  const RopeFreq& rf, const int32_t* kv_len, int32_t cap, int32_t max_pos,
-                                 void* cache_k, void* cache_v);
+                                 void* q_out, void* cache_k, void* cache_v);
 size_t decode_attn_partial_floats(int32_t B, int32_t Hq, int32_t D, int32_t cap);
-hipError_t launch_decode_attention(hipStream_t s, bool bf16, const void* q, int32_t q_ld,
+hipError_t launch_decode_attention(hipStream_t s, rp_dtype dt, const void* q, int32_t q_ld,
                                    const void* cache_k, const void* cache_v, const int32_t* kv_len,
                                    int32_t cap, int32_t max_pos, int32_t B, int32_t Hq, int32_t Hkv,
                                    int32_t D, float scale, float* partials, void* o);

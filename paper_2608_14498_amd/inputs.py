@@ -14,8 +14,13 @@ Recipe (stands in for the paper's video RL datasets, which are not available):
     per sequence placed before its text tokens; token and response ids
     uniform over the vocabulary;
   * bf16 workloads draw in fp32 and round once, to nearest-even, to bf16; both
-    the GPU path and the oracle consume exactly those rounded values.
-bf16 tensors are held as their raw 16-bit patterns (``numpy.uint16``).
+    the GPU path and the oracle consume exactly those rounded values;
+  * f16 workloads are the same bf16 model stored in binary16: the bf16-rounded
+    values converted to fp16 (exact inside fp16's normal range; the few weights
+    below 2^-14 in magnitude land on the fp16 subnormal grid, changing them by
+    at most 2^-25).  The oracle consumes the fp16 values.
+bf16 tensors are held as their raw 16-bit patterns (``numpy.uint16``), f16 tensors
+as ``numpy.float16``.
 """
 from __future__ import annotations
 
@@ -63,7 +68,7 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
 
 
 def to_f32(a: np.ndarray) -> np.ndarray:
-    """Float32 values of a stored tensor (bf16 patterns are widened exactly)."""
+    """Float32 values of a stored tensor (bf16 patterns and fp16 are widened exactly)."""
     if a is None:
         return None
     if a.dtype == np.uint16:
@@ -71,12 +76,16 @@ def to_f32(a: np.ndarray) -> np.ndarray:
     return np.asarray(a, dtype=np.float32)
 
 
+def _storage(dtype: str):
+    return {"bf16": np.uint16, "f16": np.float16}.get(dtype, np.float32)
+
+
 # ----------------------------------------------------------------------------------------
 # chunked, threaded normal draws
 # ----------------------------------------------------------------------------------------
 def _draw_normal(shape, seed: List[int], std: float, dtype: str, mean: float = 0.0) -> np.ndarray:
     n = int(np.prod(shape)) if len(shape) else 1
-    out = np.empty(n, dtype=np.uint16 if dtype == "bf16" else np.float32)
+    out = np.empty(n, dtype=_storage(dtype))
     nchunks = (n + CHUNK - 1) // CHUNK
 
     def work(c):
@@ -88,13 +97,18 @@ def _draw_normal(shape, seed: List[int], std: float, dtype: str, mean: float = 0
             v *= np.float32(std)
         if mean != 0.0:
             v += np.float32(mean)
-        if dtype == "bf16":
+        if dtype in ("bf16", "f16"):
+            # the model is defined by the bf16-rounded draw; an "f16" model stores those
+            # same values in binary16 (exact within fp16's normal range)
             u = v.view(np.uint32)
             t = (u >> np.uint32(16)) & np.uint32(1)
             t += np.uint32(0x7FFF)
             u += t
             u >>= np.uint32(16)
-            out[lo:hi] = u
+            if dtype == "bf16":
+                out[lo:hi] = u
+            else:
+                out[lo:hi] = (u << np.uint32(16)).view(np.float32).astype(np.float16)
         else:
             out[lo:hi] = v
 
@@ -110,7 +124,7 @@ def _draw_normal(shape, seed: List[int], std: float, dtype: str, mean: float = 0
 def _ones(shape, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return np.full(shape, 0x3F80, dtype=np.uint16)
-    return np.ones(shape, dtype=np.float32)
+    return np.ones(shape, dtype=_storage(dtype))
 
 
 # ----------------------------------------------------------------------------------------
@@ -125,7 +139,7 @@ class HostWeights:
     layers: List[Dict[str, Optional[np.ndarray]]]
 
     def as_f32(self) -> "HostWeights":
-        """Float32 copy (bf16 patterns widened exactly) for the oracle."""
+        """Float32 copy (16-bit storage widened exactly) for the oracle."""
         return HostWeights(self.model, to_f32(self.embed), to_f32(self.lm_head),
                            to_f32(self.final_norm),
                            [{k: to_f32(v) for k, v in lw.items()} for lw in self.layers])

@@ -38,7 +38,7 @@ class DeviceModel:
         m: ModelShape = host_weights.model
         self.shape = m
         self.device = torch.device(device)
-        self.dtype = torch.bfloat16 if m.dtype == "bf16" else torch.float32
+        self.dtype = {"bf16": torch.bfloat16, "f16": torch.float16}.get(m.dtype, torch.float32)
         self.max_position = int(max_position)
         up = lambda a: to_device(a, self.device)
         self.embed = up(host_weights.embed)

@@ -6,6 +6,8 @@ max error relative to the largest reference magnitude: bf16 storage of K/V alone
 contributes up to 2^-9 relative per element, and activations are rounded to bf16
 between kernels, so 3e-2 bounds the bf16 cases; the fp32 model must match to 1e-5.
 """
+from dataclasses import replace
+
 import numpy as np
 import pytest
 import torch
@@ -38,10 +40,19 @@ BF16_SMALL = configs.ModelShape(n_layers=2, d_model=384, n_q_heads=6, n_kv_heads
                                 ffn_dim=768, vocab=1000, dtype="bf16")
 BF16_D64 = configs.ModelShape(n_layers=2, d_model=256, n_q_heads=8, n_kv_heads=2, head_dim=64,
                               ffn_dim=512, vocab=2051, dtype="bf16")
+# wide enough (K >= 2048) that the suffix GEMMs split K and SwiGLU runs unfused
+BF16_WIDE = configs.ModelShape(n_layers=1, d_model=2048, n_q_heads=16, n_kv_heads=2, head_dim=128,
+                               ffn_dim=4096, vocab=1000, dtype="bf16")
+# the same models stored in fp16 (same kernels, fp16 MFMA)
+F16_SMALL = replace(BF16_SMALL, dtype="f16")
+F16_D64 = replace(BF16_D64, dtype="f16")
+F16_WIDE = replace(BF16_WIDE, dtype="f16")
 
 
 @pytest.mark.parametrize("model,norm,bias", [(BF16_SMALL, "ones", False), (BF16_SMALL, "random", True),
-                                             (BF16_D64, "random", True)])
+                                             (BF16_D64, "random", True), (BF16_WIDE, "random", True),
+                                             (F16_SMALL, "random", True), (F16_D64, "random", True),
+                                             (F16_WIDE, "random", True)])
 def test_bf16_ragged_batch_matches_oracle(model, norm, bias):
     P, Vis, S = [1, 70, 300, 129], [0, 60, 256, 100], [3, 0, 65, 130]
     w = configs.custom(model, P, Vis, S, index=41)
@@ -49,7 +60,7 @@ def test_bf16_ragged_batch_matches_oracle(model, norm, bias):
     bt = inputs.make_batch(w)
     got = gpu_run(w, hw, bt)
     ref = oracle_run(w, hw, bt)
-    r = _report(f"bf16 D={model.head_dim} {norm} bias={bias}", *got, *ref)
+    r = _report(f"{model.dtype} d={model.d_model} D={model.head_dim} {norm} bias={bias}", *got, *ref)
     assert r["lp"] <= 2e-2
     assert r["kv"] <= 3e-2 and r["h"] <= 3e-2
 
@@ -66,7 +77,7 @@ def test_fp32_ragged_edges_match_oracle():
     assert r["lp"] <= 1e-4 and r["kv"] <= 1e-5 and r["h"] <= 1e-5
 
 
-@pytest.mark.parametrize("model", [BF16_SMALL, configs.TINY])
+@pytest.mark.parametrize("model", [BF16_SMALL, configs.TINY, BF16_WIDE, F16_WIDE])
 def test_packing_is_bitwise_invariant(model):
     """A packed ragged batch gives exactly the per-sequence results of running each alone."""
     P, Vis, S = [90, 257, 3], [80, 200, 0], [17, 40, 5]
@@ -87,7 +98,7 @@ def test_packing_is_bitwise_invariant(model):
         assert np.array_equal(lp[cs[b]:cs[b + 1]], lp1)
 
 
-@pytest.mark.parametrize("model", [BF16_SMALL, configs.TINY])
+@pytest.mark.parametrize("model", [BF16_SMALL, configs.TINY, F16_SMALL])
 def test_decode_step_matches_oracle(model):
     from paper_2608_14498_amd.runtime import DeviceModel, to_device
     w = configs.custom(model, [1], [0], [1], index=53)
