@@ -88,8 +88,8 @@ def colocation(args, w):
     # constant context: every step writes slot kv_len and attends to kv_len + 1 keys
     gen = torch.Generator(device=dev).manual_seed(w.index * 1000 + 20)
     shape = (m.n_layers, Bd, cap, m.n_kv_heads, m.head_dim)
-    ck = torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
-    cv = torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    ck = torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(dm.dtype)
+    cv = torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(dm.dtype)
     kv_len = torch.full((Bd,), kvl, dtype=torch.int32, device=dev)
     tok = torch.randint(0, m.vocab, (Bd,), generator=gen, device=dev, dtype=torch.int32)
     nxt = torch.empty(Bd, dtype=torch.int32, device=dev)
@@ -227,6 +227,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-prefix-len", type=int, default=0,
                     help="truncate the CPU-baseline sample prefix (0 = full)")
+    ap.add_argument("--dtype", choices=["bf16", "f16"], default=None,
+                    help="run the workload's model in this 16-bit storage type (default: as named)")
+    ap.add_argument("--no-f16-variant", action="store_true",
+                    help="skip timing the fp16 variant of a bf16 workload")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -246,18 +250,98 @@ def main():
               f"sequence and is measured on one GPU's share.", file=sys.stderr)
         sys.exit(2)
 
+    from paper_2608_14498_amd import configs, perf
+
+    w = configs.get(args.workload)
+    if args.dtype:
+        w = configs.with_model(w, dtype=args.dtype)
+    if w.decode is not None:
+        return colocation(args, w)
+    m = w.model
+    res = run_passes(w, args, profile=True)
+    T, R, B, kernels = res["T"], res["R"], res["B"], res["kernels"]
+    ms_step, pre_ms, suf_ms = res["ms_step"], res["pre_ms"], res["suf_ms"]
+    bt = res["bt"]
+
+    pf = perf.prefix_flops(m, bt.prefix_lens)
+    sf = perf.suffix_flops(m, bt.prefix_lens, bt.suffix_lens)
+    peak = perf.PEAK_FP32_FLOPS if m.dtype == "f32" else perf.PEAK_BF16_FLOPS
+    gu_flops = perf.gemm_flops(T, 2 * m.ffn_dim, m.d_model)
+    gu = kernels.get("prefix.gemm_gate_up")
+    roofline = None
+    if gu:
+        ach = gu_flops / (gu["avg_ms"] * 1e-3) / 1e12
+        traffic = None
+        if w.name == "qwen7b_b4_p4096_s256" and m.dtype == "bf16":
+            traffic = measured_traffic("paper_2608_14498_amd/csrc/gemm.hip",
+                                       "profiles/gemm_gate_up_qwen7b_p4096_traffic.json")
+        roofline = {"kernel": "prefix.gemm_gate_up (fused SwiGLU)", "bound": "mfma", "achieved": ach,
+                    "peak": peak / 1e12, "unit": "TFLOP/s", "frac": ach / (peak / 1e12),
+                    "traffic": traffic, "algorithmic_per_launch": gu_flops,
+                    "algorithmic_bytes_per_launch": 2 * (T * m.d_model + 2 * m.ffn_dim * m.d_model
+                                                         + T * m.ffn_dim)}
+    ls = kernels.get("suffix.logsoftmax_gather")
+    k12 = None
+    if ls:
+        gbs = perf.logsoftmax_bytes(R, m.vocab) / (ls["avg_ms"] * 1e-3) / 1e9
+        k12 = {"bound": "hbm", "achieved": gbs, "peak": perf.PEAK_HBM_BPS / 1e9, "unit": "GB/s",
+               "frac": gbs / (perf.PEAK_HBM_BPS / 1e9)}
+
+    out = {
+        "metric": "prefix prefill tokens/s + suffix logprob tokens/s; % bf16 MFMA peak",
+        "value": (T + R) / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": m.dtype,
+        "data": "synthetic (seeded; N(0,0.02) weights, N(0,1) visual embeddings, uniform ids)",
+        "config": {"workload": w.name, "layers": m.n_layers, "d_model": m.d_model,
+                   "q_heads": m.n_q_heads, "kv_heads": m.n_kv_heads, "head_dim": m.head_dim,
+                   "ffn": m.ffn_dim, "vocab": m.vocab, "batch": B, "prefix_tokens": T,
+                   "suffix_tokens": R, "parallelism": "single GPU"},
+        "prefix_tokens_per_s": T / (pre_ms * 1e-3),
+        "suffix_tokens_per_s": R / (suf_ms * 1e-3),
+        "prefix_ms": pre_ms,
+        "suffix_ms": suf_ms,
+        "prefix_tflops": pf["total"] / (pre_ms * 1e-3) / 1e12,
+        "prefix_mfma_frac": pf["total"] / (pre_ms * 1e-3) / peak,
+        "suffix_tflops": sf["total"] / (suf_ms * 1e-3) / 1e12,
+        "suffix_mfma_frac": sf["total"] / (suf_ms * 1e-3) / peak,
+        "roofline": roofline,
+        "logsoftmax_roofline": k12,
+        "kernels": kernels,
+    }
+    if m.dtype == "bf16" and not args.no_f16_variant:
+        # the same model stored in fp16 (bf16 weights converted exactly): same kernels with
+        # fp16 MFMA, the precision that meets the full-size log-prob bar
+        wf = configs.with_model(w, dtype="f16")
+        rf = run_passes(wf, args, profile=False)
+        out["f16_variant"] = {
+            "value": (rf["T"] + rf["R"]) / (rf["ms_step"] * 1e-3), "unit": "tokens/s",
+            "ms_per_step": rf["ms_step"], "prefix_ms": rf["pre_ms"], "suffix_ms": rf["suf_ms"],
+            "prefix_mfma_frac": pf["total"] / (rf["pre_ms"] * 1e-3) / perf.PEAK_BF16_FLOPS}
+    if not args.no_cpu_baseline:
+        log("CPU baseline: oracle on sequence 0")
+        out["cpu_baseline"] = cpu_baseline(w, res["hw"], bt, args.cpu_prefix_len)
+    print(json.dumps(out), flush=True)
+
+
+def run_passes(w, args, profile: bool):
+    """Time prefix + suffix steps of workload w; optionally per-kernel durations."""
     import numpy as np
     import torch
 
     from paper_2608_14498_amd import binding as rb
-    from paper_2608_14498_amd import configs, inputs, perf
+    from paper_2608_14498_amd import inputs
     from paper_2608_14498_amd.runtime import DeviceModel, to_device
 
-    w = configs.get(args.workload)
-    if w.decode is not None:
-        return colocation(args, w)
     m = w.model
-    log(f"workload {w.name}: generating seeded inputs")
+    log(f"workload {w.name} ({m.dtype}): generating seeded inputs")
     t0 = time.time()
     hw = inputs.make_weights(w)
     bt = inputs.make_batch(w)
@@ -309,77 +393,24 @@ def main():
     if not np.all(np.isfinite(lp[:R].cpu().numpy())):
         raise RuntimeError("non-finite log-probs")
 
-    # per-kernel durations: HIP events around every launch, on the launch stream
-    log(f"per-kernel timing over {args.profile_steps} steps")
-    rb.rp_profile_reset()
-    rb.rp_profile_enable(True, 4096)
-    for _ in range(args.profile_steps):
-        step()
-        torch.cuda.synchronize()
-        rb.rp_profile_collect()
-    kern = rb.rp_profile_read_all()
-    rb.rp_profile_enable(False)
-    kernels = {k: {"launches": n, "avg_ms": ms / max(n, 1), "ms_per_step": ms / args.profile_steps}
-               for k, (n, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1])}
-
-    pf = perf.prefix_flops(m, bt.prefix_lens)
-    sf = perf.suffix_flops(m, bt.prefix_lens, bt.suffix_lens)
-    peak = perf.PEAK_BF16_FLOPS if m.dtype == "bf16" else perf.PEAK_FP32_FLOPS
-    gu_flops = perf.gemm_flops(T, 2 * m.ffn_dim, m.d_model)
-    gu = kernels.get("prefix.gemm_gate_up")
-    roofline = None
-    if gu:
-        ach = gu_flops / (gu["avg_ms"] * 1e-3) / 1e12
-        traffic = None
-        if w.name == "qwen7b_b4_p4096_s256":
-            traffic = measured_traffic("paper_2608_14498_amd/csrc/gemm.hip",
-                                       "profiles/gemm_gate_up_qwen7b_p4096_traffic.json")
-        roofline = {"kernel": "prefix.gemm_gate_up (fused SwiGLU)", "bound": "mfma", "achieved": ach,
-                    "peak": peak / 1e12, "unit": "TFLOP/s", "frac": ach / (peak / 1e12),
-                    "traffic": traffic, "algorithmic_per_launch": gu_flops,
-                    "algorithmic_bytes_per_launch": 2 * (T * m.d_model + 2 * m.ffn_dim * m.d_model
-                                                         + T * m.ffn_dim)}
-    ls = kernels.get("suffix.logsoftmax_gather")
-    k12 = None
-    if ls:
-        gbs = perf.logsoftmax_bytes(R, m.vocab) / (ls["avg_ms"] * 1e-3) / 1e9
-        k12 = {"bound": "hbm", "achieved": gbs, "peak": perf.PEAK_HBM_BPS / 1e9, "unit": "GB/s",
-               "frac": gbs / (perf.PEAK_HBM_BPS / 1e9)}
-
-    out = {
-        "metric": "prefix prefill tokens/s + suffix logprob tokens/s; % bf16 MFMA peak",
-        "value": (T + R) / (ms_step * 1e-3),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": m.dtype,
-        "data": "synthetic (seeded; N(0,0.02) weights, N(0,1) visual embeddings, uniform ids)",
-        "config": {"workload": w.name, "layers": m.n_layers, "d_model": m.d_model,
-                   "q_heads": m.n_q_heads, "kv_heads": m.n_kv_heads, "head_dim": m.head_dim,
-                   "ffn": m.ffn_dim, "vocab": m.vocab, "batch": B, "prefix_tokens": T,
-                   "suffix_tokens": R, "parallelism": "single GPU"},
-        "prefix_tokens_per_s": T / (pre_ms * 1e-3),
-        "suffix_tokens_per_s": R / (suf_ms * 1e-3),
-        "prefix_ms": pre_ms,
-        "suffix_ms": suf_ms,
-        "prefix_tflops": pf["total"] / (pre_ms * 1e-3) / 1e12,
-        "prefix_mfma_frac": pf["total"] / (pre_ms * 1e-3) / peak,
-        "suffix_tflops": sf["total"] / (suf_ms * 1e-3) / 1e12,
-        "suffix_mfma_frac": sf["total"] / (suf_ms * 1e-3) / peak,
-        "roofline": roofline,
-        "logsoftmax_roofline": k12,
-        "kernels": kernels,
-    }
-    if not args.no_cpu_baseline:
-        log("CPU baseline: oracle on sequence 0")
-        out["cpu_baseline"] = cpu_baseline(w, hw, bt, args.cpu_prefix_len)
+    kernels = {}
+    if profile:
+        # per-kernel durations: HIP events around every launch, on the launch stream
+        log(f"per-kernel timing over {args.profile_steps} steps")
+        rb.rp_profile_reset()
+        rb.rp_profile_enable(True, 4096)
+        for _ in range(args.profile_steps):
+            step()
+            torch.cuda.synchronize()
+            rb.rp_profile_collect()
+        kern = rb.rp_profile_read_all()
+        rb.rp_profile_enable(False)
+        kernels = {k: {"launches": n, "avg_ms": ms / max(n, 1), "ms_per_step": ms / args.profile_steps}
+                   for k, (n, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1])}
     dm.close()
-    print(json.dumps(out), flush=True)
+    del K, V, ids, vis, resp, ws_p, ws_s
+    torch.cuda.empty_cache()
+    return dict(T=T, R=R, B=B, bt=bt, hw=hw, ms_step=ms_step, pre_ms=pre_ms, suf_ms=suf_ms, kernels=kernels)
 
 
 if __name__ == "__main__":

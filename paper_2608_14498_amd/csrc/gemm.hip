@@ -37,9 +37,6 @@ struct GemmArgs {
   int tiles_m, tiles_n;
   int k_chunk;       // K range per split (multiple of the k slab)
   float* partials;   // split-K: [splitk][M][N] fp32
-  // LDS-DMA kernel only: the B segments as byte offsets from one base
-  const void* Bbase;
-  uint32_t boff[3];
 };
 
 template <typename T>
@@ -242,6 +239,41 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&
             make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
       }
     const int k = lane & 31;
+    if (vec && ncol0 + TN <= g.N) {
+      // every column of the wave tile is in range: read the staged rows, then (residual)
+      // the matching rows of C at once, then add and store; rows past M are clamped for
+      // the read and skipped for the store
+      // two batches of 8 rows keep the staged values and C within the register budget
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        float4 v[8], c[8];
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const int r = 2 * (hb * 8 + s) + (lane >> 5);
+          v[s] = *reinterpret_cast<const float4*>(stage + r * 512 + ((k ^ (r & 15)) << 4));
+        }
+        if (EPI == EPI_ADD_F32) {
+#pragma unroll
+          for (int s = 0; s < 8; ++s) {
+            const int m = min(mw + i * 32 + 2 * (hb * 8 + s) + (lane >> 5), g.M - 1);
+            c[s] = *reinterpret_cast<const float4*>(out + (int64_t)m * ld + ncol0 + k * 4);
+          }
+        }
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const int m = mw + i * 32 + 2 * (hb * 8 + s) + (lane >> 5);
+          float4 o = v[s];
+          if (EPI == EPI_ADD_F32) {
+            o.x += c[s].x;
+            o.y += c[s].y;
+            o.z += c[s].z;
+            o.w += c[s].w;
+          }
+          if (m < g.M) *reinterpret_cast<float4*>(out + (int64_t)m * ld + ncol0 + k * 4) = o;
+        }
+      }
+      continue;
+    }
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
       const int r = 2 * s + (lane >> 5);
@@ -450,32 +482,39 @@ __global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
 
   // Load instruction i of this wave fills LDS rows wave*8*LOADS + 8i .. +8; lane l writes
   // physical chunk l%8 of row +l/8, which holds logical chunk (l%8) ^ swz(row).  Sources
-  // are byte offsets into one buffer resource per operand (the host guarantees every
-  // operand byte lies within 2 GiB of the resource base); the slab offset is uniform.
-  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, 0x7fffffff, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc((void*)g.Bbase, 0, 0x7fffffff, 0x00020000);
-  uint32_t aoff[LOADS], boff[LOADS];
-#pragma unroll
-  for (int i = 0; i < LOADS; ++i) {
-    const int r = wave * 8 * LOADS + 8 * i + (lane >> 3);
-    const int c = (lane & 7) ^ swz(r);
-    aoff[i] = 2u * ((uint32_t)min(m0 + r, g.M - 1) * (uint32_t)g.lda + (uint32_t)(kbeg + c * 8));
-    int br;
+  // are byte offsets into the buffer resource of A or of the B segment that holds the
+  // instruction's 8 rows (the host checked that every block lies in one segment of less
+  // than 4 GiB); the slab offset is uniform.
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsB0 = __builtin_amdgcn_make_buffer_rsrc((void*)g.B.b0, 0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsB1 = __builtin_amdgcn_make_buffer_rsrc((void*)g.B.b1, 0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsB2 = __builtin_amdgcn_make_buffer_rsrc((void*)g.B.b2, 0, -1, 0x00020000);
+  auto b_logical = [&](int r) -> int {
     if (EPI == EPI_SWIGLU) {  // per 128-row half: 64 gate rows then the matching 64 up rows
       const int w = r >> 7, cc = r & 127;
-      br = (cc >= 64 ? g.B.n1 : 0) + min(tn * 128 + w * 64 + (cc & 63), g.N - 1);
-    } else {
-      br = min(tn * GB_N + r, g.N - 1);
+      return (cc >= 64 ? g.B.n1 : 0) + min(tn * 128 + w * 64 + (cc & 63), g.N - 1);
     }
-    const uint32_t seg = br < g.B.n1 ? g.boff[0] : br < g.B.n2 ? g.boff[1] : g.boff[2];
-    const int rin = br < g.B.n1 ? br : br < g.B.n2 ? br - g.B.n1 : br - g.B.n2;
-    boff[i] = seg + 2u * ((uint32_t)rin * (uint32_t)g.ldb + (uint32_t)(kbeg + c * 8));
+    return min(tn * GB_N + r, g.N - 1);
+  };
+  uint32_t aoff[LOADS], boff[LOADS];
+  __amdgpu_buffer_rsrc_t rsB[LOADS];
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) {
+    const int r0 = wave * 8 * LOADS + 8 * i;  // first row of the block (wave-uniform)
+    const int br0 = b_logical(r0);
+    const int seg = br0 < g.B.n1 ? 0 : br0 < g.B.n2 ? 1 : 2;
+    rsB[i] = seg == 0 ? rsB0 : seg == 1 ? rsB1 : rsB2;
+    const int sbeg = seg == 0 ? 0 : seg == 1 ? g.B.n1 : g.B.n2;
+    const int r = r0 + (lane >> 3);
+    const int c = (lane & 7) ^ swz(r);
+    aoff[i] = 2u * ((uint32_t)min(m0 + r, g.M - 1) * (uint32_t)g.lda + (uint32_t)(kbeg + c * 8));
+    boff[i] = 2u * ((uint32_t)(b_logical(r) - sbeg) * (uint32_t)g.ldb + (uint32_t)(kbeg + c * 8));
   }
 #define D_LOAD(DA, DB, kt_)                                                                            \
   _Pragma("unroll") for (int i = 0; i < LOADS; ++i) {                                                 \
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)(DA + (wave * LOADS + i) * 64), 16, aoff[i], \
                                              (kt_) * (GB_K * 2), 0, 0);                                \
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void*)(DB + (wave * LOADS + i) * 64), 16, boff[i], \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB[i], (lds_void*)(DB + (wave * LOADS + i) * 64), 16, boff[i], \
                                              (kt_) * (GB_K * 2), 0, 0);                                \
   }
 #define D_FRAGS(AF, BF, SA, SB, ks_)                                          \
@@ -644,29 +683,25 @@ size_t gemm_partial_floats(int32_t M, int32_t N, int32_t splitk) {
   return splitk > 1 ? (size_t)splitk * M * N : 0;
 }
 
-// The LDS-DMA kernel addresses each operand through a buffer resource with 32-bit byte
-// offsets: it is usable when A, and all used B segments together, span less than 2 GiB.
-// b_rows is the number of logical B rows (N, or n1 + N for the fused SwiGLU layout).
-static bool dma_setup(GemmArgs& g, int64_t b_rows) {
-  constexpr uint64_t kLim = 0x7FFFFF00ull;  // the resources cover 2 GiB
+// The LDS-DMA kernel addresses A and each B segment through its own buffer resource with
+// 32-bit byte offsets, and picks the B segment per load instruction (8 consecutive tile
+// rows).  Usable when A and every used B segment span less than 4 GiB and no 8-row block
+// straddles a segment boundary: boundaries at multiples of 8 rows (q/k/v), or the fused
+// SwiGLU layout, whose 64-row gate and up runs never mix within a block.  b_rows is the
+// number of logical B rows (N, or n1 + N for the fused SwiGLU layout).
+static bool dma_setup(const GemmArgs& g, int64_t b_rows, bool swiglu) {
+  constexpr uint64_t kLim = 0xFFFFFF00ull;
   if (g.M <= 0 || g.K <= 0) return false;
   const uint64_t a_ext = ((uint64_t)(g.M - 1) * (uint64_t)g.lda + (uint64_t)g.K) * 2u;
   if (a_ext > kLim) return false;
-  const void* base[3] = {g.B.b0, g.B.b1, g.B.b2};
   const int64_t start[3] = {0, g.B.n1, g.B.n2};
   const int64_t end[3] = {g.B.n1, g.B.n2, b_rows};
-  uintptr_t lo = UINTPTR_MAX, hi = 0;
-  int64_t rows[3];
   for (int k = 0; k < 3; ++k) {
-    rows[k] = std::min(end[k], b_rows) - start[k];
-    if (rows[k] <= 0) continue;
-    const uintptr_t p = (uintptr_t)base[k];
-    lo = std::min(lo, p);
-    hi = std::max(hi, p + (uintptr_t)(((uint64_t)(rows[k] - 1) * (uint64_t)g.ldb + (uint64_t)g.K) * 2u));
+    const int64_t rows = std::min(end[k], b_rows) - start[k];
+    if (rows <= 0) continue;
+    if (((uint64_t)(rows - 1) * (uint64_t)g.ldb + (uint64_t)g.K) * 2u > kLim) return false;
+    if (!swiglu && k > 0 && start[k] % 8 != 0) return false;
   }
-  if (hi <= lo || hi - lo > kLim) return false;
-  g.Bbase = (const void*)lo;
-  for (int k = 0; k < 3; ++k) g.boff[k] = rows[k] > 0 ? (uint32_t)((uintptr_t)base[k] - lo) : 0u;
   return true;
 }
 
@@ -674,7 +709,7 @@ static bool dma_setup(GemmArgs& g, int64_t b_rows) {
 // streamed by the LDS-DMA kernel unless they span more than its 2 GiB buffer window.
 template <int EPI, typename T16>
 static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, bool allow_dma = true) {
-  if (allow_dma && dma_setup(g, b_rows))
+  if (allow_dma && dma_setup(g, b_rows, EPI == EPI_SWIGLU))
     k_gemm_bf16_dma<EPI, T16><<<grid, 512, 0, s>>>(g);
   else
     k_gemm_bf16<EPI, T16, 4><<<grid, 512, 0, s>>>(g);
