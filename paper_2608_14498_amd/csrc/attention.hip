@@ -51,18 +51,75 @@ __device__ __forceinline__ QBlock find_qblock(const SeqTable& st, int qbl, int B
 }
 
 // ------------------------------------------------------------------------------------
-// bf16 MFMA flash attention
+// bf16 / fp16 MFMA flash attention
 //
-// K and V tiles are both staged row-major ([key][Dh], 16-byte chunks, per-operand XOR
-// swizzle).  S^T = K Q^T reads K fragments with ds_read_b128.  The V^T operand of
-// O^T += V^T P^T is read with ds_read_b64_tr_b16: within a 16-lane group, lane i receives
-// column i%4 of the 8-byte chunks addressed by lanes i/4, i/4+4, i/4+8, i/4+12, so lane
-// p addressing V[k0 + p/4][d0 + 4(p%4)] hands lane i the four keys k0..k0+3 of head
+// K and V tiles are staged row-major in LDS ([key][Dh], 16-byte chunks, per-operand XOR
+// swizzle) by direct global->LDS loads (buffer_load ... lds): one load instruction fills
+// 64 consecutive chunks, and the swizzle is applied by choosing which global chunk each
+// lane fetches.  The two LDS buffers are separate arrays and the tile loop is unrolled
+// by two, so every LDS access names its buffer at compile time and the compiler waits
+// on exactly the loads that filled it.  Each key segment of the sequence is one buffer
+// resource whose extent ends at the segment's last row: rows past the end read as
+// zeros (keys that the causal mask removes, with zero values), so no index is clamped.
+//
+// S^T = K Q^T reads K fragments with ds_read_b128.  The V^T operand of O^T += V^T P^T
+// is read with ds_read_b64_tr_b16: within a 16-lane group, lane i receives column i%4
+// of the 8-byte chunks addressed by lanes i/4, i/4+4, i/4+8, i/4+12, so lane p
+// addressing V[k0 + p/4][d0 + 4(p%4)] hands lane i the four keys k0..k0+3 of head
 // dimension d0+i -- the MFMA operand, with no transposed copy of V.
 // ------------------------------------------------------------------------------------
+// Block -> (q block, q head), XCD-aware.  Workgroup i runs on XCD i % 8, which has its
+// own L2, so the q heads that share a kv head (one GQA group, reading the same K/V
+// tiles) are kept on one XCD: with Hkv dividing 8, each group gets 8/Hkv XCDs that take
+// its (q block, head) items in turn; with Hkv a multiple of 8, XCD x gets the groups
+// g = x mod 8.  Items run q-block-major, longest q blocks first.  Other head counts use
+// the plain order.  Returns the grid size; blocks past the work map to q blocks
+// beyond the last (find_qblock reports none).
+struct FaMap {
+  int mode, G, X;  // mode 0: plain, 1: 8/Hkv XCDs per group, 2: Hkv/8 groups per XCD
+};
+__host__ __device__ inline FaMap fa_map(int Hq, int Hkv) {
+  FaMap m;
+  m.G = Hq / Hkv;
+  if (8 % Hkv == 0) {
+    m.mode = 1;
+    m.X = 8 / Hkv;
+  } else if (Hkv % 8 == 0) {
+    m.mode = 2;
+    m.X = Hkv / 8;
+  } else {
+    m.mode = 0;
+    m.X = 1;
+  }
+  return m;
+}
+inline int fa_grid(const FaMap& m, int nqb, int Hq) {
+  if (m.mode == 1) return 8 * ((nqb * m.G + m.X - 1) / m.X);
+  return nqb * Hq;
+}
+__device__ __forceinline__ void fa_block(const FaMap& m, int bid, int Hq, int* qbl, int* h) {
+  const int x = bid & 7, r = bid >> 3;
+  if (m.mode == 1) {
+    const int i = r * m.X + x % m.X;
+    *qbl = i / m.G;
+    *h = (x / m.X) * m.G + i % m.G;
+  } else if (m.mode == 2) {
+    const int per = m.X * m.G;  // items of one q block on one XCD
+    const int rem = r % per;
+    *qbl = r / per;
+    *h = ((rem / m.G) * 8 + x) * m.G + rem % m.G;
+  } else {
+    *qbl = bid / Hq;
+    *h = bid % Hq;
+  }
+}
+
 constexpr float kMaskVal = -1e30f;
+constexpr float kLazy = 8.f;  // log2 headroom of the lazily updated softmax max
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 template <int D>
 __device__ __forceinline__ int kswz(int key) { return D == 128 ? (key & 15) : (key & 7); }
@@ -71,35 +128,98 @@ __device__ __forceinline__ int vswz(int key) { return (key & 3) << 1; }
 template <typename T16, int D, int QW, int KT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QW == 1 ? 2 : 1, QW == 1 ? 2 : 1)))
 void k_attn_bf16(SeqTable st, AttnArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
   typedef Half16<T16> H;
   typedef typename H::V8 V8;
   constexpr int BQ = 4 * 32 * QW;
-  constexpr int CH = D / 8;              // 16-byte chunks per K/V row
-  constexpr int KSTEPS = D / 16;         // MFMA k-steps of S^T (over Dh)
-  constexpr int DB = D / 32;             // 32-row blocks of O^T
-  constexpr int KB = KT / 32;            // 32-key blocks per tile
-  constexpr int LOADS = (KT * CH) / 256;  // 16-byte chunks per thread per matrix
-  static_assert(LOADS == 1 || LOADS == 2 || LOADS == 4, "tile loader");
-  __shared__ uint4 Ks[2][KT * CH];
-  __shared__ uint4 Vs[2][KT * CH];
+  constexpr int CH = D / 8;               // 16-byte chunks per K/V row
+  constexpr int KSTEPS = D / 16;          // MFMA k-steps of S^T (over Dh)
+  constexpr int DB = D / 32;              // 32-row blocks of O^T
+  constexpr int KB = KT / 32;             // 32-key blocks per tile
+  constexpr int LOADS = (KT * CH) / 256;  // load instructions per wave per matrix
+  static_assert(LOADS >= 1 && (KT * CH) % 256 == 0 && 64 % CH == 0, "tile loader");
+  __shared__ u32x4_t Ks0[KT * CH], Ks1[KT * CH], Vs0[KT * CH], Vs1[KT * CH];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int h = blockIdx.x % a.Hq;
-  const QBlock qb = find_qblock(st, blockIdx.x / a.Hq, BQ);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int h, qbl;
+  fa_block(fa_map(a.Hq, a.Hkv), blockIdx.x, a.Hq, &qbl, &h);
+  QBlock qb = find_qblock(st, qbl, BQ);
   if (qb.b < 0) return;
-  const int b = qb.b;
+  // Block-uniform values, moved to scalar registers (the sequence table is indexed
+  // dynamically, which the compiler cannot prove uniform).
+  const int b = __builtin_amdgcn_readfirstlane(qb.b);
+  qb.q_begin = __builtin_amdgcn_readfirstlane(qb.q_begin);
+  qb.q_end = __builtin_amdgcn_readfirstlane(qb.q_end);
   const int G = a.Hq / a.Hkv, g = h / G;
-  const int n0 = st.pos0(b);
-  const int qpos_first = n0 + (qb.q_begin - st.q_cu[b]);
-  const int qpos_last = n0 + (qb.q_end - 1 - st.q_cu[b]);
+  const int krow0 = __builtin_amdgcn_readfirstlane(st.k_cu[b]);
+  const int n0 = __builtin_amdgcn_readfirstlane(st.k_cu[b + 1]) - krow0;
+  const int qrow0 = __builtin_amdgcn_readfirstlane(st.q_cu[b]);
+  const int nq = __builtin_amdgcn_readfirstlane(st.q_cu[b + 1]) - qrow0;
+  const int qpos_first = n0 + (qb.q_begin - qrow0);
+  const int qpos_last = n0 + (qb.q_end - 1 - qrow0);
   const int nk = qpos_last + 1;  // keys needed by this block
   const int ntiles = (nk + KT - 1) / KT;
+
+  // Key segments as buffer resources: segment 0 = the n0 prefix rows, segment 1 = the
+  // nq rows of the queries; key kv of segment s is at byte (kv - start_s) * row_bytes.
+  // The host guarantees those offsets, past-the-end tile rows included, fit 32 bits.
   const int64_t kv_ld = (int64_t)a.Hkv * D;
-  const T16* k0 = (const T16*)a.k0 + (int64_t)g * D;
-  const T16* v0 = (const T16*)a.v0 + (int64_t)g * D;
-  const T16* k1 = (const T16*)a.k1 + (int64_t)g * D;
-  const T16* v1 = (const T16*)a.v1 + (int64_t)g * D;
-  const int krow0 = st.k_cu[b], qrow0 = st.q_cu[b];
+  const uint32_t row_bytes = (uint32_t)kv_ld * sizeof(T16);
+  const uint32_t ext0 = n0 > 0 ? (uint32_t)(n0 - 1) * row_bytes + D * sizeof(T16) : 0u;
+  const uint32_t ext1 = (uint32_t)(nq - 1) * row_bytes + D * sizeof(T16);
+  const int64_t e0 = (int64_t)krow0 * kv_ld + (int64_t)g * D, e1 = (int64_t)qrow0 * kv_ld + (int64_t)g * D;
+  // (64-bit products are formed in vector registers: uniform_ptr returns them to scalar
+  // registers, where a buffer resource must live.)
+  const __amdgpu_buffer_rsrc_t rsK0 =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr((void*)((const T16*)a.k0 + e0)), 0, (int)ext0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsV0 =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr((void*)((const T16*)a.v0 + e0)), 0, (int)ext0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsK1 =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr((void*)((const T16*)a.k1 + e1)), 0, (int)ext1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsV1 =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr((void*)((const T16*)a.v1 + e1)), 0, (int)ext1, 0x00020000);
+
+  // Load instruction j of this wave fills LDS chunks (wave*LOADS + j)*64 + lane, i.e.
+  // tile key (wave*LOADS + j)*64/CH + lane/CH, physical chunk lane%CH, which holds
+  // logical chunk (lane%CH) ^ swizzle(key).
+  uint32_t koff[LOADS], voff[LOADS];
+#pragma unroll
+  for (int j = 0; j < LOADS; ++j) {
+    const int slot = (wave * LOADS + j) * 64 + lane, key = slot / CH, cp = slot % CH;
+    koff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ kswz<D>(key)) * 16);
+    voff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ vswz(key)) * 16);
+  }
+#define FA_DMA(RS_, OFF_, DST_, j_) \
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(RS_, (lds_void_t*)((DST_) + (wave * LOADS + (j_)) * 64), 16, OFF_, 0, 0, 0)
+#define FA_LOAD_SEG(RK_, RV_, KD_, VD_, so_)            \
+  _Pragma("unroll") for (int j = 0; j < LOADS; ++j) {   \
+    FA_DMA(RK_, koff[j] + (so_), KD_, j);               \
+    FA_DMA(RV_, voff[j] + (so_), VD_, j);               \
+  }
+  // Every branch names its buffer resources (a selected resource would be formed in
+  // vector registers); all offsets go in the range-checked vector offset (the scalar
+  // offset is not range-checked).
+#define FA_LOAD(KD_, VD_, t_)                                                         \
+  {                                                                                   \
+    const int klo = (t_) * KT;                                                        \
+    if (klo >= n0) {                                                                  \
+      FA_LOAD_SEG(rsK1, rsV1, KD_, VD_, (uint32_t)(klo - n0) * row_bytes);            \
+    } else if (klo + KT <= n0) {                                                      \
+      FA_LOAD_SEG(rsK0, rsV0, KD_, VD_, (uint32_t)klo * row_bytes);                   \
+    } else { /* the tile straddling the segment boundary: segment per lane */         \
+      _Pragma("unroll") for (int j = 0; j < LOADS; ++j) {                             \
+        const int kv = klo + (wave * LOADS + j) * (64 / CH) + lane / CH;              \
+        if (kv < n0) {                                                                \
+          FA_DMA(rsK0, koff[j] + (uint32_t)klo * row_bytes, KD_, j);                  \
+          FA_DMA(rsV0, voff[j] + (uint32_t)klo * row_bytes, VD_, j);                  \
+        } else {                                                                      \
+          FA_DMA(rsK1, koff[j] + (uint32_t)(klo - n0) * row_bytes, KD_, j);           \
+          FA_DMA(rsV1, voff[j] + (uint32_t)(klo - n0) * row_bytes, VD_, j);           \
+        }                                                                             \
+      }                                                                               \
+    }                                                                                 \
+  }
 
   // ---- queries of this lane: column (lane & 31) of each 32-query block ----
   const int fr = lane & 31, fk = lane >> 5;
@@ -115,25 +235,6 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
     for (int ks = 0; ks < KSTEPS; ++ks) qf[qi][ks] = H::as_v8(*reinterpret_cast<const uint4*>(qp + ks * 16));
   }
 
-  // ---- tile loader: chunk id = i*256 + tid -> (key = id / CH, c = id % CH) ----
-  uint4 rk0, rk1, rk2, rk3, rv0, rv1, rv2, rv3;
-#define FA_LD1(i_, t_)                                                                                   \
-  if (i_ < LOADS) {                                                                                      \
-    const int id = i_ * 256 + tid, key = id / CH, c = id % CH;                                           \
-    const int kv = min((t_) * KT + key, nk - 1);                                                         \
-    const int64_t roff = kv < n0 ? (int64_t)(krow0 + kv) * kv_ld : (int64_t)(qrow0 + kv - n0) * kv_ld;   \
-    rk##i_ = *reinterpret_cast<const uint4*>((kv < n0 ? k0 : k1) + roff + c * 8);                        \
-    rv##i_ = *reinterpret_cast<const uint4*>((kv < n0 ? v0 : v1) + roff + c * 8);                        \
-  }
-#define FA_GLOAD(t_) FA_LD1(0, t_) FA_LD1(1, t_) FA_LD1(2, t_) FA_LD1(3, t_)
-#define FA_ST1(i_, buf_)                                                  \
-  if (i_ < LOADS) {                                                       \
-    const int id = i_ * 256 + tid, key = id / CH, c = id % CH;            \
-    Ks[(buf_)][key * CH + (c ^ kswz<D>(key))] = rk##i_;                   \
-    Vs[(buf_)][key * CH + (c ^ vswz(key))] = rv##i_;                      \
-  }
-#define FA_LSTORE(buf_) FA_ST1(0, buf_) FA_ST1(1, buf_) FA_ST1(2, buf_) FA_ST1(3, buf_)
-
   f32x16_t o[QW][DB];
   float m_run[QW], l_run[QW];
 #pragma unroll
@@ -148,74 +249,76 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   const float c2 = a.scale * 1.4426950408889634f;  // scores in log2 units
   // V^T fragment addressing (see header): 16-lane group -> d0, lane p = lane % 16
   const int tr_p = lane & 15;
-  const int tr_key = fk * 4 + (tr_p >> 2);                 // + kb*32 + hh*16 (+8 for the second read)
+  const int tr_key = fk * 4 + (tr_p >> 2);                     // + kb*32 + hh*16 (+8 for the second read)
   const int tr_col = ((lane & 16) ? 16 : 0) + 4 * (tr_p & 3);  // + db*32
 
-  FA_GLOAD(0);
-  FA_LSTORE(0);
-  __syncthreads();
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) { FA_GLOAD(t + 1); }
+  // One key tile: loads of tile t+1 into (Kn, Vn) are issued first and land while tile t
+  // is computed from (Kc, Vc); the closing barrier (which waits for this wave's loads)
+  // makes them visible to every wave.
+  auto tile = [&](const u32x4_t* Kc, const u32x4_t* Vc, u32x4_t* Kn, u32x4_t* Vn, int t) __attribute__((always_inline)) {
+    if (t + 1 < ntiles) FA_LOAD(Kn, Vn, t + 1);
 
     // ---- S^T = K Q^T: s[qi][kb][e] = score(key t*KT + kb*32 + 8(e/4) + 4 fk + e%4, query fr) ----
     f32x16_t s[QW][KB];
-#pragma unroll
-    for (int qi = 0; qi < QW; ++qi)
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[qi][kb][e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         const int key = kb * 32 + fr;
-        const V8 kf = H::as_v8(Ks[buf][key * CH + ((ks * 2 + fk) ^ kswz<D>(key))]);
+        const V8 kf = __builtin_bit_cast(V8, Kc[key * CH + ((ks * 2 + fk) ^ kswz<D>(key))]);
 #pragma unroll
         for (int qi = 0; qi < QW; ++qi)
-          s[qi][kb] = H::mma(kf, qf[qi][ks], s[qi][kb]);
+          s[qi][kb] = H::mma(kf, qf[qi][ks], ks == 0 ? f32x16_t{} : s[qi][kb]);
       }
     }
 
-    // ---- mask, online softmax (per lane = per query) ----
+    // ---- mask (diagonal tiles only), online softmax per lane = per query ----
+    // Scores stay raw until the exponent: p = 2^(s*c2 - m) with m in log2 units.  The
+    // running max m is raised only when some lane's tile max exceeds it by more than
+    // kLazy (wave-uniform test), so p <= 2^kLazy and the O^T rescale is skipped on most
+    // tiles; numerator and denominator share the same m, so the result is unchanged.
     const bool need_mask = (t * KT + KT - 1) > qpos_first;
 #pragma unroll
     for (int qi = 0; qi < QW; ++qi) {
+      if (need_mask) {
+        const int lim = qpos[qi] - t * KT - 4 * fk;  // key offset in the tile - 4 fk
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (kb * 32 + 8 * (e >> 2) + (e & 3) > lim) s[qi][kb][e] = kMaskVal;
+      }
       float mx = kMaskVal;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = t * KT + kb * 32 + 8 * (e >> 2) + 4 * fk + (e & 3);
-          float v = s[qi][kb][e] * c2;
-          if (need_mask && key > qpos[qi]) v = kMaskVal;
-          s[qi][kb][e] = v;
-          mx = fmaxf(mx, v);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float m_new = fmaxf(m_run[qi], mx);
-      const float alpha = exp2f(m_run[qi] - m_new);
-      m_run[qi] = m_new;
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[qi][kb][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * c2;
+      if (__any(mx > m_run[qi] + kLazy)) {
+        const float m_new = fmaxf(m_run[qi], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qi] - m_new);
+        m_run[qi] = m_new;
+        l_run[qi] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[qi][db][e] *= alpha;
+      }
+      const float nm = -m_run[qi];
       float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float p = exp2f(s[qi][kb][e] - m_new);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[qi][kb][e], c2, nm));
           s[qi][kb][e] = p;
           ls += p;
         }
-      l_run[qi] = l_run[qi] * alpha + ls;
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[qi][db][e] *= alpha;
+      l_run[qi] += ls;
     }
 
     // ---- O^T += V^T P^T over the sixteen-key steps (kb, hh) ----
-    const T16* vbase = reinterpret_cast<const T16*>(&Vs[buf][0]);
+    const T16* vbase = reinterpret_cast<const T16*>(Vc);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
@@ -242,14 +345,20 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
         }
       }
     }
-
-    if (t + 1 < ntiles) { FA_LSTORE(buf ^ 1); }
     __syncthreads();
+  };
+
+  FA_LOAD(Ks0, Vs0, 0);
+  __syncthreads();
+  int t = 0;
+  for (; t + 2 <= ntiles; t += 2) {
+    tile(Ks0, Vs0, Ks1, Vs1, t);
+    tile(Ks1, Vs1, Ks0, Vs0, t + 1);
   }
-#undef FA_LD1
-#undef FA_GLOAD
-#undef FA_ST1
-#undef FA_LSTORE
+  if (t < ntiles) tile(Ks0, Vs0, Ks1, Vs1, t);
+#undef FA_DMA
+#undef FA_LOAD_SEG
+#undef FA_LOAD
 
   // ---- normalise and store: o[qi][db][e] = O^T(dh = db*32 + 8(e/4) + 4 fk + e%4, query fr) ----
 #pragma unroll
@@ -270,6 +379,7 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
         *reinterpret_cast<uint2*>(op + dh) = w;
       }
   }
+#endif
 }
 
 // ------------------------------------------------------------------------------------
@@ -342,22 +452,29 @@ int count_qblocks(const SeqTable& st, int BQ) {
 // Timing-harness hook: forced tile shape (0: 32 queries/wave x 64-key tiles,
 // 1: 64 queries/wave x 32-key tiles).
 hipError_t launch_attention_variant(hipStream_t s, int variant, const SeqTable& st, const AttnArgs& a) {
+  const FaMap m = fa_map(a.Hq, a.Hkv);
   if (variant == 0)
-    k_attn_bf16<bf16_t, 128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+    k_attn_bf16<bf16_t, 128, 1, 64><<<fa_grid(m, count_qblocks(st, 128), a.Hq), 256, 0, s>>>(st, a);
   else
-    k_attn_bf16<bf16_t, 128, 2, 32><<<count_qblocks(st, 256) * a.Hq, 256, 0, s>>>(st, a);
+    k_attn_bf16<bf16_t, 128, 2, 32><<<fa_grid(m, count_qblocks(st, 256), a.Hq), 256, 0, s>>>(st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, const AttnArgs& a, int32_t total_q) {
   if (total_q <= 0) return hipSuccess;
   if (dt != RP_F32) {
+    // The 16-bit kernel addresses a sequence's keys with 32-bit byte offsets.
+    for (int b = 0; b < st.n; ++b) {
+      const int64_t keys = (int64_t)st.pos0(b) + (st.q_cu[b + 1] - st.q_cu[b]);
+      if ((keys + 64) * a.Hkv * a.D * 2 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
+    }
     with_half16(dt, [&](auto tag_) {
       using H = decltype(tag_);
+      const int grid = fa_grid(fa_map(a.Hq, a.Hkv), count_qblocks(st, 128), a.Hq);
       if (a.D == 128)
-        k_attn_bf16<H, 128, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+        k_attn_bf16<H, 128, 1, 64><<<grid, 256, 0, s>>>(st, a);
       else
-        k_attn_bf16<H, 64, 1, 64><<<count_qblocks(st, 128) * a.Hq, 256, 0, s>>>(st, a);
+        k_attn_bf16<H, 64, 1, 64><<<grid, 256, 0, s>>>(st, a);
     });
   } else {
     const int nqb = count_qblocks(st, 64);

@@ -41,25 +41,24 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_ca
 
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// float -> bf16, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 
-// Pack two floats into two bf16 (lo in bits 0..15).
+// float -> bf16 and fp16 by the gfx950 packed conversions (v_cvt_pk_bf16_f32,
+// v_cvt_pk_f16_f32): round to nearest even, NaN stays NaN, overflow goes to inf.
+// Two floats pack into one word, lo in bits 0..15.
 __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
-  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
+__device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)(pack_bf2(f, 0.f) & 0xffffu); }
 
-// float -> fp16, round to nearest even (the conversion instruction's default mode);
-// pack two into one word (lo in bits 0..15).
-__device__ __forceinline__ f16_t f2h(float f) { return (f16_t)f; }
 __device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, f2h(lo)) | ((uint32_t)__builtin_bit_cast(uint16_t, f2h(hi)) << 16);
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2_t));
 }
+__device__ __forceinline__ f16_t f2h(float f) { return (f16_t)f; }
 __device__ __forceinline__ float h2f_bits(uint32_t bits16) {
   return (float)__builtin_bit_cast(f16_t, (uint16_t)bits16);
 }
@@ -95,6 +94,14 @@ template <> struct Half16<f16_t> {
   static __device__ __forceinline__ float lo_f(uint32_t w) { return h2f_bits(w & 0xffffu); }
   static __device__ __forceinline__ float hi_f(uint32_t w) { return h2f_bits(w >> 16); }
 };
+
+// A pointer the caller knows to be the same in every lane, moved to scalar registers.
+template <typename T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+  const uint64_t u = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u), hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (T*)(((uint64_t)hi << 32) | lo);
+}
 
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
