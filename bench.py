@@ -274,7 +274,7 @@ def main():
         traffic = None
         if w.name == "qwen7b_b4_p4096_s256" and m.dtype == "bf16":
             traffic = measured_traffic("paper_2608_14498_amd/csrc/gemm.hip",
-                                       "profiles/gemm_gate_up_qwen7b_p4096_traffic.json")
+                                       "profiles/gemm_gate_up_qwen7b_b4_p4096_s256_traffic.json")
         roofline = {"kernel": "prefix.gemm_gate_up (fused SwiGLU)", "bound": "mfma", "achieved": ach,
                     "peak": peak / 1e12, "unit": "TFLOP/s", "frac": ach / (peak / 1e12),
                     "traffic": traffic, "algorithmic_per_launch": gu_flops,
