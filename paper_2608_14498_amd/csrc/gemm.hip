@@ -24,6 +24,8 @@
 #include "device_common.h"
 #include "rp_internal.h"
 
+#include <stdlib.h>
+
 namespace rp {
 
 struct GemmArgs {
@@ -159,7 +161,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)
 template <int EPI, typename T16, int MI, int NJ, int TM, int TN>
 __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&acc)[MI][NJ], uint8_t* stage,
                                                   int tm, int tn, int wm, int wn, int lane) {
-  static_assert(MI == 2 && NJ == 4 && TM == 64 && TN == 128, "8-wave tile only");
+  static_assert((MI == 2 || MI == 4) && NJ == 4 && TM == 32 * MI && TN == 128, "wave tile 64x128 or 128x128");
   const int fr = lane & 31, fk = lane >> 5;
   const int mw = tm * GB_M + wm * TM;  // first row of the wave tile
   if (EPI == EPI_SWIGLU || EPI == EPI_STORE) {
@@ -188,7 +190,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&
     const bool vec = (g.ldc & 7) == 0 && ((uintptr_t)g.C & 15) == 0;
     const int k = lane % LPR;
 #pragma unroll
-    for (int s = 0; s < 64 / RPI; ++s) {
+    for (int s = 0; s < TM / RPI; ++s) {
       const int r = s * RPI + lane / LPR;
       uint4 v = *reinterpret_cast<const uint4*>(stage + r * (W8 * 8) + ((k ^ ((r & XM) >> 1)) << 4));
       if (r & 1) {  // the two 8-byte halves were stored swapped
@@ -454,10 +456,10 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 // chunk each lane fetches.  The two LDS buffers are separate arrays and the k loop is
 // unrolled by two, so every LDS access names its buffer at compile time.
 // ------------------------------------------------------------------------------------
-template <int EPI, typename T16>
-__global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
+template <int EPI, typename T16, int WGM>
+__global__ __launch_bounds__(WGM * 128) __attribute__((amdgpu_waves_per_eu(WGM == 2 ? 1 : 2, WGM == 2 ? 1 : 2)))
+void k_gemm_bf16_dma(GemmArgs g) {
 #if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
-  constexpr int WGM = 4;  // 4 x 2 waves of 64 x 128
   constexpr int NT = WGM * 2 * 64;
   constexpr int TM = GB_M / WGM, TN = GB_N / 2;
   constexpr int MI = TM / 32, NJ = TN / 32;
@@ -470,6 +472,10 @@ __global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
   __shared__ u32x4_t As0[GB_M * 8], As1[GB_M * 8];
   __shared__ u32x4_t Bs0[GB_N * 8], Bs1[GB_N * 8];
 
+  // 128x128 wave tiles hold 256 accumulator registers, which must live in the AGPR file.
+  // An empty asm statement that names an AGPR keeps the compiler from assuming that the
+  // kernel uses none (it would then put MFMA results in VGPRs and spill).
+  if (WGM == 2) asm volatile("" ::: "a0");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -530,11 +536,13 @@ __global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
   _Pragma("unroll") for (int i = 0; i < MI; ++i)                              \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j)                              \
     acc[i][j] = Half16<T16>::mma(BF[j], AF[i], acc[i][j]);
-  // One 64-deep slab read from (SA, SB) while slab kt_+1 streams into (DA, DB).  The
-  // barrier sits before the last k-step: the fragments of k-step 0 of the next slab are
-  // read (from DA, DB) under the MFMAs of k-step 3, so no slab starts with a wait on
-  // LDS.  DA/DB are free at the top of the slab: their last reads (k-step 3 fragments of
-  // the previous slab) were issued before the previous barrier.
+  // One 64-deep slab read from (SA, SB); slab kt_+1 is already streaming into (DA, DB).
+  // The barrier sits before the last k-step: every wave's copies of slab kt_+1 have
+  // landed and every wave has finished reading (SA, SB), so the fragments of k-step 0 of
+  // the next slab are read (from DA, DB) under the MFMAs of k-step 3, and the copies of
+  // slab kt_+2 go into (SA, SB) right there.  Issued straight after the barrier, a slab's
+  // copies have a whole slab of MFMA time to land and each CU keeps L2 misses in flight
+  // without a gap (the misses' fabric bandwidth, not the MFMAs, bounds the large GEMMs).
 #define D_REGION(n_mem_, mem_mask_)                                                        \
   __builtin_amdgcn_sched_group_barrier(0x100, MI + NJ, 0);                                 \
   _Pragma("unroll") for (int q = 0; q < MM; ++q) {                                         \
@@ -543,11 +551,9 @@ __global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
   }
 #define D_TILE(SA, SB, DA, DB, kt_)                                           \
   {                                                                           \
-    const int ktn_ = (kt_) + 1 < KT ? (kt_) + 1 : (kt_);                      \
     D_FRAGS(af1, bf1, SA, SB, 1);                                             \
     D_MMA(af0, bf0);                                                          \
-    D_LOAD(DA, DB, ktn_);                                                     \
-    D_REGION(2 * LOADS, 0x010);                                               \
+    D_REGION(0, 0x000);                                                       \
     __builtin_amdgcn_sched_barrier(0);                                        \
     D_FRAGS(af0, bf0, SA, SB, 2);                                             \
     D_MMA(af1, bf1);                                                          \
@@ -560,7 +566,8 @@ __global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
     __syncthreads();                                                          \
     D_FRAGS(af0, bf0, DA, DB, 0);                                             \
     D_MMA(af1, bf1);                                                          \
-    D_REGION(0, 0x000);                                                       \
+    D_LOAD(SA, SB, min((kt_) + 2, KT - 1));                                   \
+    D_REGION(2 * LOADS, 0x010);                                               \
     __builtin_amdgcn_sched_barrier(0);                                        \
   }
 
@@ -578,6 +585,7 @@ __global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
     D_LOAD(As0, Bs0, 0);
     __syncthreads();
     D_FRAGS(af0, bf0, As0, Bs0, 0);
+    D_LOAD(As1, Bs1, min(1, KT - 1));  // beyond the last slab: a harmless re-load into an idle buffer
     int kt = 0;
     for (; kt + 2 <= KT; kt += 2) {
       D_TILE(As0, Bs0, As1, Bs1, kt);
@@ -591,7 +599,8 @@ __global__ __launch_bounds__(512) void k_gemm_bf16_dma(GemmArgs g) {
 #undef D_TILE
 #undef D_REGION
   __syncthreads();  // every wave is done with the slab buffers
-  uint8_t* stage = (uint8_t*)(wave < 2 ? As0 : wave < 4 ? As1 : wave < 6 ? Bs0 : Bs1) + (wave & 1) * 16384;
+  uint8_t* stage = WGM == 2 ? (uint8_t*)(wave == 0 ? As0 : wave == 1 ? As1 : wave == 2 ? Bs0 : Bs1)
+                            : (uint8_t*)(wave < 2 ? As0 : wave < 4 ? As1 : wave < 6 ? Bs0 : Bs1) + (wave & 1) * 16384;
   gemm_epilogue_lds<EPI, T16, MI, NJ, TM, TN>(g, acc, stage, tm, tn, wm, wn, lane);
 #endif
 }
@@ -705,12 +714,24 @@ static bool dma_setup(const GemmArgs& g, int64_t b_rows, bool swiglu) {
   return true;
 }
 
+static int gemm_waves() {
+  static const int w = [] {
+    const char* e = getenv("RP_GEMM_WAVES");
+    return e && atoi(e) == 4 ? 4 : 8;
+  }();
+  return w;
+}
+
 // bf16 GEMMs run 8 waves per workgroup (two per SIMD, 64x128 per wave); operands are
 // streamed by the LDS-DMA kernel unless they span more than its 2 GiB buffer window.
 template <int EPI, typename T16>
 static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, bool allow_dma = true) {
-  if (allow_dma && dma_setup(g, b_rows, EPI == EPI_SWIGLU))
-    k_gemm_bf16_dma<EPI, T16><<<grid, 512, 0, s>>>(g);
+  if (allow_dma && dma_setup(g, b_rows, EPI == EPI_SWIGLU)) {
+    if (gemm_waves() == 4)
+      k_gemm_bf16_dma<EPI, T16, 2><<<grid, 256, 0, s>>>(g);
+    else
+      k_gemm_bf16_dma<EPI, T16, 4><<<grid, 512, 0, s>>>(g);
+  }
   else
     k_gemm_bf16<EPI, T16, 4><<<grid, 512, 0, s>>>(g);
 }
