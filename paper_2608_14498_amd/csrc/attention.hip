@@ -488,156 +488,345 @@ hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, cons
 
 // ------------------------------------------------------------------------------------
 // Decode attention: split-KV partials + merge.
+//
+// A decode step reads every cached key and value once and does ~7 flop per byte for a
+// 7-head GQA group, so it is bound by HBM bandwidth.  Each wave owns one 512-key chunk
+// of one (sequence, kv head) and streams it with no block barrier: LPK lanes hold one
+// key row (8 head dims each, one 16-byte load), KPW keys per pass, and an R-deep ring of
+// K/V loads stays in flight (16 KB per wave at 16-bit) while earlier passes are scored.
+// All G q heads of the group read the same loaded row.  Each group of LPK lanes keeps an
+// online softmax per head (log2 domain, running max raised only when a score exceeds it
+// by more than 2^8, so the rescale branch is rarely taken); the groups are merged with
+// lane shuffles and the wave writes (max, sum, o[D]) per head for the merge kernel.
 // ------------------------------------------------------------------------------------
-constexpr int DC_KEYS = 256;  // keys per chunk
-constexpr int DC_MAXG = 8;   // q heads per kv head (validated on the host)
+constexpr int DC_KEYS = 512;  // keys per chunk (one wave)
+constexpr int DC_MAXG = 8;    // q heads per kv head (validated on the host)
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_decode_attn_part(const T* __restrict__ q, int q_ld,
                                                           const T* __restrict__ ck, const T* __restrict__ cv,
                                                           const int32_t* __restrict__ kv_len, int cap,
-                                                          int max_pos, int Hq, int Hkv, float scale,
+                                                          int max_pos, int B, int Hq, int Hkv, float scale,
                                                           int nchunks, float* __restrict__ part) {
-  constexpr int LPK = D / 8;        // lanes per key row (8 head dims each, 16-byte loads)
-  constexpr int KPW = kWave / LPK;  // keys per wave pass
-  __shared__ float qs[DC_MAXG][D];
-  __shared__ float ps[DC_MAXG][DC_KEYS];
-  __shared__ float red[DC_MAXG][4];
-  __shared__ float osum[4][DC_MAXG][D];
-  const int c = blockIdx.x % nchunks;
-  const int bg = blockIdx.x / nchunks;
+  constexpr int LPK = D / 8;                  // lanes per key row
+  constexpr int KPW = kWave / LPK;            // keys per pass
+  constexpr int NPASS = DC_KEYS / KPW;        // passes per chunk
+  constexpr int R = sizeof(T) == 4 ? 4 : 8;   // passes in flight
+  static_assert(NPASS % R == 0, "ring");
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int c = wid % nchunks, bg = wid / nchunks;
+  if (bg >= B * Hkv) return;
   const int g = bg % Hkv, b = bg / Hkv;
   const int G = Hq / Hkv;
   const int n = min(max(kv_len[b], 0), min(cap, max_pos) - 1);  // new token slot; keys 0..n
   const int k_begin = c * DC_KEYS;
   const int nkeys = min(DC_KEYS, n + 1 - k_begin);
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   float* out = part + ((int64_t)(b * Hq + g * G) * nchunks + c) * (D + 2);
   const int64_t head_stride = (int64_t)nchunks * (D + 2);
   if (nkeys <= 0) {
-    if (tid < G) {
-      out[tid * head_stride] = -INFINITY;
-      out[tid * head_stride + 1] = 0.f;
+    if (lane < G) {
+      out[lane * head_stride] = -INFINITY;
+      out[lane * head_stride + 1] = 0.f;
     }
     return;
   }
-  for (int i = tid; i < G * D; i += 256)
-    qs[i / D][i % D] = ldf(q + (int64_t)b * q_ld + (g * G + i / D) * D + i % D);
-  __syncthreads();
-  const int64_t row_ld = (int64_t)Hkv * D;
-  const T* kbase = ck + ((int64_t)b * cap) * row_ld + g * D;
-  const T* vbase = cv + ((int64_t)b * cap) * row_ld + g * D;
   const int sub = lane % LPK, kk = lane / LPK;
+  const float c2 = scale * 1.4426950408889634f;  // scores in log2 units
+  float qr[DC_MAXG][8];
+#pragma unroll
+  for (int h = 0; h < DC_MAXG; ++h) {
+    if (h < G) {
+      float t[8];
+      const T* qp = q + (int64_t)b * q_ld + (g * G + h) * D + sub * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = ldf(qp + e);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qr[h][e] = t[e] * c2;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qr[h][e] = 0.f;
+    }
+  }
+  const int64_t row_ld = (int64_t)Hkv * D;
+  const T* kb = ck + ((int64_t)b * cap + k_begin) * row_ld + g * D + sub * 8;
+  const T* vb = cv + ((int64_t)b * cap + k_begin) * row_ld + g * D + sub * 8;
+  // rows past the chunk's last key re-read that key (in bounds) and are masked
+  auto row = [&](int p) -> int64_t { return (int64_t)min(p * KPW + kk, nkeys - 1) * row_ld; };
+  typename Raw8<T>::type kr[R], vr[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    kr[r] = ld_raw8(kb + row(r));
+    vr[r] = ld_raw8(vb + row(r));
+  }
+  float m[DC_MAXG], l[DC_MAXG], o[DC_MAXG][8];
+#pragma unroll
+  for (int h = 0; h < DC_MAXG; ++h) {
+    m[h] = -1e30f;
+    l[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+  }
+  const int npass = (nkeys + KPW - 1) / KPW;
+  for (int p0 = 0; p0 < npass; p0 += R) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int p = p0 + r;
+      if (p < npass) {
+        float kv[8];
+        unpack8(kr[r], kv);
+        if (p + R < NPASS) kr[r] = ld_raw8(kb + row(p + R));
+        const bool valid = p * KPW + kk < nkeys;
+        float sc[DC_MAXG];
+        bool raise = false;
+#pragma unroll
+        for (int h = 0; h < DC_MAXG; ++h) {
+          if (h < G) {
+            float a = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) a = fmaf(qr[h][e], kv[e], a);
+            a = LPK == 16 ? row16_sum(a) : oct8_sum(a);
+            sc[h] = valid ? a : -1e30f;
+            raise |= sc[h] > m[h] + 8.f;
+          }
+        }
+        if (__any(raise)) {
+#pragma unroll
+          for (int h = 0; h < DC_MAXG; ++h) {
+            if (h < G) {
+              const float mn = fmaxf(m[h], sc[h]);
+              const float al = __builtin_amdgcn_exp2f(m[h] - mn);
+              m[h] = mn;
+              l[h] *= al;
+#pragma unroll
+              for (int e = 0; e < 8; ++e) o[h][e] *= al;
+            }
+          }
+        }
+        float vv[8];
+        unpack8(vr[r], vv);
+        if (p + R < NPASS) vr[r] = ld_raw8(vb + row(p + R));
+#pragma unroll
+        for (int h = 0; h < DC_MAXG; ++h) {
+          if (h < G) {
+            const float pk = __builtin_amdgcn_exp2f(sc[h] - m[h]);
+            l[h] += pk;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[h][e] = fmaf(pk, vv[e], o[h][e]);
+          }
+        }
+      }
+    }
+  }
+  // merge the KPW key groups of the wave, then write (max in natural-log units, sum, o)
+#pragma unroll
+  for (int h = 0; h < DC_MAXG; ++h) {
+    if (h < G) {
+      float M = m[h];
+#pragma unroll
+      for (int off = LPK; off < kWave; off <<= 1) M = fmaxf(M, __shfl_xor(M, off, kWave));
+      const float f = __builtin_amdgcn_exp2f(m[h] - M);
+      float L = l[h] * f;
+#pragma unroll
+      for (int off = LPK; off < kWave; off <<= 1) L += __shfl_xor(L, off, kWave);
+      float ov[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float a = o[h][e] * f;
+#pragma unroll
+        for (int off = LPK; off < kWave; off <<= 1) a += __shfl_xor(a, off, kWave);
+        ov[e] = a;
+      }
+      float* oh = out + h * head_stride;
+      if (lane == 0) {
+        oh[0] = M * 0.6931471805599453f;
+        oh[1] = L;
+      }
+      if (kk == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) oh[2 + sub * 8 + e] = ov[e];
+      }
+    }
+  }
+}
 
-  // ---- scores: LPK lanes per key row, partial dots reduced across them.  All of this
-  // lane's K loads for the chunk are issued before any is consumed (memory-level
-  // parallelism: a decode step is bound by HBM bandwidth) ----
-  constexpr int NP = DC_KEYS / (4 * KPW);  // passes over the chunk
-  {
-    float qreg[DC_MAXG][8];
-#pragma unroll
-    for (int hg = 0; hg < DC_MAXG; ++hg)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qreg[hg][e] = hg < G ? qs[hg][sub * 8 + e] : 0.f;
-    typename Raw8<T>::type kr[NP];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const int key = w * KPW + kk + p * 4 * KPW;
-      kr[p] = key < nkeys ? ld_raw8(kbase + (int64_t)(k_begin + key) * row_ld + sub * 8)
-                          : typename Raw8<T>::type{};
+// 16-bit models: the same split-KV chunks on the matrix cores.  One wave owns one chunk
+// of one (sequence, kv head); the G q heads of the group are the query columns of the
+// prefix kernel's tile (S^T = K Q^T with v_mfma_f32_32x32x16, the scores reused as the
+// B operand of O^T += V^T P^T, V^T read with ds_read_b64_tr_b16; columns >= G are
+// zero and ignored).  32-key K and V tiles stream into a 3-stage per-wave LDS ring by
+// direct global->LDS loads through a buffer resource whose extent ends at the
+// sequence's last key, so rows past it read as zeros; the wave needs no barrier: the
+// compiler waits on the loads that filled a stage before reading it, and a stage is
+// refilled only after the MFMAs that consumed it.
+template <typename T16, int D>
+__global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__ q, int q_ld,
+                                                         const T16* __restrict__ ck, const T16* __restrict__ cv,
+                                                         const int32_t* __restrict__ kv_len, int cap, int max_pos,
+                                                         int B, int Hq, int Hkv, float scale, int nchunks,
+                                                         float* __restrict__ part) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef Half16<T16> H;
+  typedef typename H::V8 V8;
+  constexpr int KT = 32;                 // keys per tile
+  constexpr int NT = DC_KEYS / KT;       // tiles per chunk
+  constexpr int CH = D / 8;              // 16-byte chunks per row
+  constexpr int KSTEPS = D / 16;
+  constexpr int DB = D / 32;
+  constexpr int LOADS = (KT * CH) / 64;  // load instructions per matrix per tile
+  static_assert(NT % 3 == 0 || NT > 3, "ring");
+  __shared__ u32x4_t Ks0[KT * CH], Ks1[KT * CH], Ks2[KT * CH], Vs0[KT * CH], Vs1[KT * CH], Vs2[KT * CH];
+  const int lane = threadIdx.x;
+  const int c = blockIdx.x % nchunks, bg = blockIdx.x / nchunks;
+  const int g = bg % Hkv, b = bg / Hkv;
+  const int G = Hq / Hkv;
+  const int n = min(max(kv_len[b], 0), min(cap, max_pos) - 1);  // keys 0..n
+  const int k_begin = c * DC_KEYS;
+  const int nkeys = min(DC_KEYS, n + 1 - k_begin);
+  float* out = part + ((int64_t)(b * Hq + g * G) * nchunks + c) * (D + 2);
+  const int64_t head_stride = (int64_t)nchunks * (D + 2);
+  if (nkeys <= 0) {
+    if (lane < G) {
+      out[lane * head_stride] = -INFINITY;
+      out[lane * head_stride + 1] = 0.f;
     }
+    return;
+  }
+  const int ntiles = (nkeys + KT - 1) / KT;
+  // keys of this chunk as a buffer resource: rows k_begin .. n of (b, g); byte offsets
+  // key * row_bytes fit 32 bits (cap * Hkv * D * 2 bytes is checked on the host)
+  const uint32_t row_bytes = (uint32_t)Hkv * D * sizeof(T16);
+  const uint32_t ext = (uint32_t)(nkeys - 1) * row_bytes + D * sizeof(T16);
+  const int64_t e0 = ((int64_t)b * cap + k_begin) * Hkv * D + (int64_t)g * D;
+  const __amdgpu_buffer_rsrc_t rsK =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr((void*)(ck + e0)), 0, (int)ext, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsV =
+      __builtin_amdgcn_make_buffer_rsrc(uniform_ptr((void*)(cv + e0)), 0, (int)ext, 0x00020000);
+  uint32_t koff[LOADS], voff[LOADS];
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const int key = w * KPW + kk + p * 4 * KPW;
-      float kv8[8];
-      unpack8(kr[p], kv8);
+  for (int j = 0; j < LOADS; ++j) {
+    const int slot = j * 64 + lane, key = slot / CH, cp = slot % CH;
+    koff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ kswz<D>(key)) * 16);
+    voff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ vswz(key)) * 16);
+  }
+#define DM_LOAD(KD_, VD_, t_)                                                                                \
+  _Pragma("unroll") for (int j = 0; j < LOADS; ++j) {                                                       \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsK, (lds_void_t*)((KD_) + j * 64), 16, koff[j] + (uint32_t)(t_) * KT * row_bytes, 0, 0, 0); \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsV, (lds_void_t*)((VD_) + j * 64), 16, voff[j] + (uint32_t)(t_) * KT * row_bytes, 0, 0, 0); \
+  }
+  // query columns: lane column fr is q head g*G + fr (zero beyond G)
+  const int fr = lane & 31, fk = lane >> 5;
+  V8 qf[KSTEPS];
 #pragma unroll
-      for (int hg = 0; hg < DC_MAXG; ++hg) {
-        if (hg < G) {
-          float a = 0.f;
+  for (int ks = 0; ks < KSTEPS; ++ks) {
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (fr < G) v = *reinterpret_cast<const uint4*>(q + (int64_t)b * q_ld + (g * G + fr) * D + ks * 16 + fk * 8);
+    qf[ks] = H::as_v8(v);
+  }
+  f32x16_t o[DB];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) a = fmaf(qreg[hg][e], kv8[e], a);
-          a = LPK == 16 ? row16_sum(a) : oct8_sum(a);
-          if (sub == 0 && key < nkeys) ps[hg][key] = a * scale;
-        }
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[db][e] = 0.f;
+  float m_run = kMaskVal, l_run = 0.f;
+  const float c2 = scale * 1.4426950408889634f;
+  const int tr_p = lane & 15;
+  const int tr_key = fk * 4 + (tr_p >> 2);
+  const int tr_col = ((lane & 16) ? 16 : 0) + 4 * (tr_p & 3);
+
+  auto tile = [&](const u32x4_t* Kc, const u32x4_t* Vc, int t) __attribute__((always_inline)) {
+    f32x16_t sc;
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const V8 kf = __builtin_bit_cast(V8, Kc[fr * CH + ((ks * 2 + fk) ^ kswz<D>(fr))]);
+      sc = H::mma(kf, qf[ks], ks == 0 ? f32x16_t{} : sc);
+    }
+    // sc[e] = score(key t*KT + 8(e/4) + 4 fk + e%4, head fr)
+    const int lim = nkeys - 1 - t * KT - 4 * fk;
+    if (t * KT + KT > nkeys) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (8 * (e >> 2) + (e & 3) > lim) sc[e] = kMaskVal;
+    }
+    float mx = kMaskVal;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * c2;
+    if (__any(mx > m_run + kLazy)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
+    }
+    const float nm = -m_run;
+    float ls = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float pv = __builtin_amdgcn_exp2f(fmaf(sc[e], c2, nm));
+      sc[e] = pv;
+      ls += pv;
+    }
+    l_run += ls;
+    const T16* vbase = reinterpret_cast<const T16*>(Vc);
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const V8 pf = H::as_v8(make_uint4(H::pack2(sc[hh * 8 + 0], sc[hh * 8 + 1]), H::pack2(sc[hh * 8 + 2], sc[hh * 8 + 3]),
+                                        H::pack2(sc[hh * 8 + 4], sc[hh * 8 + 5]), H::pack2(sc[hh * 8 + 6], sc[hh * 8 + 7])));
+      const int ka = hh * 16 + tr_key, kc = ka + 8;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int col = db * 32 + tr_col;
+        const int ca = ((col >> 3) ^ vswz(ka)) * 8 + (col & 7);
+        const int cc = ((col >> 3) ^ vswz(kc)) * 8 + (col & 7);
+        const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + ka * D + ca));
+        const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + kc * D + cc));
+        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        o[db] = H::mma(H::as_v8(make_uint4(l2.x, l2.y, h2.x, h2.y)), pf, o[db]);
       }
     }
-  }
-  // V loads for the chunk go out now, to land while the softmax runs
-  typename Raw8<T>::type vr[NP];
-#pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const int key = w * KPW + kk + p * 4 * KPW;
-    vr[p] = key < nkeys ? ld_raw8(vbase + (int64_t)(k_begin + key) * row_ld + sub * 8)
-                        : typename Raw8<T>::type{};
-  }
-  __syncthreads();
-  // ---- per-head max, exp, sum over the chunk (thread = key) ----
-  for (int hg = 0; hg < G; ++hg) {
-    const float mx = wave_max(tid < nkeys ? ps[hg][tid] : -INFINITY);
-    if (lane == 0) red[hg][w] = mx;
-  }
-  __syncthreads();
-  float mxs[DC_MAXG];
-#pragma unroll
-  for (int hg = 0; hg < DC_MAXG; ++hg)
-    mxs[hg] = hg < G ? fmaxf(fmaxf(red[hg][0], red[hg][1]), fmaxf(red[hg][2], red[hg][3])) : 0.f;
-  __syncthreads();  // everyone has read red[] before it is reused for the sums
-  for (int hg = 0; hg < G; ++hg) {
-    float p = 0.f;
-    if (tid < nkeys) {
-      p = expf(ps[hg][tid] - mxs[hg]);
-      ps[hg][tid] = p;
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // tile t reads stage t % 3; after it, the stage is refilled with tile t + 3 (tiles past
+  // the chunk's last key read as zeros and are never used)
+  DM_LOAD(Ks0, Vs0, 0);
+  DM_LOAD(Ks1, Vs1, 1);
+  DM_LOAD(Ks2, Vs2, 2);
+  for (int t = 0; t < ntiles; t += 3) {
+    tile(Ks0, Vs0, t);
+    if (t + 3 < ntiles) { DM_LOAD(Ks0, Vs0, t + 3); }
+    if (t + 1 < ntiles) {
+      tile(Ks1, Vs1, t + 1);
+      if (t + 4 < ntiles) { DM_LOAD(Ks1, Vs1, t + 4); }
     }
-    p = wave_sum(p);
-    if (lane == 0) red[hg][w] = p;
+    if (t + 2 < ntiles) {
+      tile(Ks2, Vs2, t + 2);
+      if (t + 5 < ntiles) { DM_LOAD(Ks2, Vs2, t + 5); }
+    }
   }
-  __syncthreads();
-  // ---- o[hg][d] = sum_k p[hg][k] v[k][d]: LPK lanes per V row, KPW key groups per wave ----
-  {
-    float acc[DC_MAXG][8];
+#undef DM_LOAD
+  __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the wave
+  // o[db][e] = O^T(dim db*32 + 8(e/4) + 4 fk + e%4, head fr), unnormalised
+  const float l = l_run + __shfl_xor(l_run, 32, kWave);
+  if (fr < G) {
+    float* oh = out + fr * head_stride;
+    if (fk == 0) {
+      oh[0] = m_run * 0.6931471805599453f;
+      oh[1] = l;
+    }
 #pragma unroll
-    for (int hg = 0; hg < DC_MAXG; ++hg)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[hg][e] = 0.f;
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const int k = w * KPW + kk + p * 4 * KPW;
-      float v8[8];
-      unpack8(vr[p], v8);
-      const int kc = min(k, DC_KEYS - 1);  // rows beyond nkeys hold zeros
-#pragma unroll
-      for (int hg = 0; hg < DC_MAXG; ++hg) {
-        if (hg < G) {
-          const float pk = k < nkeys ? ps[hg][kc] : 0.f;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[hg][e] = fmaf(pk, v8[e], acc[hg][e]);
-        }
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int dh = db * 32 + 8 * e4 + 4 * fk;
+        *reinterpret_cast<float4*>(oh + 2 + dh) =
+            make_float4(o[db][4 * e4], o[db][4 * e4 + 1], o[db][4 * e4 + 2], o[db][4 * e4 + 3]);
       }
-    }
-    // reduce the KPW key groups of the wave (lanes with equal sub), then the 4 waves
-#pragma unroll
-    for (int hg = 0; hg < DC_MAXG; ++hg) {
-      if (hg < G) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          float a = acc[hg][e];
-#pragma unroll
-          for (int o = LPK; o < kWave; o <<= 1) a += __shfl_xor(a, o, kWave);
-          if (kk == 0) osum[w][hg][sub * 8 + e] = a;
-        }
-      }
-    }
   }
-  __syncthreads();
-  for (int hg = 0; hg < G; ++hg) {
-    float* o = out + hg * head_stride;
-    if (tid == 0) {
-      o[0] = mxs[hg];
-      o[1] = red[hg][0] + red[hg][1] + red[hg][2] + red[hg][3];
-    }
-    if (tid < D) o[2 + tid] = osum[0][hg][tid] + osum[1][hg][tid] + osum[2][hg][tid] + osum[3][hg][tid];
-  }
+#endif
 }
 
 template <typename T, int D>
@@ -668,17 +857,39 @@ hipError_t launch_decode_attention(hipStream_t s, rp_dtype dt, const void* q, in
                                    int32_t cap, int32_t max_pos, int32_t B, int32_t Hq, int32_t Hkv,
                                    int32_t D, float scale, float* partials, void* o) {
   const int nchunks = (cap + DC_KEYS - 1) / DC_KEYS;
-  const int grid = B * Hkv * nchunks;
-#define RP_DEC(T, DD)                                                                            \
-  k_decode_attn_part<T, DD><<<grid, 256, 0, s>>>((const T*)q, q_ld, (const T*)cache_k,         \
-                                                 (const T*)cache_v, kv_len, cap, max_pos, Hq, Hkv, \
-                                                 scale, nchunks, partials);                    \
-  k_decode_attn_merge<T, DD><<<B * Hq, DD, 0, s>>>(partials, nchunks, Hq, (T*)o);
-  with_storage(dt, [&](auto tag_) {
-    using E = decltype(tag_);
-    if (D == 128) { RP_DEC(E, 128) } else { RP_DEC(E, 64) }
+  if (dt == RP_F32) {
+    const int grid = (B * Hkv * nchunks + 3) / 4;  // one wave per chunk, 4 waves per workgroup
+    if (D == 128)
+      k_decode_attn_part<float, 128><<<grid, 256, 0, s>>>((const float*)q, q_ld, (const float*)cache_k,
+                                                          (const float*)cache_v, kv_len, cap, max_pos, B, Hq, Hkv,
+                                                          scale, nchunks, partials);
+    else
+      k_decode_attn_part<float, 64><<<grid, 256, 0, s>>>((const float*)q, q_ld, (const float*)cache_k,
+                                                         (const float*)cache_v, kv_len, cap, max_pos, B, Hq, Hkv,
+                                                         scale, nchunks, partials);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (D == 128)
+      k_decode_attn_merge<float, 128><<<B * Hq, 128, 0, s>>>(partials, nchunks, Hq, (float*)o);
+    else
+      k_decode_attn_merge<float, 64><<<B * Hq, 64, 0, s>>>(partials, nchunks, Hq, (float*)o);
+    return hipGetLastError();
+  }
+  // the 16-bit kernel addresses a sequence's cache rows with 32-bit byte offsets
+  if ((int64_t)cap * Hkv * D * 2 > (int64_t)INT32_MAX) return hipErrorInvalidValue;
+  const int grid = B * Hkv * nchunks;  // one wave per chunk
+  with_half16(dt, [&](auto tag_) {
+    using H = decltype(tag_);
+    if (D == 128) {
+      k_decode_attn_mfma<H, 128><<<grid, 64, 0, s>>>((const H*)q, q_ld, (const H*)cache_k, (const H*)cache_v, kv_len,
+                                                    cap, max_pos, B, Hq, Hkv, scale, nchunks, partials);
+      k_decode_attn_merge<H, 128><<<B * Hq, 128, 0, s>>>(partials, nchunks, Hq, (H*)o);
+    } else {
+      k_decode_attn_mfma<H, 64><<<grid, 64, 0, s>>>((const H*)q, q_ld, (const H*)cache_k, (const H*)cache_v, kv_len,
+                                                   cap, max_pos, B, Hq, Hkv, scale, nchunks, partials);
+      k_decode_attn_merge<H, 64><<<B * Hq, 64, 0, s>>>(partials, nchunks, Hq, (H*)o);
+    }
   });
-#undef RP_DEC
   return hipGetLastError();
 }
 

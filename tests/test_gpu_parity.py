@@ -98,13 +98,18 @@ def test_packing_is_bitwise_invariant(model):
         assert np.array_equal(lp[cs[b]:cs[b + 1]], lp1)
 
 
-@pytest.mark.parametrize("model", [BF16_SMALL, configs.TINY, F16_SMALL])
-def test_decode_step_matches_oracle(model):
+@pytest.mark.parametrize("model,cap,lens", [(BF16_SMALL, 300, [0, 1, 63, 256, 299]),
+                                            (configs.TINY, 300, [0, 1, 63, 256, 299]),
+                                            (F16_SMALL, 300, [0, 1, 63, 256, 299]),
+                                            # several 512-key chunks per sequence, chunk edges
+                                            (BF16_SMALL, 1100, [511, 512, 1023, 700, 1099]),
+                                            (configs.TINY, 1100, [0, 513, 1024, 1099, 5])])
+def test_decode_step_matches_oracle(model, cap, lens):
     from paper_2608_14498_amd.runtime import DeviceModel, to_device
     w = configs.custom(model, [1], [0], [1], index=53)
     hw = inputs.make_weights(w, norm="random", bias=True)
-    B, cap = 5, 300
-    kv_len = np.array([0, 1, 63, 256, 299], np.int32)
+    B = len(lens)
+    kv_len = np.array(lens, np.int32)
     dec = inputs.make_decode(w, batch=B, kv_len=kv_len, cap=cap)
     dm = DeviceModel(hw, cap + 1)
     ck, cv = to_device(dec.cache_k, dm.device), to_device(dec.cache_v, dm.device)
