@@ -163,6 +163,33 @@ rp_status rp_suffix_logprob(const rp_model *model, void *stream, int32_t B,
                             void *workspace, size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
+ * Shared-prefix suffix pass (Section "Prefix Sharing": the N sampled responses
+ * of a GRPO prompt group share one video-text prefix, whose prefix pass runs
+ * once per group and is reused by every response).  n_suffix sequences score
+ * against n_prefix prefixes: sequence s reads prefix p = prefix_of_suffix[s]
+ * (host int32 [n_suffix], each in [0, n_prefix)), i.e. KV rows
+ * prefix_cu[p] .. prefix_cu[p+1]-1 of kv (read only) and h_last[p]
+ * (fp32 [n_prefix, d], 16-byte aligned).  Its response occupies rows
+ * suffix_cu[s] .. suffix_cu[s+1]-1 of response_ids / logprobs at positions
+ * P_p + j; logprobs[suffix_cu[s]+j] = log p(r_s,j | prefix_p, r_s,<j) exactly
+ * as in rp_suffix_logprob, which is this call with prefix_of_suffix[s] = s.
+ * Any prefix may serve any number of suffixes (also none).  n_prefix and
+ * n_suffix are in [1, RP_MAX_SEQS]; P_p >= 1, S_s >= 0 and
+ * P_p + S_s <= max_position, else RP_ERR_SHAPE; a prefix index out of range
+ * is RP_ERR_SHAPE.  Ownership, asynchrony and workspace rules as above.
+ * ------------------------------------------------------------------------- */
+rp_status rp_suffix_grouped_workspace_bytes(const rp_model *model, int32_t n_prefix,
+                                            const int32_t *prefix_cu_host, int32_t n_suffix,
+                                            const int32_t *prefix_of_suffix_host,
+                                            const int32_t *suffix_cu_host, size_t *bytes);
+rp_status rp_suffix_logprob_grouped(const rp_model *model, void *stream, int32_t n_prefix,
+                                    const int32_t *prefix_cu_host, int32_t n_suffix,
+                                    const int32_t *prefix_of_suffix_host,
+                                    const int32_t *suffix_cu_host, rp_kv kv, const float *h_last,
+                                    const int32_t *response_ids, float *logprobs, void *workspace,
+                                    size_t workspace_bytes);
+
+/* ---------------------------------------------------------------------------
  * Rollout decode step (the memory-bound phase that the prefix pass overlaps
  * with; Section "Observation and Opportunity" and Eq. (1)).  One new token
  * per sequence: token_ids[b] runs at position kv_len[b], its K/V are written

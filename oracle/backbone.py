@@ -264,6 +264,21 @@ def suffix_logprob(weights, cfg, cu_prefix, cu_suffix, K, V, h_last, response_id
     return out
 
 
+def suffix_logprob_grouped(weights, cfg, cu_prefix, prefix_of_suffix, cu_suffix, K, V, h_last, response_ids):
+    """Shared-prefix suffix pass (Section "Prefix Sharing": the responses of a GRPO group
+    reuse their group's one prefix pass).  Suffix s is scored against prefix
+    prefix_of_suffix[s]: its KV rows and its boundary state.  Returns logprobs [R]."""
+    cp, cs = np.asarray(cu_prefix), np.asarray(cu_suffix)
+    grp = np.asarray(prefix_of_suffix)
+    out = np.empty(int(cs[-1]))
+    rid = np.asarray(response_ids)
+    for s in range(len(cs) - 1):
+        p = int(grp[s])
+        out[cs[s]:cs[s + 1]] = suffix_logprob_one(
+            weights, cfg, K[:, cp[p]:cp[p + 1]], V[:, cp[p]:cp[p + 1]], h_last[p], rid[cs[s]:cs[s + 1]])
+    return out
+
+
 def unsplit_logprob(weights, cfg, cu_prefix, cu_suffix, token_ids, visual, response_ids):
     cp, cs = np.asarray(cu_prefix), np.asarray(cu_suffix)
     B = len(cp) - 1

@@ -176,14 +176,38 @@ rp_status check_suffix_cu(const rp_model* m, int32_t B, const int32_t* pcu, cons
   return RP_OK;
 }
 
-rp::SeqTable make_table(int32_t B, const int32_t* q_cu, const int32_t* k_cu) {
+// Sequence table: query rows q_cu[0..B]; the key segment of sequence b is prefix grp[b]
+// (b when grp is NULL) of the n_k prefixes k_cu[0..n_k] (none when k_cu is NULL).
+// Shared-prefix suffixes: n_suffix sequences, sequence s scores against prefix
+// prefix_of_suffix[s] of the n_prefix prefixes.
+rp_status check_grouped_cu(const rp_model* m, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
+                           const int32_t* grp, const int32_t* scu) {
+  rp_status st = check_prefix_cu(m, n_prefix, pcu, "prefix_cu");
+  if (st != RP_OK) return st;
+  if (n_suffix < 1 || n_suffix > RP_MAX_SEQS)
+    return fail(RP_ERR_SHAPE, "suffix count %d outside [1, %d]", n_suffix, RP_MAX_SEQS);
+  if (!grp || !scu) return fail(RP_ERR_INVALID_ARG, "prefix_of_suffix and suffix_cu are required");
+  if (scu[0] != 0) return fail(RP_ERR_SHAPE, "suffix_cu[0] must be 0");
+  for (int s = 0; s < n_suffix; ++s) {
+    if (grp[s] < 0 || grp[s] >= n_prefix)
+      return fail(RP_ERR_SHAPE, "prefix_of_suffix[%d] = %d outside [0, %d)", s, grp[s], n_prefix);
+    const int64_t S = (int64_t)scu[s + 1] - scu[s];
+    if (S < 0) return fail(RP_ERR_SHAPE, "suffix sequence %d has negative length %lld", s, (long long)S);
+    const int64_t last = (int64_t)(pcu[grp[s] + 1] - pcu[grp[s]]) + S;
+    if (last > m->cfg.max_position)
+      return fail(RP_ERR_SHAPE, "suffix %d: prefix + suffix = %lld exceeds max_position %d", s, (long long)last,
+                  m->cfg.max_position);
+  }
+  return RP_OK;
+}
+
+rp::SeqTable make_table(int32_t B, const int32_t* q_cu, int32_t n_k, const int32_t* k_cu, const int32_t* grp) {
   rp::SeqTable t;
   memset(&t, 0, sizeof t);
   t.n = B;
-  for (int b = 0; b <= B; ++b) {
-    t.q_cu[b] = q_cu[b];
-    t.k_cu[b] = k_cu ? k_cu[b] : 0;
-  }
+  for (int b = 0; b <= B; ++b) t.q_cu[b] = q_cu[b];
+  for (int p = 0; p <= n_k && k_cu; ++p) t.k_cu[p] = k_cu[p];
+  for (int b = 0; b < B; ++b) t.grp[b] = grp ? grp[b] : b;
   return t;
 }
 
@@ -371,6 +395,44 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   return RP_OK;
 }
 
+// Suffix pass over n_suffix sequences; sequence s reads prefix grp[s] (s when grp is
+// NULL) of the n_prefix prefixes: its KV rows pcu[grp[s]].. and boundary state
+// h_last[grp[s]].  Lengths were validated by the caller.
+rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
+                     const int32_t* grp, const int32_t* scu, rp_kv kv, const float* h_last,
+                     const int32_t* response_ids, float* logprobs, void* ws, size_t ws_bytes) {
+  const int64_t T = pcu[n_prefix], R = scu[n_suffix];
+  rp_status st;
+  if ((st = check_kv(m, kv, T, "kv")) != RP_OK) return st;
+  if (!h_last) return fail(RP_ERR_INVALID_ARG, "h_last is NULL");
+  if (!aligned16(h_last)) return fail(RP_ERR_INVALID_ARG, "h_last must be 16-byte aligned");
+  if (R > 0 && (!response_ids || !logprobs)) return fail(RP_ERR_INVALID_ARG, "response_ids and logprobs are required");
+  const size_t need = suffix_ws(m, R, nullptr, nullptr);
+  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
+  if (R == 0) return RP_OK;
+
+  hipStream_t s = (hipStream_t)stream;
+  const rp_config& c = m->cfg;
+  const rp_dtype dt = c.dtype;
+  SuffixWS w;
+  suffix_ws(m, R, ws, &w);
+  const rp::SeqTable tab = make_table(n_suffix, scu, n_prefix, pcu, grp);
+  RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, dt, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const void* kl = layer_ptr(m, kv.k, kv.layer_stride, l);
+    const void* vl = layer_ptr(m, kv.v, kv.layer_stride, l);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, w.plan, w.gemm_part, kSuffixNames);
+    if (st != RP_OK) return st;
+  }
+  RP_TRY_LAUNCH_N("suffix.final_norm", rp::launch_final_norm_rows(s, dt, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
+                                           c.d_model, w.L.N));
+  rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
+  RP_TRY_LAUNCH_N("suffix.gemm_lm_head", rp::launch_gemm(s, dt, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
+                                c.vocab, rp::EPI_STORE_F32, 1, nullptr));
+  RP_TRY_LAUNCH_N("suffix.logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
+  return RP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -455,7 +517,7 @@ rp_status rp_prefix_forward(const rp_model* m, void* stream, int32_t B, const in
   int32_t* vis_idx = nullptr;
   prefix_ws(m, T, ws, hidden_out == nullptr, &w, &vis_idx);
   if (hidden_out) w.X = hidden_out;
-  const rp::SeqTable tab = make_table(B, cu, nullptr);
+  const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
   const LayerPlan plan = plan_layer(c, (int32_t)T, Pass::kPrefix);
 
   RP_TRY_LAUNCH_N("prefix.visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
@@ -486,35 +548,27 @@ rp_status rp_suffix_logprob(const rp_model* m, void* stream, int32_t B, const in
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
   rp_status st = check_suffix_cu(m, B, pcu, scu);
   if (st != RP_OK) return st;
-  const int64_t T = pcu[B], R = scu[B];
-  if ((st = check_kv(m, kv, T, "kv")) != RP_OK) return st;
-  if (!h_last) return fail(RP_ERR_INVALID_ARG, "h_last is NULL");
-  if (!aligned16(h_last)) return fail(RP_ERR_INVALID_ARG, "h_last must be 16-byte aligned");
-  if (R > 0 && (!response_ids || !logprobs)) return fail(RP_ERR_INVALID_ARG, "response_ids and logprobs are required");
-  const size_t need = suffix_ws(m, R, nullptr, nullptr);
-  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
-  if (R == 0) return RP_OK;
+  return suffix_run(m, stream, B, pcu, B, nullptr, scu, kv, h_last, response_ids, logprobs, ws, ws_bytes);
+}
 
-  hipStream_t s = (hipStream_t)stream;
-  const rp_config& c = m->cfg;
-  const rp_dtype dt = c.dtype;
-  SuffixWS w;
-  suffix_ws(m, R, ws, &w);
-  const rp::SeqTable tab = make_table(B, scu, pcu);
-  RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, dt, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
-  for (int l = 0; l < c.n_layers; ++l) {
-    const void* kl = layer_ptr(m, kv.k, kv.layer_stride, l);
-    const void* vl = layer_ptr(m, kv.v, kv.layer_stride, l);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, w.plan, w.gemm_part, kSuffixNames);
-    if (st != RP_OK) return st;
-  }
-  RP_TRY_LAUNCH_N("suffix.final_norm", rp::launch_final_norm_rows(s, dt, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
-                                           c.d_model, w.L.N));
-  rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
-  RP_TRY_LAUNCH_N("suffix.gemm_lm_head", rp::launch_gemm(s, dt, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
-                                c.vocab, rp::EPI_STORE_F32, 1, nullptr));
-  RP_TRY_LAUNCH_N("suffix.logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
+rp_status rp_suffix_grouped_workspace_bytes(const rp_model* m, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
+                                            const int32_t* prefix_of_suffix, const int32_t* scu, size_t* bytes) {
+  if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
+  rp_status s = check_grouped_cu(m, n_prefix, pcu, n_suffix, prefix_of_suffix, scu);
+  if (s != RP_OK) return s;
+  *bytes = suffix_ws(m, scu[n_suffix], nullptr, nullptr);
   return RP_OK;
+}
+
+rp_status rp_suffix_logprob_grouped(const rp_model* m, void* stream, int32_t n_prefix, const int32_t* pcu,
+                                    int32_t n_suffix, const int32_t* prefix_of_suffix, const int32_t* scu, rp_kv kv,
+                                    const float* h_last, const int32_t* response_ids, float* logprobs, void* ws,
+                                    size_t ws_bytes) {
+  if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  rp_status st = check_grouped_cu(m, n_prefix, pcu, n_suffix, prefix_of_suffix, scu);
+  if (st != RP_OK) return st;
+  return suffix_run(m, stream, n_prefix, pcu, n_suffix, prefix_of_suffix, scu, kv, h_last, response_ids, logprobs, ws,
+                    ws_bytes);
 }
 
 rp_status rp_decode_workspace_bytes(const rp_model* m, int32_t B, int32_t cap, size_t* bytes) {

@@ -152,8 +152,8 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   qb.q_begin = __builtin_amdgcn_readfirstlane(qb.q_begin);
   qb.q_end = __builtin_amdgcn_readfirstlane(qb.q_end);
   const int G = a.Hq / a.Hkv, g = h / G;
-  const int krow0 = __builtin_amdgcn_readfirstlane(st.k_cu[b]);
-  const int n0 = __builtin_amdgcn_readfirstlane(st.k_cu[b + 1]) - krow0;
+  const int krow0 = __builtin_amdgcn_readfirstlane(st.k_beg(b));
+  const int n0 = __builtin_amdgcn_readfirstlane(st.pos0(b));
   const int qrow0 = __builtin_amdgcn_readfirstlane(st.q_cu[b]);
   const int nq = __builtin_amdgcn_readfirstlane(st.q_cu[b + 1]) - qrow0;
   const int qpos_first = n0 + (qb.q_begin - qrow0);
@@ -396,7 +396,7 @@ __global__ __launch_bounds__(64) void k_attn_f32(SeqTable st, AttnArgs a) {
   const int b = qb.b;
   const int g = h / (a.Hq / a.Hkv);
   const int n0 = st.pos0(b);
-  const int qrow0 = st.q_cu[b], krow0 = st.k_cu[b];
+  const int qrow0 = st.q_cu[b], krow0 = st.k_beg(b);
   const int qrow_raw = qb.q_begin + threadIdx.x;
   const int qrow = min(qrow_raw, qb.q_end - 1);
   const int qpos = n0 + (qrow_raw - qrow0);

@@ -147,7 +147,7 @@ __global__ __launch_bounds__(256) void k_final_norm_rows(SeqTable st, const floa
   __shared__ float red[16];
   const int r = blockIdx.x;
   const int b = seq_of_row(st, r);
-  const float* src = (r == st.q_cu[b]) ? h_last + (int64_t)b * d : Y + (int64_t)(r - 1) * d;
+  const float* src = (r == st.q_cu[b]) ? h_last + (int64_t)st.grp[b] * d : Y + (int64_t)(r - 1) * d;
   rmsnorm_row(src, w, eps, d, out + (int64_t)r * d, red);
 }
 

@@ -15,8 +15,12 @@ namespace rp {
 struct SeqTable {
   int32_t n;                       // sequences
   int32_t q_cu[RP_MAX_SEQS + 1];   // query rows of sequence b: q_cu[b] .. q_cu[b+1]-1
-  int32_t k_cu[RP_MAX_SEQS + 1];   // rows of the first key segment (prefix KV) of sequence b
-  __host__ __device__ int32_t pos0(int b) const { return k_cu[b + 1] - k_cu[b]; }
+  int32_t k_cu[RP_MAX_SEQS + 1];   // prefix p's KV rows: k_cu[p] .. k_cu[p+1]-1
+  int32_t grp[RP_MAX_SEQS];        // prefix of sequence b (b itself unless prefixes are shared)
+  // first row and length of sequence b's first key segment; the length is also the
+  // position of b's first query row
+  __host__ __device__ int32_t k_beg(int b) const { return k_cu[grp[b]]; }
+  __host__ __device__ int32_t pos0(int b) const { return k_cu[grp[b] + 1] - k_cu[grp[b]]; }
 };
 
 // Row r of the packed queries -> sequence index (binary search over q_cu).
@@ -57,7 +61,8 @@ hipError_t launch_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const in
 hipError_t launch_rmsnorm(hipStream_t s, rp_dtype dt, const float* X, const void* w, float eps, int32_t M,
                           int32_t d, void* out);
 // Final norm of the suffix rows with boundary assembly: row r of sequence b reads
-// h_last[b] if it is the sequence's first response row, else Y[r-1].
+// h_last[grp[b]] (its prefix's boundary state) if it is the sequence's first response
+// row, else Y[r-1].
 hipError_t launch_final_norm_rows(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* Y,
                                   const float* h_last, const void* w, float eps, int32_t R, int32_t d,
                                   void* out);
@@ -82,9 +87,9 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
 size_t gemm_partial_floats(int32_t M, int32_t N, int32_t splitk);
 
 // Attention over packed sequences.  Queries: rows st.q_cu[b].. of q (row stride q_ld,
-// head h at column h*D), positions st.pos0(b) + i.  Keys: segment 0 = rows st.k_cu[b]..
-// (st.k_cu[b+1]-st.k_cu[b] rows, positions 0..) of k0/v0; segment 1 = the query rows
-// themselves of k1/v1 (positions st.pos0(b)+j).  Key visible iff key pos <= query pos.
+// head h at column h*D), positions st.pos0(b) + i.  Keys: segment 0 = rows st.k_beg(b)..
+// (st.pos0(b) rows, positions 0..) of k0/v0, the KV of b's prefix; segment 1 = the query
+// rows themselves of k1/v1 (positions st.pos0(b)+j).  Key visible iff key pos <= query pos.
 // k/v rows are [Hkv][D] contiguous.  Output o rows [Hq*D].
 struct AttnArgs {
   const void* q;

@@ -104,6 +104,19 @@ class DeviceModel:
                              rb.make_kv(K, V, K[0].numel()), h_last, response_ids, logprobs, ws, ws.numel())
         return logprobs
 
+    def suffix_grouped(self, prefix_cu, prefix_of_suffix, suffix_cu, K, V, h_last, response_ids, logprobs=None,
+                       workspace=None, stream=None):
+        """Suffix pass where suffix s reads prefix prefix_of_suffix[s] (shared prefixes)."""
+        P, S, R = len(prefix_cu) - 1, len(suffix_cu) - 1, int(suffix_cu[-1])
+        if logprobs is None:
+            logprobs = torch.empty(max(R, 1), dtype=torch.float32, device=self.device)[:R]
+        nbytes = rb.rp_suffix_grouped_workspace_bytes(self.handle, P, prefix_cu, S, prefix_of_suffix, suffix_cu)
+        ws = workspace if workspace is not None else self.workspace(nbytes)
+        rb.rp_suffix_logprob_grouped(self.handle, stream_ptr(stream), P, prefix_cu, S, prefix_of_suffix,
+                                     suffix_cu, rb.make_kv(K, V, K[0].numel()), h_last, response_ids,
+                                     logprobs, ws, ws.numel())
+        return logprobs
+
     def decode(self, cache_k, cache_v, kv_len, token_ids, logits=None, next_ids=None, workspace=None,
                stream=None):
         B, cap = cache_k.shape[1], cache_k.shape[2]

@@ -137,6 +137,42 @@ def test_bad_suffix_lengths(lib):
         rb.rp_destroy(h)
 
 
+@pytest.mark.parametrize("n_prefix,pcu,n_suffix,grp,scu", [
+    (2, [0, 4, 8], 3, [0, 2, 1], [0, 1, 2, 3]),      # prefix index out of range
+    (2, [0, 4, 8], 2, [0, -1], [0, 1, 2]),           # negative prefix index
+    (2, [0, 4, 8], 0, [], [0]),                      # no suffixes
+    (2, [0, 4, 8], 2, [0, 1], [0, 3, 2]),            # decreasing suffix_cu
+    (1, [0, 1010], 2, [0, 0], [0, 10, 30]),          # prefix + suffix > max_position
+    (2, [0, 4, 4], 1, [0], [0, 2]),                  # empty prefix
+])
+def test_bad_grouped_suffix_arguments(lib, n_prefix, pcu, n_suffix, grp, scu):
+    h, keep = make()
+    try:
+        st, msg = status_of(rb.rp_suffix_grouped_workspace_bytes, h, n_prefix, pcu, n_suffix, grp, scu)
+        assert st == rb.RP_ERR_SHAPE and msg
+    finally:
+        rb.rp_destroy(h)
+
+
+def test_grouped_suffix_workspace_and_validation(lib):
+    h, keep = make()
+    try:
+        # eight responses of one prompt group over one prefix: same workspace as eight suffixes
+        n = rb.rp_suffix_grouped_workspace_bytes(h, 1, [0, 512], 8, [0] * 8, list(range(0, 72, 8)))
+        assert n == rb.rp_suffix_workspace_bytes(h, 8, list(range(0, 8 * 64 + 1, 64)), list(range(0, 72, 8)))
+        m = configs.TINY
+        kv = rb.make_kv(FAKE, FAKE + (1 << 30), 512 * m.n_kv_heads * m.head_dim)
+        args = [h, None, 1, [0, 512], 2, [0, 0], [0, 3, 5], kv, None, FAKE + (1 << 31), FAKE + (1 << 32),
+                FAKE + (1 << 33), 1 << 30]
+        assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_INVALID_ARG   # h_last NULL
+        args[8] = FAKE + (1 << 34)
+        need = rb.rp_suffix_grouped_workspace_bytes(h, 1, [0, 512], 2, [0, 0], [0, 3, 5])
+        args[12] = need - 1
+        assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_WORKSPACE
+    finally:
+        rb.rp_destroy(h)
+
+
 def _prefix_args(h, T=64, ws_bytes=None, stride=None, tokens=FAKE, ws=FAKE + (1 << 30)):
     m = configs.TINY
     kv = rb.make_kv(FAKE + (1 << 32), FAKE + (1 << 33),

@@ -143,3 +143,40 @@ def test_decode_step_matches_oracle(model, cap, lens):
         mask[kv_len[b]] = False
         assert np.array_equal(ckg[:, b, mask], ref_k[:, b, mask])
     dm.close()
+
+
+@pytest.mark.parametrize("model", [BF16_SMALL, configs.TINY, F16_D64])
+def test_shared_prefix_suffix_matches_oracle_and_duplicated_prefix(model):
+    """GRPO groups: several responses scored against one prefix pass (Section "Prefix
+    Sharing").  Matches the oracle, and is bitwise the plain suffix pass run over a copy
+    of each response's prefix KV and boundary state."""
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+    P, Vis = [70, 129, 33], [40, 100, 0]
+    w = configs.custom(model, P, Vis, [1, 1, 1], index=61)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    grp = np.array([1, 0, 1, 1, 0, 1], np.int32)   # prefix 1 serves four responses, prefix 2 none
+    lens = [5, 0, 65, 1, 17, 30]
+    cs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    resp = np.random.default_rng(62).integers(0, model.vocab, int(cs[-1])).astype(np.int32)
+    cp = [int(x) for x in bt.cu_prefix]
+    dm = DeviceModel(hw, max(P) + max(lens) + 1)
+    dev = dm.device
+    K, V, h = dm.prefix(cp, to_device(bt.token_ids, dev), to_device(bt.visual, dev))
+    rd = to_device(resp, dev)
+    lp = dm.suffix_grouped(cp, grp.tolist(), cs.tolist(), K, V, h, rd)
+    # the same responses over an explicit copy of each one's prefix
+    Kd = torch.cat([K[:, cp[g]:cp[g + 1]] for g in grp], dim=1).contiguous()
+    Vd = torch.cat([V[:, cp[g]:cp[g + 1]] for g in grp], dim=1).contiguous()
+    hd = h[torch.as_tensor(grp, device=dev).long()].contiguous()
+    dcu = np.concatenate([[0], np.cumsum([P[g] for g in grp])]).astype(np.int32).tolist()
+    lpd = dm.suffix(dcu, cs.tolist(), Kd, Vd, hd, rd)
+    torch.cuda.synchronize()
+    assert torch.equal(lp, lpd)
+    W = hw.as_f32()
+    Ko, Vo, Ho = oracle.prefix_forward(W, model, bt.cu_prefix, bt.token_ids, inputs.to_f32(bt.visual))
+    lpo = oracle.suffix_logprob_grouped(W, model, bt.cu_prefix, grp, cs, Ko, Vo, Ho, resp)
+    err = max_abs(lp.cpu().numpy(), lpo)
+    print(f"[parity] shared prefix {model.dtype}: max|d logprob| = {err}", flush=True)
+    assert err <= (1e-4 if model.dtype == "f32" else 2e-2)
+    dm.close()

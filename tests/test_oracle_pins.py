@@ -241,6 +241,25 @@ def test_packed_batch_equals_each_alone_and_permutation():
         np.testing.assert_array_equal(H[b], h)
 
 
+def test_shared_prefix_suffixes_equal_unsplit_forward():
+    """Shared prefixes (GRPO groups): every suffix scored against its group's one prefix
+    pass equals the unsplit causal forward of [that prefix ; that response]."""
+    w, W, bt = _setup(P=(9, 14, 5), Vis=(5, 10, 0), S=(3, 4, 2), index=23)
+    K, V, H = oracle.prefix_forward(W, SMALL, bt.cu_prefix, bt.token_ids, inputs.to_f32(bt.visual))
+    grp = np.array([1, 0, 1, 1, 2], np.int32)           # prefix 1 serves three responses
+    lens = [4, 0, 6, 1, 3]
+    cs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    resp = np.random.default_rng(5).integers(0, SMALL.vocab, int(cs[-1])).astype(np.int32)
+    lp = oracle.suffix_logprob_grouped(W, SMALL, bt.cu_prefix, grp, cs, K, V, H, resp)
+    for s_ in range(len(lens)):
+        ids, vis, _ = _seq(bt, int(grp[s_]))
+        ref = oracle.unsplit_logprob_one(W, SMALL, ids, vis, resp[cs[s_]:cs[s_ + 1]])
+        assert np.max(np.abs(lp[cs[s_]:cs[s_ + 1]] - ref), initial=0.0) < 1e-10
+    # suffixes of different prefixes differ (the pairing matters)
+    lp_wrong = oracle.suffix_logprob_grouped(W, SMALL, bt.cu_prefix, np.zeros(5, np.int32), cs, K, V, H, resp)
+    assert np.max(np.abs(lp_wrong[cs[2]:cs[3]] - lp[cs[2]:cs[3]])) > 1e-3
+
+
 def test_prefix_is_response_independent():
     w, W, bt = _setup(P=(12,), Vis=(8,), S=(5,))
     ids, vis, resp = _seq(bt, 0)
