@@ -264,7 +264,9 @@ def main():
     bt = res["bt"]
 
     pf = perf.prefix_flops(m, bt.prefix_lens)
-    sf = perf.suffix_flops(m, bt.prefix_lens, bt.suffix_lens)
+    grp = bt.prefix_of_suffix
+    pre_of_suf = bt.prefix_lens if grp is None else [bt.prefix_lens[g] for g in grp]
+    sf = perf.suffix_flops(m, pre_of_suf, bt.suffix_lens)
     peak = perf.PEAK_FP32_FLOPS if m.dtype == "f32" else perf.PEAK_BF16_FLOPS
     gu_flops = perf.gemm_flops(T, 2 * m.ffn_dim, m.d_model)
     gu = kernels.get("prefix.gemm_gate_up")
@@ -303,7 +305,9 @@ def main():
         "config": {"workload": w.name, "layers": m.n_layers, "d_model": m.d_model,
                    "q_heads": m.n_q_heads, "kv_heads": m.n_kv_heads, "head_dim": m.head_dim,
                    "ffn": m.ffn_dim, "vocab": m.vocab, "batch": B, "prefix_tokens": T,
-                   "suffix_tokens": R, "parallelism": "single GPU"},
+                   "suffix_tokens": R, "parallelism": "single GPU",
+                   **({} if bt.prefix_of_suffix is None else
+                      {"responses_per_prompt": w.group, "responses": len(bt.suffix_lens)})},
         "prefix_tokens_per_s": T / (pre_ms * 1e-3),
         "suffix_tokens_per_s": R / (suf_ms * 1e-3),
         "prefix_ms": pre_ms,
@@ -346,7 +350,9 @@ def run_passes(w, args, profile: bool):
     hw = inputs.make_weights(w)
     bt = inputs.make_batch(w)
     log(f"inputs ready in {time.time() - t0:.1f} s; uploading")
-    maxp = max(p + s for p, s in zip(bt.prefix_lens, bt.suffix_lens)) + 1
+    grp = bt.prefix_of_suffix
+    pre_of_suf = bt.prefix_lens if grp is None else [bt.prefix_lens[g] for g in grp]
+    maxp = max(p + s for p, s in zip(pre_of_suf, bt.suffix_lens)) + 1
     dm = DeviceModel(hw, maxp)
     dev = dm.device
     ids = to_device(bt.token_ids, dev)
@@ -359,7 +365,11 @@ def run_passes(w, args, profile: bool):
     h_last = torch.empty((B, m.d_model), dtype=torch.float32, device=dev)
     lp = torch.empty(max(R, 1), dtype=torch.float32, device=dev)
     ws_p = dm.workspace(rb.rp_prefix_workspace_bytes(dm.handle, B, cu_p))
-    ws_s = dm.workspace(rb.rp_suffix_workspace_bytes(dm.handle, B, cu_p, cu_s))
+    if grp is None:
+        ws_s = dm.workspace(rb.rp_suffix_workspace_bytes(dm.handle, B, cu_p, cu_s))
+    else:
+        grp_l = [int(g) for g in grp]
+        ws_s = dm.workspace(rb.rp_suffix_grouped_workspace_bytes(dm.handle, B, cu_p, len(grp_l), grp_l, cu_s))
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -368,7 +378,11 @@ def run_passes(w, args, profile: bool):
         dm.prefix(cu_p, ids, vis, kv=(K, V), h_last=h_last, workspace=ws_p, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        dm.suffix(cu_p, cu_s, K, V, h_last, resp, logprobs=lp[:R], workspace=ws_s, stream=stream)
+        if grp is None:
+            dm.suffix(cu_p, cu_s, K, V, h_last, resp, logprobs=lp[:R], workspace=ws_s, stream=stream)
+        else:
+            dm.suffix_grouped(cu_p, grp_l, cu_s, K, V, h_last, resp, logprobs=lp[:R], workspace=ws_s,
+                              stream=stream)
         if ev is not None:
             ev[2].record(stream)
 

@@ -51,6 +51,8 @@ class Workload:
     suffix_lens: Optional[List[int]] = None
     ragged: Optional[dict] = None               # draw spec for ragged batches
     decode: Optional[dict] = None               # co-location decode spec
+    group: Optional[int] = None                 # responses per prompt sharing its prefix (GRPO);
+                                                # suffix_lens then lists every response
     note: str = ""
 
 
@@ -77,8 +79,14 @@ WORKLOADS = {
                                          prefix_lens=[8192] * 4, visual_lens=[7680] * 4,
                                          suffix_lens=[0] * 4,
                                          decode=dict(batch=64, kv_len=8192, cap=8192 + 64)),
+    # GRPO groups (Section "Experimental Setup": N = 8 responses per prompt; Section "Prefix
+    # Sharing": a group's prefix runs once): 4 prompts x 8 responses of 256 tokens
+    "qwen7b_grpo_g4_p4096_n8_s256": Workload(5, "qwen7b_grpo_g4_p4096_n8_s256", QWEN7B_SLICE,
+                                             prefix_lens=[4096] * 4, visual_lens=[3840] * 4,
+                                             suffix_lens=[256] * 32, group=8),
 }
 
+# the five benchmark configurations; other workloads are extra measurements
 ORDER = ["tiny_f32", "qwen7b_b4_p4096_s256", "qwen32b_b2_p16384_s512", "qwen7b_ragged_b8",
          "qwen7b_coloc_p4x8192_d64"]
 

@@ -200,6 +200,7 @@ class HostBatch:
     token_ids: np.ndarray          # int32 [T]; -1 marks a visual slot
     visual: np.ndarray             # [N_vis, d] storage dtype, consumed in slot order
     response_ids: np.ndarray       # int32 [R]
+    prefix_of_suffix: Optional[np.ndarray] = None   # int32 [n_suffix] when prefixes are shared
 
     @property
     def batch(self) -> int:
@@ -232,8 +233,12 @@ def make_batch(w: Workload, lengths=None) -> HostBatch:
     B = len(P)
     cu_p = np.zeros(B + 1, np.int32)
     cu_p[1:] = np.cumsum(P)
-    cu_s = np.zeros(B + 1, np.int32)
+    cu_s = np.zeros(len(S) + 1, np.int32)
     cu_s[1:] = np.cumsum(S)
+    grp = None
+    if w.group:  # responses grouped by prompt: suffix s belongs to prefix s // group
+        assert len(S) == B * w.group
+        grp = np.repeat(np.arange(B, dtype=np.int32), w.group)
     T, R, NV = int(cu_p[-1]), int(cu_s[-1]), int(sum(Vis))
     text = np.random.default_rng([w.index, T_TEXT_IDS]).integers(0, m.vocab, T - NV, dtype=np.int32)
     ids = np.empty(T, np.int32)
@@ -246,7 +251,7 @@ def make_batch(w: Workload, lengths=None) -> HostBatch:
         ti += nt
     visual = _draw_normal((NV, m.d_model), [w.index, T_VISUAL], 1.0, m.dtype)
     resp = np.random.default_rng([w.index, T_RESP_IDS]).integers(0, m.vocab, R, dtype=np.int32)
-    return HostBatch(list(P), list(Vis), list(S), cu_p, cu_s, ids, visual, resp)
+    return HostBatch(list(P), list(Vis), list(S), cu_p, cu_s, ids, visual, resp, grp)
 
 
 # ----------------------------------------------------------------------------------------
