@@ -231,6 +231,8 @@ def main():
                     help="run the workload's model in this 16-bit storage type (default: as named)")
     ap.add_argument("--no-f16-variant", action="store_true",
                     help="skip timing the fp16 variant of a bf16 workload")
+    ap.add_argument("--no-fused-variant", action="store_true",
+                    help="skip timing the suffix with the fused lm_head + log-sum-exp scoring")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -329,13 +331,23 @@ def main():
             "value": (rf["T"] + rf["R"]) / (rf["ms_step"] * 1e-3), "unit": "tokens/s",
             "ms_per_step": rf["ms_step"], "prefix_ms": rf["pre_ms"], "suffix_ms": rf["suf_ms"],
             "prefix_mfma_frac": pf["total"] / (rf["pre_ms"] * 1e-3) / perf.PEAK_BF16_FLOPS}
+    if m.dtype != "f32" and not args.no_fused_variant:
+        # the suffix scored by the lm_head with an online log-sum-exp epilogue: the [R, V]
+        # logits are never stored (RP_SUFFIX_FUSED_LOGPROB)
+        from paper_2608_14498_amd import binding as rb
+
+        rfu = run_passes(w, args, profile=False, flags=rb.RP_SUFFIX_FUSED_LOGPROB)
+        out["fused_logprob_variant"] = {
+            "value": (rfu["T"] + rfu["R"]) / (rfu["ms_step"] * 1e-3), "unit": "tokens/s",
+            "ms_per_step": rfu["ms_step"], "suffix_ms": rfu["suf_ms"],
+            "suffix_tokens_per_s": rfu["R"] / (rfu["suf_ms"] * 1e-3)}
     if not args.no_cpu_baseline:
         log("CPU baseline: oracle on sequence 0")
         out["cpu_baseline"] = cpu_baseline(w, res["hw"], bt, args.cpu_prefix_len)
     print(json.dumps(out), flush=True)
 
 
-def run_passes(w, args, profile: bool):
+def run_passes(w, args, profile: bool, flags: int = 0):
     """Time prefix + suffix steps of workload w; optionally per-kernel durations."""
     import numpy as np
     import torch
@@ -365,11 +377,13 @@ def run_passes(w, args, profile: bool):
     h_last = torch.empty((B, m.d_model), dtype=torch.float32, device=dev)
     lp = torch.empty(max(R, 1), dtype=torch.float32, device=dev)
     ws_p = dm.workspace(rb.rp_prefix_workspace_bytes(dm.handle, B, cu_p))
-    if grp is None:
+    grouped = grp is not None or flags != 0
+    if not grouped:
         ws_s = dm.workspace(rb.rp_suffix_workspace_bytes(dm.handle, B, cu_p, cu_s))
     else:
-        grp_l = [int(g) for g in grp]
-        ws_s = dm.workspace(rb.rp_suffix_grouped_workspace_bytes(dm.handle, B, cu_p, len(grp_l), grp_l, cu_s))
+        grp_l = [int(g) for g in grp] if grp is not None else list(range(B))
+        ws_s = dm.workspace(rb.rp_suffix_grouped_workspace_bytes(dm.handle, B, cu_p, len(grp_l), grp_l, cu_s,
+                                                                 flags))
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -378,11 +392,11 @@ def run_passes(w, args, profile: bool):
         dm.prefix(cu_p, ids, vis, kv=(K, V), h_last=h_last, workspace=ws_p, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        if grp is None:
+        if not grouped:
             dm.suffix(cu_p, cu_s, K, V, h_last, resp, logprobs=lp[:R], workspace=ws_s, stream=stream)
         else:
             dm.suffix_grouped(cu_p, grp_l, cu_s, K, V, h_last, resp, logprobs=lp[:R], workspace=ws_s,
-                              stream=stream)
+                              stream=stream, flags=flags)
         if ev is not None:
             ev[2].record(stream)
 

@@ -177,17 +177,28 @@ rp_status rp_suffix_logprob(const rp_model *model, void *stream, int32_t B,
  * n_suffix are in [1, RP_MAX_SEQS]; P_p >= 1, S_s >= 0 and
  * P_p + S_s <= max_position, else RP_ERR_SHAPE; a prefix index out of range
  * is RP_ERR_SHAPE.  Ownership, asynchrony and workspace rules as above.
+ *
+ * flags (bits; others are RP_ERR_INVALID_ARG):
+ *   RP_SUFFIX_FUSED_LOGPROB  score with an lm_head whose epilogue keeps an online
+ *     log-sum-exp per row and the target logit, so the [R, V] logits are never
+ *     stored (the same log-probs up to fp32 summation order; the workspace
+ *     holds R * 8 * 2 * ceil(V / 256) bytes of partials instead of R * V * 4
+ *     bytes of logits).  16-bit models only; an fp32 model ignores the bit.
+ *     The workspace size depends on flags: query it with the same flags.
  * ------------------------------------------------------------------------- */
+#define RP_SUFFIX_FUSED_LOGPROB 1u
+#define RP_SUFFIX_FLAGS 1u /* all defined flag bits */
 rp_status rp_suffix_grouped_workspace_bytes(const rp_model *model, int32_t n_prefix,
                                             const int32_t *prefix_cu_host, int32_t n_suffix,
                                             const int32_t *prefix_of_suffix_host,
-                                            const int32_t *suffix_cu_host, size_t *bytes);
+                                            const int32_t *suffix_cu_host, uint32_t flags,
+                                            size_t *bytes);
 rp_status rp_suffix_logprob_grouped(const rp_model *model, void *stream, int32_t n_prefix,
                                     const int32_t *prefix_cu_host, int32_t n_suffix,
                                     const int32_t *prefix_of_suffix_host,
-                                    const int32_t *suffix_cu_host, rp_kv kv, const float *h_last,
-                                    const int32_t *response_ids, float *logprobs, void *workspace,
-                                    size_t workspace_bytes);
+                                    const int32_t *suffix_cu_host, uint32_t flags, rp_kv kv,
+                                    const float *h_last, const int32_t *response_ids, float *logprobs,
+                                    void *workspace, size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
  * Rollout decode step (the memory-bound phase that the prefix pass overlaps

@@ -20,6 +20,7 @@ RP_OK, RP_ERR_INVALID_ARG, RP_ERR_SHAPE, RP_ERR_UNSUPPORTED, RP_ERR_WORKSPACE, R
 RP_F32, RP_BF16, RP_F16 = 0, 1, 2
 _DTYPES = {"f32": RP_F32, "bf16": RP_BF16, "f16": RP_F16}
 RP_MAX_SEQS = 256
+RP_SUFFIX_FUSED_LOGPROB = 1
 SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_forward",
            "rp_suffix_workspace_bytes", "rp_suffix_logprob", "rp_suffix_grouped_workspace_bytes",
            "rp_suffix_logprob_grouped", "rp_decode_workspace_bytes",
@@ -77,10 +78,11 @@ def lib():
             "rp_suffix_logprob": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), POINTER(c_int32),
                                           RpKV, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t]),
             "rp_suffix_grouped_workspace_bytes": (c_int, [c_void_p, c_int32, POINTER(c_int32), c_int32,
-                                                          POINTER(c_int32), POINTER(c_int32), POINTER(c_size_t)]),
+                                                          POINTER(c_int32), POINTER(c_int32), c_uint32,
+                                                          POINTER(c_size_t)]),
             "rp_suffix_logprob_grouped": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_int32,
-                                                  POINTER(c_int32), POINTER(c_int32), RpKV, c_void_p, c_void_p,
-                                                  c_void_p, c_void_p, c_size_t]),
+                                                  POINTER(c_int32), POINTER(c_int32), c_uint32, RpKV, c_void_p,
+                                                  c_void_p, c_void_p, c_void_p, c_size_t]),
             "rp_decode_workspace_bytes": (c_int, [c_void_p, c_int32, c_int32, POINTER(c_size_t)]),
             "rp_decode_step": (c_int, [c_void_p, c_void_p, c_int32, RpKV, c_int32, c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_size_t]),
@@ -181,18 +183,18 @@ def rp_suffix_logprob(model: int, stream, B: int, prefix_cu, suffix_cu, kv: RpKV
 
 
 def rp_suffix_grouped_workspace_bytes(model: int, n_prefix: int, prefix_cu, n_suffix: int, prefix_of_suffix,
-                                      suffix_cu) -> int:
+                                      suffix_cu, flags: int = 0) -> int:
     n = c_size_t()
     _check(lib().rp_suffix_grouped_workspace_bytes(model, n_prefix, _i32(prefix_cu), n_suffix,
-                                                   _i32(prefix_of_suffix), _i32(suffix_cu), byref(n)))
+                                                   _i32(prefix_of_suffix), _i32(suffix_cu), int(flags), byref(n)))
     return n.value
 
 
 def rp_suffix_logprob_grouped(model: int, stream, n_prefix: int, prefix_cu, n_suffix: int, prefix_of_suffix,
-                              suffix_cu, kv: RpKV, h_last, response_ids, logprobs, workspace,
+                              suffix_cu, flags: int, kv: RpKV, h_last, response_ids, logprobs, workspace,
                               workspace_bytes: int) -> None:
     _check(lib().rp_suffix_logprob_grouped(model, _ptr(stream), n_prefix, _i32(prefix_cu), n_suffix,
-                                           _i32(prefix_of_suffix), _i32(suffix_cu), kv, _ptr(h_last),
+                                           _i32(prefix_of_suffix), _i32(suffix_cu), int(flags), kv, _ptr(h_last),
                                            _ptr(response_ids), _ptr(logprobs), _ptr(workspace),
                                            int(workspace_bytes)))
 

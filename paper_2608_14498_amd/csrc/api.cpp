@@ -274,12 +274,19 @@ struct SuffixWS {
   LayerWS L;
   void* Ks;
   void* Vs;
-  float* logits;
+  float* logits;     // [R, V] fp32 (unfused scoring)
+  float* lse;        // [R, n_part] float2 and
+  float* tgt;        // [R] (fused scoring: RP_SUFFIX_FUSED_LOGPROB)
   float* gemm_part;
   LayerPlan plan;
 };
 
-size_t suffix_ws(const rp_model* m, int64_t R, void* base, SuffixWS* w) {
+// The fused lm_head needs 16-bit MFMA; an fp32 model always scores unfused.
+bool fused_scoring(const rp_model* m, uint32_t flags) {
+  return (flags & RP_SUFFIX_FUSED_LOGPROB) && half_dtype(m->cfg);
+}
+
+size_t suffix_ws(const rp_model* m, int64_t R, uint32_t flags, void* base, SuffixWS* w) {
   Carver c(base);
   SuffixWS tmp;
   SuffixWS* s = w ? w : &tmp;
@@ -288,7 +295,13 @@ size_t suffix_ws(const rp_model* m, int64_t R, void* base, SuffixWS* w) {
   const int64_t kvrow = (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim;
   s->Ks = c.take(R * kvrow * elem_size(m->cfg));
   s->Vs = c.take(R * kvrow * elem_size(m->cfg));
-  s->logits = (float*)c.take(R * (int64_t)m->cfg.vocab * 4);
+  s->logits = s->lse = s->tgt = nullptr;
+  if (fused_scoring(m, flags)) {
+    s->lse = (float*)c.take(R * (int64_t)rp::lse_parts(m->cfg.vocab) * 8);
+    s->tgt = (float*)c.take(R * 4);
+  } else {
+    s->logits = (float*)c.take(R * (int64_t)m->cfg.vocab * 4);
+  }
   s->gemm_part = (float*)c.take(s->plan.part_floats * 4);
   return c.off + 256;
 }
@@ -399,7 +412,7 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
 // NULL) of the n_prefix prefixes: its KV rows pcu[grp[s]].. and boundary state
 // h_last[grp[s]].  Lengths were validated by the caller.
 rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
-                     const int32_t* grp, const int32_t* scu, rp_kv kv, const float* h_last,
+                     const int32_t* grp, const int32_t* scu, uint32_t flags, rp_kv kv, const float* h_last,
                      const int32_t* response_ids, float* logprobs, void* ws, size_t ws_bytes) {
   const int64_t T = pcu[n_prefix], R = scu[n_suffix];
   rp_status st;
@@ -407,7 +420,7 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   if (!h_last) return fail(RP_ERR_INVALID_ARG, "h_last is NULL");
   if (!aligned16(h_last)) return fail(RP_ERR_INVALID_ARG, "h_last must be 16-byte aligned");
   if (R > 0 && (!response_ids || !logprobs)) return fail(RP_ERR_INVALID_ARG, "response_ids and logprobs are required");
-  const size_t need = suffix_ws(m, R, nullptr, nullptr);
+  const size_t need = suffix_ws(m, R, flags, nullptr, nullptr);
   if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
   if (R == 0) return RP_OK;
 
@@ -415,7 +428,7 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   const rp_config& c = m->cfg;
   const rp_dtype dt = c.dtype;
   SuffixWS w;
-  suffix_ws(m, R, ws, &w);
+  suffix_ws(m, R, flags, ws, &w);
   const rp::SeqTable tab = make_table(n_suffix, scu, n_prefix, pcu, grp);
   RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, dt, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
   for (int l = 0; l < c.n_layers; ++l) {
@@ -427,6 +440,13 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   RP_TRY_LAUNCH_N("suffix.final_norm", rp::launch_final_norm_rows(s, dt, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
                                            c.d_model, w.L.N));
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
+  if (fused_scoring(m, flags)) {
+    const rp::LseOut lo = {response_ids, w.lse, w.tgt};
+    RP_TRY_LAUNCH_N("suffix.gemm_lm_head_lse", rp::launch_gemm(s, dt, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm,
+                                                          c.d_model, nullptr, c.vocab, rp::EPI_LSE, 1, nullptr, &lo));
+    RP_TRY_LAUNCH_N("suffix.lse_combine", rp::launch_lse_combine(s, w.lse, w.tgt, (int32_t)R, rp::lse_parts(c.vocab), logprobs));
+    return RP_OK;
+  }
   RP_TRY_LAUNCH_N("suffix.gemm_lm_head", rp::launch_gemm(s, dt, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
                                 c.vocab, rp::EPI_STORE_F32, 1, nullptr));
   RP_TRY_LAUNCH_N("suffix.logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
@@ -538,7 +558,7 @@ rp_status rp_suffix_workspace_bytes(const rp_model* m, int32_t B, const int32_t*
   if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
   rp_status s = check_suffix_cu(m, B, pcu, scu);
   if (s != RP_OK) return s;
-  *bytes = suffix_ws(m, scu[B], nullptr, nullptr);
+  *bytes = suffix_ws(m, scu[B], 0u, nullptr, nullptr);
   return RP_OK;
 }
 
@@ -548,27 +568,30 @@ rp_status rp_suffix_logprob(const rp_model* m, void* stream, int32_t B, const in
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
   rp_status st = check_suffix_cu(m, B, pcu, scu);
   if (st != RP_OK) return st;
-  return suffix_run(m, stream, B, pcu, B, nullptr, scu, kv, h_last, response_ids, logprobs, ws, ws_bytes);
+  return suffix_run(m, stream, B, pcu, B, nullptr, scu, 0u, kv, h_last, response_ids, logprobs, ws, ws_bytes);
 }
 
 rp_status rp_suffix_grouped_workspace_bytes(const rp_model* m, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
-                                            const int32_t* prefix_of_suffix, const int32_t* scu, size_t* bytes) {
+                                            const int32_t* prefix_of_suffix, const int32_t* scu, uint32_t flags,
+                                            size_t* bytes) {
   if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
+  if (flags & ~RP_SUFFIX_FLAGS) return fail(RP_ERR_INVALID_ARG, "unknown suffix flags 0x%x", flags);
   rp_status s = check_grouped_cu(m, n_prefix, pcu, n_suffix, prefix_of_suffix, scu);
   if (s != RP_OK) return s;
-  *bytes = suffix_ws(m, scu[n_suffix], nullptr, nullptr);
+  *bytes = suffix_ws(m, scu[n_suffix], flags, nullptr, nullptr);
   return RP_OK;
 }
 
 rp_status rp_suffix_logprob_grouped(const rp_model* m, void* stream, int32_t n_prefix, const int32_t* pcu,
-                                    int32_t n_suffix, const int32_t* prefix_of_suffix, const int32_t* scu, rp_kv kv,
-                                    const float* h_last, const int32_t* response_ids, float* logprobs, void* ws,
-                                    size_t ws_bytes) {
+                                    int32_t n_suffix, const int32_t* prefix_of_suffix, const int32_t* scu,
+                                    uint32_t flags, rp_kv kv, const float* h_last, const int32_t* response_ids,
+                                    float* logprobs, void* ws, size_t ws_bytes) {
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  if (flags & ~RP_SUFFIX_FLAGS) return fail(RP_ERR_INVALID_ARG, "unknown suffix flags 0x%x", flags);
   rp_status st = check_grouped_cu(m, n_prefix, pcu, n_suffix, prefix_of_suffix, scu);
   if (st != RP_OK) return st;
-  return suffix_run(m, stream, n_prefix, pcu, n_suffix, prefix_of_suffix, scu, kv, h_last, response_ids, logprobs, ws,
-                    ws_bytes);
+  return suffix_run(m, stream, n_prefix, pcu, n_suffix, prefix_of_suffix, scu, flags, kv, h_last, response_ids,
+                    logprobs, ws, ws_bytes);
 }
 
 rp_status rp_decode_workspace_bytes(const rp_model* m, int32_t B, int32_t cap, size_t* bytes) {

@@ -400,6 +400,32 @@ hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const in
   return hipGetLastError();
 }
 
+// Log-probs from the lm_head's online log-sum-exp partials (EPI_LSE): one wave per row
+// merges the row's n_part (max, sum) pairs, lp = tgt - (M + log2 S) ln 2.
+__global__ __launch_bounds__(64) void k_lse_combine(const float2* __restrict__ lse, const float* __restrict__ tgt,
+                                                    int n_part, float* __restrict__ lp) {
+  const int r = blockIdx.x;
+  const float2* p = lse + (int64_t)r * n_part;
+  float m = -INFINITY, s = 0.f;
+  for (int i = threadIdx.x; i < n_part; i += 64) {
+    const float2 v = p[i];
+    lse_merge(m, s, v.x, v.y);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float mo = __shfl_xor(m, o, kWave), so = __shfl_xor(s, o, kWave);
+    lse_merge(m, s, mo, so);
+  }
+  if (threadIdx.x == 0) lp[r] = tgt[r] - (m + log2f(s)) * kLn2;
+}
+
+hipError_t launch_lse_combine(hipStream_t s, const float* lse, const float* tgt, int32_t R, int32_t n_part,
+                              float* lp) {
+  if (R <= 0) return hipSuccess;
+  k_lse_combine<<<R, 64, 0, s>>>(reinterpret_cast<const float2*>(lse), tgt, n_part, lp);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------------------------
 // Greedy argmax per row (lowest index on ties).
 // ------------------------------------------------------------------------------------

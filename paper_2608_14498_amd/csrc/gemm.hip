@@ -39,6 +39,8 @@ struct GemmArgs {
   int tiles_m, tiles_n;
   int k_chunk;       // K range per split (multiple of the k slab)
   float* partials;   // split-K: [splitk][M][N] fp32
+  LseOut lse;        // EPI_LSE outputs
+  int n_part;        // EPI_LSE column blocks per row
 };
 
 template <typename T>
@@ -151,6 +153,46 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16_t (&acc)
       }
   }
 }
+
+// Online log-sum-exp epilogue of the lm_head (EPI_LSE): each wave reduces every row of
+// its 64 x 128 block over the block's in-range columns to (max, sum 2^(x log2e - max))
+// in log2 units, the two lanes of a row (column halves fk = 0, 1) merged by a shuffle;
+// the lane holding column ids[m] writes the target logit.  Column block p = tn*2 + wn.
+template <int MI, int NJ, int TM, int TN>
+__device__ __forceinline__ void gemm_epilogue_lse(const GemmArgs& g, f32x16_t (&acc)[MI][NJ], int tm, int tn, int wm,
+                                                  int wn, int fr, int fk) {
+  static_assert(TN == 128, "two 128-column blocks per 256-column tile");
+  constexpr float kL2e = 1.4426950408889634f;
+  const int c0 = tn * GB_N + wn * TN + 4 * fk;
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    const int m = tm * GB_M + wm * TM + i * 32 + fr;
+    const int mc = min(m, g.M - 1);
+    const int id = min(max(g.lse.ids[mc], 0), g.N - 1);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (c0 + j * 32 + 8 * (e >> 2) + (e & 3) < g.N) mx = fmaxf(mx, acc[i][j][e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float ms = mx * kL2e;
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int col = c0 + j * 32 + 8 * (e >> 2) + (e & 3);
+        if (col < g.N) sum += exp2f(fmaf(acc[i][j][e], kL2e, -ms));
+        if (col == id && m < g.M) g.lse.tgt[m] = acc[i][j][e];
+      }
+    sum += __shfl_xor(sum, 32, kWave);
+    if (fk == 0 && m < g.M)
+      *reinterpret_cast<float2*>(g.lse.lse + ((int64_t)m * g.n_part + tn * 2 + wn) * 2) = make_float2(ms, sum);
+  }
+}
+
+int32_t lse_parts(int32_t N) { return ((N + GB_N - 1) / GB_N) * 2; }
 
 // Epilogue through LDS for the 8-wave kernels (wave tile 64 x 128).  After the main
 // loop the LDS is free: each wave stages its sub-tile in a private 16 KiB region and
@@ -442,7 +484,10 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 #undef G_MMA
 #undef G_INTERLEAVE
 
-  gemm_epilogue<EPI, T16, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
+  if (EPI == EPI_LSE)
+    gemm_epilogue_lse<MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
+  else
+    gemm_epilogue<EPI, T16, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
 }
 
 // ------------------------------------------------------------------------------------
@@ -598,6 +643,11 @@ void k_gemm_bf16_dma(GemmArgs g) {
 #undef D_MMA
 #undef D_TILE
 #undef D_REGION
+  if (EPI == EPI_LSE) {
+    __syncthreads();  // no copy into LDS outlives the workgroup
+    gemm_epilogue_lse<MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, lane & 31, lane >> 5);
+    return;
+  }
   __syncthreads();  // every wave is done with the slab buffers
   uint8_t* stage = WGM == 2 ? (uint8_t*)(wave == 0 ? As0 : wave == 1 ? As1 : wave == 2 ? Bs0 : Bs1)
                             : (uint8_t*)(wave < 2 ? As0 : wave < 4 ? As1 : wave < 6 ? Bs0 : Bs1) + (wave & 1) * 16384;
@@ -738,10 +788,11 @@ static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, b
 
 hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
-                       int32_t splitk, float* partials) {
+                       int32_t splitk, float* partials, const LseOut* lse) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const bool half = dt != RP_F32;
   if (epi == EPI_SWIGLU && (!half || splitk > 1)) return hipErrorInvalidValue;
+  if (epi == EPI_LSE && (!half || splitk > 1 || !lse)) return hipErrorInvalidValue;
   GemmArgs g;
   g.M = M;
   g.N = N;
@@ -753,6 +804,8 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
   g.C = C;
   g.ldc = ldc;
   g.partials = partials;
+  g.lse = lse ? *lse : LseOut{nullptr, nullptr, nullptr};
+  g.n_part = lse_parts(N);
   if (splitk < 1) splitk = 1;
   const int bk = half ? GB_K : GF_K;
   const int kblocks = (K + bk - 1) / bk;
@@ -775,6 +828,8 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
         launch_half<EPI_STORE_F32, H>(s, g, grid, b_rows);
       else if (epi == EPI_SWIGLU)
         launch_half<EPI_SWIGLU, H>(s, g, grid, b_rows);
+      else if (epi == EPI_LSE)
+        launch_half<EPI_LSE, H>(s, g, grid, b_rows);
       else
         launch_half<EPI_ADD_F32, H>(s, g, grid, b_rows);
     });

@@ -42,7 +42,19 @@ enum Epi : int {
   EPI_STORE_F32 = 1,  // C[f32] = acc
   EPI_ADD_F32 = 2,    // C[f32] += acc  (residual stream)
   EPI_SWIGLU = 3,     // C[T][m, f] = silu(gate) * up; B = {gate rows, up rows}, N = ffn features
+  EPI_LSE = 4,        // no C: per-row log-sum-exp partials and the target logit (LseOut)
 };
+
+// Outputs of the EPI_LSE epilogue (an lm_head GEMM whose logits are never stored):
+// lse[m * n_part + p] = (max, sum of 2^(x log2 e - max)) over column block p of row m, in
+// log2 units, n_part = lse_parts(N) blocks of 128 columns; tgt[m] = logit of column ids[m]
+// (ids clamped to [0, N)).
+struct LseOut {
+  const int32_t* ids;
+  float* lse;  // float2 [M][n_part]
+  float* tgt;  // [M]
+};
+int32_t lse_parts(int32_t N);
 
 // B operand of a GEMM given as up to three row segments of nn.Linear weights:
 // logical row n < n1 -> b0 + n*ldb; n < n2 -> b1 + (n-n1)*ldb; else b2 + (n-n2)*ldb.
@@ -82,7 +94,10 @@ hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t 
 // epilogue writes silu(A.gate_f) * (A.up_f).  splitk > 1 needs EPI != EPI_SWIGLU.
 hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
-                       int32_t splitk, float* partials);
+                       int32_t splitk, float* partials, const LseOut* lse = nullptr);
+// lp[r] = tgt[r] - log sum_v exp(logit_rv) from the EPI_LSE partials.
+hipError_t launch_lse_combine(hipStream_t s, const float* lse, const float* tgt, int32_t R, int32_t n_part,
+                              float* lp);
 // Required float count of `partials` for a split-K GEMM.
 size_t gemm_partial_floats(int32_t M, int32_t N, int32_t splitk);
 

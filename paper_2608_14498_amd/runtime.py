@@ -105,15 +105,17 @@ class DeviceModel:
         return logprobs
 
     def suffix_grouped(self, prefix_cu, prefix_of_suffix, suffix_cu, K, V, h_last, response_ids, logprobs=None,
-                       workspace=None, stream=None):
-        """Suffix pass where suffix s reads prefix prefix_of_suffix[s] (shared prefixes)."""
+                       workspace=None, stream=None, flags: int = 0):
+        """Suffix pass where suffix s reads prefix prefix_of_suffix[s] (shared prefixes);
+        flags = rb.RP_SUFFIX_FUSED_LOGPROB scores without storing the logits."""
         P, S, R = len(prefix_cu) - 1, len(suffix_cu) - 1, int(suffix_cu[-1])
         if logprobs is None:
             logprobs = torch.empty(max(R, 1), dtype=torch.float32, device=self.device)[:R]
-        nbytes = rb.rp_suffix_grouped_workspace_bytes(self.handle, P, prefix_cu, S, prefix_of_suffix, suffix_cu)
+        nbytes = rb.rp_suffix_grouped_workspace_bytes(self.handle, P, prefix_cu, S, prefix_of_suffix, suffix_cu,
+                                                      flags)
         ws = workspace if workspace is not None else self.workspace(nbytes)
         rb.rp_suffix_logprob_grouped(self.handle, stream_ptr(stream), P, prefix_cu, S, prefix_of_suffix,
-                                     suffix_cu, rb.make_kv(K, V, K[0].numel()), h_last, response_ids,
+                                     suffix_cu, flags, rb.make_kv(K, V, K[0].numel()), h_last, response_ids,
                                      logprobs, ws, ws.numel())
         return logprobs
 

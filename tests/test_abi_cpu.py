@@ -162,13 +162,30 @@ def test_grouped_suffix_workspace_and_validation(lib):
         assert n == rb.rp_suffix_workspace_bytes(h, 8, list(range(0, 8 * 64 + 1, 64)), list(range(0, 72, 8)))
         m = configs.TINY
         kv = rb.make_kv(FAKE, FAKE + (1 << 30), 512 * m.n_kv_heads * m.head_dim)
-        args = [h, None, 1, [0, 512], 2, [0, 0], [0, 3, 5], kv, None, FAKE + (1 << 31), FAKE + (1 << 32),
+        args = [h, None, 1, [0, 512], 2, [0, 0], [0, 3, 5], 0, kv, None, FAKE + (1 << 31), FAKE + (1 << 32),
                 FAKE + (1 << 33), 1 << 30]
         assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_INVALID_ARG   # h_last NULL
-        args[8] = FAKE + (1 << 34)
+        args[9] = FAKE + (1 << 34)
         need = rb.rp_suffix_grouped_workspace_bytes(h, 1, [0, 512], 2, [0, 0], [0, 3, 5])
-        args[12] = need - 1
+        args[13] = need - 1
         assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_WORKSPACE
+        args[13], args[7] = need, 6                                                        # unknown flag bits
+        assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_INVALID_ARG
+        assert status_of(rb.rp_suffix_grouped_workspace_bytes, h, 1, [0, 512], 2, [0, 0], [0, 3, 5], 2)[0] == \
+            rb.RP_ERR_INVALID_ARG
+    finally:
+        rb.rp_destroy(h)
+
+
+def test_fused_scoring_workspace_holds_partials_not_logits(lib):
+    h, keep = make(configs.QWEN7B_SLICE, max_pos=8192)
+    try:
+        args = (h, 1, [0, 4096], 8, [0] * 8, list(range(0, 8 * 256 + 1, 256)))
+        plain = rb.rp_suffix_grouped_workspace_bytes(*args, 0)
+        fused = rb.rp_suffix_grouped_workspace_bytes(*args, rb.RP_SUFFIX_FUSED_LOGPROB)
+        R, V = 2048, configs.QWEN7B_SLICE.vocab
+        parts = 2 * ((V + 255) // 256)
+        assert plain - fused >= R * V * 4 - R * (parts * 8 + 4) - 4096
     finally:
         rb.rp_destroy(h)
 

@@ -26,6 +26,7 @@ import numpy as np
 import pytest
 import torch
 
+from paper_2608_14498_amd import binding as rb
 from paper_2608_14498_amd import configs, inputs
 from paper_2608_14498_amd.runtime import DeviceModel, to_device
 
@@ -75,10 +76,16 @@ def test_fullsize_matches_oracle(name, dtype):
     hl = h[b].cpu().numpy()
     res = dict(k=_rel(k, g["k"]), v=_rel(v, g["v"]), h_last=_rel(hl, g["h_last"]))
     if cu_s[-1] > 0:
-        lp = dm.suffix(cu_p, cu_s, K, V, h, to_device(bt.response_ids, dev))
+        rid = to_device(bt.response_ids, dev)
+        lp = dm.suffix(cu_p, cu_s, K, V, h, rid)
+        # the same scoring with the fused lm_head + online log-sum-exp (no stored logits)
+        ident = list(range(len(cu_p) - 1))
+        lpf = dm.suffix_grouped(cu_p, ident, cu_s, K, V, h, rid, flags=rb.RP_SUFFIX_FUSED_LOGPROB)
         torch.cuda.synchronize()
         got = lp[cu_s[b]:cu_s[b + 1]].cpu().numpy()
         res["logprob"] = float(np.max(np.abs(got - g["logprobs"])))
+        res["logprob_fused"] = float(np.max(np.abs(lpf[cu_s[b]:cu_s[b + 1]].cpu().numpy() - g["logprobs"])))
+        res["fused_vs_plain"] = float((lpf - lp).abs().max().item())
     del K, V
     if "dec_rows" in g:
         dec = inputs.make_decode(w)
@@ -97,6 +104,8 @@ def test_fullsize_matches_oracle(name, dtype):
     print(f"[fullsize] {name} {dtype}: {json.dumps(res)}", flush=True)
     assert res["k"] <= REL_TOL and res["v"] <= REL_TOL and res["h_last"] <= REL_TOL
     if "logprob" in res:
-        assert res["logprob"] <= tol
+        assert res["logprob"] <= tol and res["logprob_fused"] <= tol
+        # the fused epilogue reduces the same fp32 logits in another order
+        assert res["fused_vs_plain"] <= 1e-4
     if "decode_logits" in res:
         assert res["decode_logits"] <= tol and res["decode_argmax_ok"]

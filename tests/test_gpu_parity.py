@@ -180,3 +180,33 @@ def test_shared_prefix_suffix_matches_oracle_and_duplicated_prefix(model):
     print(f"[parity] shared prefix {model.dtype}: max|d logprob| = {err}", flush=True)
     assert err <= (1e-4 if model.dtype == "f32" else 2e-2)
     dm.close()
+
+
+@pytest.mark.parametrize("model", [BF16_SMALL, BF16_D64, F16_SMALL])
+def test_fused_logprob_scoring_matches_plain_and_oracle(model):
+    """lm_head with the online log-sum-exp epilogue (RP_SUFFIX_FUSED_LOGPROB): the same
+    log-probs as storing the logits and running the log-softmax kernel, up to fp32
+    summation order; vocabularies 1000 and 2051 leave partial 256-column tiles."""
+    from paper_2608_14498_amd import binding as rb
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+    P, Vis, S = [1, 70, 300, 129], [0, 60, 256, 100], [3, 0, 65, 130]
+    w = configs.custom(model, P, Vis, S, index=71)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    dm = DeviceModel(hw, max(p + s for p, s in zip(P, S)) + 1)
+    dev = dm.device
+    cp, cs = [int(x) for x in bt.cu_prefix], [int(x) for x in bt.cu_suffix]
+    K, V, h = dm.prefix(cp, to_device(bt.token_ids, dev), to_device(bt.visual, dev))
+    rid = to_device(bt.response_ids, dev)
+    lp = dm.suffix(cp, cs, K, V, h, rid)
+    lpf = dm.suffix_grouped(cp, list(range(len(P))), cs, K, V, h, rid, flags=rb.RP_SUFFIX_FUSED_LOGPROB)
+    torch.cuda.synchronize()
+    d = float((lpf - lp).abs().max().item())
+    W = hw.as_f32()
+    Ko, Vo, Ho = oracle.prefix_forward(W, model, bt.cu_prefix, bt.token_ids, inputs.to_f32(bt.visual))
+    lpo = oracle.suffix_logprob(W, model, bt.cu_prefix, bt.cu_suffix, Ko, Vo, Ho, bt.response_ids)
+    err = max_abs(lpf.cpu().numpy(), lpo)
+    print(f"[parity] fused scoring {model.dtype} V={model.vocab}: vs plain {d}, vs oracle {err}", flush=True)
+    assert d <= 1e-5
+    assert err <= 2e-2
+    dm.close()
