@@ -66,6 +66,19 @@ def rope_angles(positions, head_dim: int, theta: float):
     return np.asarray(positions, dtype=F64)[:, None] * inv_freq[None, :]
 
 
+def rope_angles_mrope(pos3, head_dim: int, theta: float, sections):
+    """Multimodal RoPE angles: pair index i takes its position from row sec(i) of pos3
+    [3, n] (temporal, height, width), where the Dh/2 pairs are split into consecutive
+    sections of sizes sections[0..2]; angle = pos3[sec(i)] * theta^(-2i/Dh), float64.
+    With the three rows equal this is rope_angles of that row."""
+    pos3 = np.asarray(pos3, dtype=F64)
+    assert pos3.shape[0] == 3 and sum(sections) == head_dim // 2
+    sec = np.repeat(np.arange(3), sections)            # section of every pair index
+    i = np.arange(head_dim // 2, dtype=F64)
+    inv_freq = np.power(F64(theta), -2.0 * i / head_dim)
+    return pos3[sec, :].T * inv_freq[None, :]
+
+
 def apply_rope(x, angles):
     """Rotate-half RoPE on x [n, H, Dh]: pair (i, i + Dh/2) is rotated by angles[:, i]."""
     half = x.shape[-1] // 2
@@ -114,11 +127,13 @@ def log_softmax_gather(logits, ids):
 # ----------------------------------------------------------------------------------------
 # one decoder layer over new tokens, with optional past keys/values
 # ----------------------------------------------------------------------------------------
-def decoder_layer(x, lw: Dict, cfg, positions, past_k=None, past_v=None, past_pos=None):
+def decoder_layer(x, lw: Dict, cfg, positions, past_k=None, past_v=None, past_pos=None, angles=None):
     """Pre-norm decoder block.  Returns (x_out, k_new, v_new) with k_new post-RoPE.
 
-    x [n, d] at absolute positions ``positions``; past_k/v [np, Hkv, Dh] are
-    keys/values (post-RoPE) of earlier positions ``past_pos``.
+    x [n, d] at absolute positions ``positions`` (token order: the causal rule);
+    past_k/v [np, Hkv, Dh] are keys/values (post-RoPE) of earlier positions
+    ``past_pos``.  RoPE rotates by ``angles`` [n, Dh/2] when given (multimodal
+    positions), else by the 1-D angles of ``positions``.
     """
     n = x.shape[0]
     Hq, Hkv, Dh = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
@@ -132,7 +147,7 @@ def decoder_layer(x, lw: Dict, cfg, positions, past_k=None, past_v=None, past_po
         k = k + _f(lw["bk"])
     if lw.get("bv") is not None:
         v = v + _f(lw["bv"])
-    ang = rope_angles(positions, Dh, cfg.rope_theta)
+    ang = rope_angles(positions, Dh, cfg.rope_theta) if angles is None else angles
     q = apply_rope(q.reshape(n, Hq, Dh), ang)
     k = apply_rope(k.reshape(n, Hkv, Dh), ang)
     v = v.reshape(n, Hkv, Dh)
@@ -165,19 +180,21 @@ def embed_prefix(embed, token_ids, visual):
 # ----------------------------------------------------------------------------------------
 # single sequence: prefix pass, suffix pass, unsplit forward
 # ----------------------------------------------------------------------------------------
-def prefix_forward_one(weights, cfg, token_ids, visual):
+def prefix_forward_one(weights, cfg, token_ids, visual, mrope=None):
     """Prefix pass of one sequence (Section "Observation and Opportunity"; Phase 1).
 
     Returns (K, V, h_last, hidden): K, V [L, P, Hkv, Dh] post-RoPE keys and
     values of every prefix position, h_last [d] the residual stream at the last
     prefix position after the last layer (before the final norm), hidden [P, d].
+    mrope = (pos3 [3, P], sections) rotates by multimodal positions instead of 0..P-1.
     """
     x, _ = embed_prefix(weights.embed, token_ids, visual)
     P = x.shape[0]
     pos = np.arange(P)
+    ang = None if mrope is None else rope_angles_mrope(mrope[0], cfg.head_dim, cfg.rope_theta, mrope[1])
     Ks, Vs = [], []
     for lw in weights.layers:
-        x, k, v = decoder_layer(x, lw, cfg, pos)
+        x, k, v = decoder_layer(x, lw, cfg, pos, angles=ang)
         Ks.append(k)
         Vs.append(v)
     return np.stack(Ks), np.stack(Vs), x[P - 1].copy(), x
@@ -193,12 +210,15 @@ def score_rows(weights, cfg, z, ids):
     return out
 
 
-def suffix_logprob_one(weights, cfg, K, V, h_last, response_ids):
+def suffix_logprob_one(weights, cfg, K, V, h_last, response_ids, rope_start=None):
     """Suffix pass of one sequence (Phase 2): log p(r_j | prefix, r_<j) for every j.
 
     Response token j runs at position P + j and sees every prefix key (K, V from
     the prefix pass) and the response keys 0..j.  Token r_j is scored from the
     hidden state one position earlier: h_last for j = 0, else response row j-1.
+    RoPE rotates token j by position rope_start + j (default P; after a prefix with
+    multimodal positions, the prefix's next rotary position: text tokens have equal
+    temporal, height and width positions, i.e. plain 1-D RoPE).
     """
     S = len(response_ids)
     if S == 0:
@@ -207,20 +227,29 @@ def suffix_logprob_one(weights, cfg, K, V, h_last, response_ids):
     y = _f(weights.embed[np.asarray(response_ids)])
     pos = P + np.arange(S)
     ppos = np.arange(P)
+    r0 = P if rope_start is None else int(rope_start)
+    ang = rope_angles(r0 + np.arange(S), cfg.head_dim, cfg.rope_theta)
     for l, lw in enumerate(weights.layers):
-        y, _, _ = decoder_layer(y, lw, cfg, pos, K[l], V[l], ppos)
+        y, _, _ = decoder_layer(y, lw, cfg, pos, K[l], V[l], ppos, angles=ang)
     z = np.concatenate([_f(h_last)[None, :], y[:S - 1]], axis=0)
     return score_rows(weights, cfg, z, np.asarray(response_ids))
 
 
-def unsplit_logprob_one(weights, cfg, token_ids, visual, response_ids):
-    """Causal forward over [prefix ; response] in one pass; lp_j from position P-1+j."""
+def unsplit_logprob_one(weights, cfg, token_ids, visual, response_ids, mrope=None, rope_start=None):
+    """Causal forward over [prefix ; response] in one pass; lp_j from position P-1+j.
+    With mrope = (pos3 [3, P], sections) the prefix rotates by multimodal positions and
+    response token j by (rope_start + j) in all three rows."""
     xp, _ = embed_prefix(weights.embed, token_ids, visual)
     P, S = xp.shape[0], len(response_ids)
     x = np.concatenate([xp, _f(weights.embed[np.asarray(response_ids)])], axis=0)
     pos = np.arange(P + S)
+    ang = None
+    if mrope is not None:
+        r0 = P if rope_start is None else int(rope_start)
+        rows = np.concatenate([np.asarray(mrope[0]), np.tile(r0 + np.arange(S), (3, 1))], axis=1)
+        ang = rope_angles_mrope(rows, cfg.head_dim, cfg.rope_theta, mrope[1])
     for lw in weights.layers:
-        x, _, _ = decoder_layer(x, lw, cfg, pos)
+        x, _, _ = decoder_layer(x, lw, cfg, pos, angles=ang)
     return score_rows(weights, cfg, x[P - 1:P - 1 + S], np.asarray(response_ids))
 
 

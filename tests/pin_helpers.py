@@ -150,3 +150,19 @@ def brute_force(weights, cfg, token_ids, visual, response_ids):
         lse = mx + math.log(sum(math.exp(v - mx) for v in logits))
         lps.append(logits[int(r)] - lse)
     return np.array(lps)
+
+
+def hf_mrope(q, k, pos3, sections, theta):
+    """q [n, Hq, Dh], k [n, Hkv, Dh] rotated by transformers' Qwen2.5-VL multimodal RoPE
+    (its section selection and rotate-half), fed float64 cos/sin of the three position rows."""
+    import torch
+    from transformers.models.qwen2_5_vl.modeling_qwen2_5_vl import apply_multimodal_rotary_pos_emb
+    Dh = q.shape[-1]
+    inv = torch.tensor(theta, dtype=torch.float64) ** (-torch.arange(0, Dh, 2, dtype=torch.float64) / Dh)
+    pos = torch.tensor(np.asarray(pos3), dtype=torch.float64)          # [3, n]
+    freqs = pos[:, None, :, None] * inv[None, None, None, :]            # [3, 1, n, Dh/2]
+    emb = torch.cat([freqs, freqs], dim=-1)
+    qt = torch.tensor(q).transpose(0, 1)[None]                          # [1, H, n, Dh]
+    kt = torch.tensor(k).transpose(0, 1)[None]
+    qo, ko = apply_multimodal_rotary_pos_emb(qt, kt, emb.cos(), emb.sin(), list(sections))
+    return qo[0].transpose(0, 1).numpy(), ko[0].transpose(0, 1).numpy()

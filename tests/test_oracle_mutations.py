@@ -13,7 +13,8 @@ import torch
 import oracle
 import oracle.backbone as ob
 from tests.pin_helpers import hf_qwen2
-from tests.test_oracle_pins import HF_TOL, SMALL, _seq, _setup
+from tests.pin_helpers import hf_mrope
+from tests.test_oracle_pins import HF_TOL, MROPE_SMALL, SMALL, _seq, _setup, video_positions
 
 
 def _pins_hold() -> bool:
@@ -37,6 +38,18 @@ def _pins_hold() -> bool:
         torch.tensor(v).transpose(0, 1)[None], is_causal=True, enable_gqa=True)[0].transpose(0, 1)
     got = ob.attention(q, k, v, np.arange(5), np.arange(5))
     ok &= bool(np.allclose(got, ref.numpy(), atol=1e-10))
+    # multimodal RoPE vs transformers, and the split invariant with 3-D prefix positions
+    pos3 = rng.integers(0, 300, (3, 7))
+    qq, kk = rng.standard_normal((7, 4, 16)), rng.standard_normal((7, 2, 16))
+    qh, _ = hf_mrope(qq, kk, pos3, MROPE_SMALL, 1e6)
+    ok &= bool(np.max(np.abs(ob.apply_rope(qq, ob.rope_angles_mrope(pos3, 16, 1e6, MROPE_SMALL)) - qh)) < 1e-12)
+    w2, W2, bt2 = _setup(P=(21,), Vis=(12,), S=(7,), index=9)
+    ids2, vis2, resp2 = _seq(bt2, 0)
+    p3, nxt = video_positions(12, 9, (2, 2, 3))
+    K2, V2, h2, _ = ob.prefix_forward_one(W2, SMALL, ids2, vis2, mrope=(p3, MROPE_SMALL))
+    lps = ob.suffix_logprob_one(W2, SMALL, K2, V2, h2, resp2, rope_start=nxt)
+    lpu2 = ob.unsplit_logprob_one(W2, SMALL, ids2, vis2, resp2, mrope=(p3, MROPE_SMALL), rope_start=nxt)
+    ok &= bool(np.max(np.abs(lps - lpu2)) < 1e-10)
     return bool(ok)
 
 
@@ -94,19 +107,19 @@ def _silu_sigmoid(z):
     return 1.0 / (1.0 + np.exp(-z))
 
 
-def _layer_no_attn_residual(x, lw, cfg, positions, past_k=None, past_v=None, past_pos=None):
-    y, k, v = ORIG["decoder_layer"](x, lw, cfg, positions, past_k, past_v, past_pos)
+def _layer_no_attn_residual(x, lw, cfg, positions, past_k=None, past_v=None, past_pos=None, angles=None):
+    y, k, v = ORIG["decoder_layer"](x, lw, cfg, positions, past_k, past_v, past_pos, angles=angles)
     lw2 = dict(lw, w_down=np.zeros_like(lw["w_down"]))
-    y_attn, _, _ = ORIG["decoder_layer"](x, lw2, cfg, positions, past_k, past_v, past_pos)
+    y_attn, _, _ = ORIG["decoder_layer"](x, lw2, cfg, positions, past_k, past_v, past_pos, angles=angles)
     return y - x, k, v  # residual input dropped
 
 
-def _layer_wo_transposed(x, lw, cfg, positions, past_k=None, past_v=None, past_pos=None):
+def _layer_wo_transposed(x, lw, cfg, positions, past_k=None, past_v=None, past_pos=None, angles=None):
     return ORIG["decoder_layer"](x, dict(lw, wo=np.ascontiguousarray(lw["wo"].T)), cfg, positions,
-                                 past_k, past_v, past_pos)
+                                 past_k, past_v, past_pos, angles=angles)
 
 
-def _suffix_shift(weights, cfg, K, V, h_last, response_ids):
+def _suffix_shift(weights, cfg, K, V, h_last, response_ids, rope_start=None):
     S = len(response_ids)
     P = K.shape[1]
     y = np.asarray(weights.embed[np.asarray(response_ids)], np.float64)
@@ -116,7 +129,7 @@ def _suffix_shift(weights, cfg, K, V, h_last, response_ids):
     return ob.score_rows(weights, cfg, z, np.asarray(response_ids))
 
 
-def _suffix_no_boundary(weights, cfg, K, V, h_last, response_ids):
+def _suffix_no_boundary(weights, cfg, K, V, h_last, response_ids, rope_start=None):
     S = len(response_ids)
     P = K.shape[1]
     y = np.asarray(weights.embed[np.asarray(response_ids)], np.float64)
@@ -125,8 +138,16 @@ def _suffix_no_boundary(weights, cfg, K, V, h_last, response_ids):
     return ob.score_rows(weights, cfg, y, np.asarray(response_ids))
 
 
+def _mrope_sections_reversed(pos3, head_dim, theta, sections):
+    return ORIG["rope_angles_mrope"](np.asarray(pos3)[::-1], head_dim, theta, tuple(sections)[::-1])
+
+
+def _suffix_restarts_at_prefix_length(weights, cfg, K, V, h_last, response_ids, rope_start=None):
+    return ORIG["suffix_logprob_one"](weights, cfg, K, V, h_last, response_ids)
+
+
 ORIG = {n: getattr(ob, n) for n in ("attention", "rmsnorm", "decoder_layer", "apply_rope",
-                                    "rope_angles", "silu", "suffix_logprob_one")}
+                                    "rope_angles", "rope_angles_mrope", "silu", "suffix_logprob_one")}
 
 MUTATIONS = {
     "rope_interleaved_pairs": ("apply_rope", _rope_interleaved),
@@ -141,6 +162,8 @@ MUTATIONS = {
     "wo_transposed": ("decoder_layer", _layer_wo_transposed),
     "suffix_positions_off_by_one": ("suffix_logprob_one", _suffix_shift),
     "suffix_scores_from_own_row": ("suffix_logprob_one", _suffix_no_boundary),
+    "mrope_sections_reversed": ("rope_angles_mrope", _mrope_sections_reversed),
+    "mrope_suffix_restarts_at_prefix_length": ("suffix_logprob_one", _suffix_restarts_at_prefix_length),
 }
 
 

@@ -13,7 +13,7 @@ import torch
 
 import oracle
 from paper_2608_14498_amd import configs, inputs
-from tests.pin_helpers import brute_force, hf_qwen2
+from tests.pin_helpers import brute_force, hf_mrope, hf_qwen2
 
 SMALL = configs.ModelShape(n_layers=2, d_model=64, n_q_heads=4, n_kv_heads=2, head_dim=16,
                            ffn_dim=96, vocab=97, dtype="f32")
@@ -221,6 +221,60 @@ def test_gqa_equals_replicated_mha():
     a = oracle.unsplit_logprob_one(W, SMALL, ids, vis, resp)
     b = oracle.unsplit_logprob_one(W2, mha, ids, vis, resp)
     assert np.max(np.abs(a - b)) < 1e-12
+
+
+# ----------------------------------------------------------------------------------------
+# multimodal RoPE (Qwen2.5-VL's 3-D positions for visual tokens; sections from the public
+# model configuration, the paper being silent)
+# ----------------------------------------------------------------------------------------
+MROPE_SMALL = (2, 3, 3)  # sections of the Dh/2 = 8 pairs of SMALL
+
+
+def video_positions(n_vis, n_text, grid, start=0):
+    """3-D rotary positions of [visual block | text]: visual token (t, y, x) of a
+    T x H x W grid at (start + 2t, start + y, start + x); text continues at one past the
+    largest visual position with equal rows.  Returns (pos3 [3, n], next position)."""
+    T, H, W = grid
+    assert T * H * W == n_vis
+    t, y, x = np.meshgrid(np.arange(T), np.arange(H), np.arange(W), indexing="ij")
+    vis = np.stack([start + 2 * t.ravel(), start + y.ravel(), start + x.ravel()])
+    nxt = int(vis.max()) + 1 if n_vis else start
+    txt = np.tile(nxt + np.arange(n_text), (3, 1))
+    return np.concatenate([vis, txt], axis=1).astype(np.int64), nxt + n_text
+
+
+def test_mrope_with_equal_rows_is_rope():
+    pos = np.array([0, 3, 17, 250])
+    a = oracle.rope_angles_mrope(np.tile(pos, (3, 1)), 16, 1e6, MROPE_SMALL)
+    np.testing.assert_array_equal(a, oracle.rope_angles(pos, 16, 1e6))
+
+
+def test_mrope_matches_transformers_multimodal_rotary():
+    rng = np.random.default_rng(11)
+    for Dh, sec in ((16, MROPE_SMALL), (128, (16, 24, 24))):
+        n = 13
+        pos3 = rng.integers(0, 300, (3, n))
+        q, k = rng.standard_normal((n, 4, Dh)), rng.standard_normal((n, 2, Dh))
+        ang = oracle.rope_angles_mrope(pos3, Dh, 1e6, sec)
+        qh, kh = hf_mrope(q, k, pos3, sec, 1e6)
+        assert np.max(np.abs(oracle.apply_rope(q, ang) - qh)) < 1e-12
+        assert np.max(np.abs(oracle.apply_rope(k, ang) - kh)) < 1e-12
+
+
+def test_mrope_split_invariant():
+    """Prefix over 3-D positions, then the response continuing at the prefix's next
+    rotary position, equals the unsplit forward with the same positions."""
+    w, W, bt = _setup(P=(21,), Vis=(12,), S=(7,), index=9)
+    ids, vis, resp = _seq(bt, 0)
+    pos3, nxt = video_positions(12, 9, (2, 2, 3))
+    mr = (pos3, MROPE_SMALL)
+    K, V, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis, mrope=mr)
+    lp = oracle.suffix_logprob_one(W, SMALL, K, V, h, resp, rope_start=nxt)
+    lpu = oracle.unsplit_logprob_one(W, SMALL, ids, vis, resp, mrope=mr, rope_start=nxt)
+    assert np.max(np.abs(lp - lpu)) < 1e-10
+    # the multimodal positions matter
+    K1, V1, h1, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+    assert np.max(np.abs(K1 - K)) > 1e-3
 
 
 # ----------------------------------------------------------------------------------------
