@@ -143,6 +143,26 @@ rp_status rp_prefix_forward(const rp_model *model, void *stream, int32_t B,
                             size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
+ * Prefix pass with multimodal RoPE (Qwen2.5-VL-style 3-D positions; the paper's
+ * models are Qwen2.5-VL, Section "Experimental Setup", and it does not describe
+ * the rotary scheme).  Identical to rp_prefix_forward except for the rotation:
+ * positions is a device int32 [3][T] array (row 0 temporal, 1 height, 2 width
+ * position of every prefix row; text tokens carry three equal values), 16-byte
+ * aligned, values clamped to [0, max_position).  mrope_section (host int32 [3],
+ * non-negative, summing to head_dim / 2, else RP_ERR_SHAPE) splits the rotary
+ * pairs i < head_dim/2 into consecutive temporal, height and width sections:
+ * pair i rotates by the position of its section.  Qwen2.5-VL uses {16, 24, 24}.
+ * The causal rule follows token order; score the responses with
+ * rp_suffix_logprob_grouped and rope_pos0 = each prefix's next rotary position.
+ * Workspace: rp_prefix_workspace_bytes.
+ * ------------------------------------------------------------------------- */
+rp_status rp_prefix_forward_mrope(const rp_model *model, void *stream, int32_t B,
+                                  const int32_t *cu_seqlens_host, const int32_t *token_ids,
+                                  const void *visual_embeds, int64_t n_visual, const int32_t *positions,
+                                  const int32_t *mrope_section, rp_kv kv_out, float *h_last,
+                                  float *hidden_out, void *workspace, size_t workspace_bytes);
+
+/* ---------------------------------------------------------------------------
  * Suffix pass (Phase 2 of Section "Cross-Phase Execution": the suffix
  * continues from the retained boundary and scores the response without
  * recomputing the prompt; prefix and suffix log-probabilities together form
@@ -178,6 +198,13 @@ rp_status rp_suffix_logprob(const rp_model *model, void *stream, int32_t B,
  * P_p + S_s <= max_position, else RP_ERR_SHAPE; a prefix index out of range
  * is RP_ERR_SHAPE.  Ownership, asynchrony and workspace rules as above.
  *
+ * rope_pos0_host (host int32 [n_prefix], nullable): rotary position of the first
+ * response token after prefix p; response token j then rotates by
+ * rope_pos0[p] + j with equal temporal, height and width positions (plain 1-D
+ * RoPE; after a prefix run with multimodal positions this is the prefix's next
+ * rotary position).  NULL means P_p.  The causal rule still follows token order.
+ * rope_pos0[p] + S_s must not exceed max_position (RP_ERR_SHAPE).
+ *
  * flags (bits; others are RP_ERR_INVALID_ARG):
  *   RP_SUFFIX_FUSED_LOGPROB  score with an lm_head whose epilogue keeps an online
  *     log-sum-exp per row and the target logit, so the [R, V] logits are never
@@ -196,9 +223,10 @@ rp_status rp_suffix_grouped_workspace_bytes(const rp_model *model, int32_t n_pre
 rp_status rp_suffix_logprob_grouped(const rp_model *model, void *stream, int32_t n_prefix,
                                     const int32_t *prefix_cu_host, int32_t n_suffix,
                                     const int32_t *prefix_of_suffix_host,
-                                    const int32_t *suffix_cu_host, uint32_t flags, rp_kv kv,
-                                    const float *h_last, const int32_t *response_ids, float *logprobs,
-                                    void *workspace, size_t workspace_bytes);
+                                    const int32_t *suffix_cu_host, const int32_t *rope_pos0_host,
+                                    uint32_t flags, rp_kv kv, const float *h_last,
+                                    const int32_t *response_ids, float *logprobs, void *workspace,
+                                    size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
  * Rollout decode step (the memory-bound phase that the prefix pass overlaps

@@ -21,7 +21,7 @@ RP_F32, RP_BF16, RP_F16 = 0, 1, 2
 _DTYPES = {"f32": RP_F32, "bf16": RP_BF16, "f16": RP_F16}
 RP_MAX_SEQS = 256
 RP_SUFFIX_FUSED_LOGPROB = 1
-SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_forward",
+SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_forward", "rp_prefix_forward_mrope",
            "rp_suffix_workspace_bytes", "rp_suffix_logprob", "rp_suffix_grouped_workspace_bytes",
            "rp_suffix_logprob_grouped", "rp_decode_workspace_bytes",
            "rp_decode_step", "rp_stream_create_cu_masked", "rp_stream_destroy",
@@ -81,8 +81,11 @@ def lib():
                                                           POINTER(c_int32), POINTER(c_int32), c_uint32,
                                                           POINTER(c_size_t)]),
             "rp_suffix_logprob_grouped": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_int32,
-                                                  POINTER(c_int32), POINTER(c_int32), c_uint32, RpKV, c_void_p,
-                                                  c_void_p, c_void_p, c_void_p, c_size_t]),
+                                                  POINTER(c_int32), POINTER(c_int32), POINTER(c_int32), c_uint32,
+                                                  RpKV, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t]),
+            "rp_prefix_forward_mrope": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
+                                                c_int64, c_void_p, POINTER(c_int32), RpKV, c_void_p, c_void_p,
+                                                c_void_p, c_size_t]),
             "rp_decode_workspace_bytes": (c_int, [c_void_p, c_int32, c_int32, POINTER(c_size_t)]),
             "rp_decode_step": (c_int, [c_void_p, c_void_p, c_int32, RpKV, c_int32, c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_size_t]),
@@ -191,12 +194,21 @@ def rp_suffix_grouped_workspace_bytes(model: int, n_prefix: int, prefix_cu, n_su
 
 
 def rp_suffix_logprob_grouped(model: int, stream, n_prefix: int, prefix_cu, n_suffix: int, prefix_of_suffix,
-                              suffix_cu, flags: int, kv: RpKV, h_last, response_ids, logprobs, workspace,
+                              suffix_cu, rope_pos0, flags: int, kv: RpKV, h_last, response_ids, logprobs, workspace,
                               workspace_bytes: int) -> None:
     _check(lib().rp_suffix_logprob_grouped(model, _ptr(stream), n_prefix, _i32(prefix_cu), n_suffix,
-                                           _i32(prefix_of_suffix), _i32(suffix_cu), int(flags), kv, _ptr(h_last),
-                                           _ptr(response_ids), _ptr(logprobs), _ptr(workspace),
+                                           _i32(prefix_of_suffix), _i32(suffix_cu), _i32(rope_pos0), int(flags),
+                                           kv, _ptr(h_last), _ptr(response_ids), _ptr(logprobs), _ptr(workspace),
                                            int(workspace_bytes)))
+
+
+def rp_prefix_forward_mrope(model: int, stream, B: int, cu_seqlens, token_ids, visual_embeds, n_visual: int,
+                            positions, mrope_section, kv_out: RpKV, h_last, hidden_out, workspace,
+                            workspace_bytes: int) -> None:
+    _check(lib().rp_prefix_forward_mrope(model, _ptr(stream), B, _i32(cu_seqlens), _ptr(token_ids),
+                                         _ptr(visual_embeds), int(n_visual), _ptr(positions), _i32(mrope_section),
+                                         kv_out, _ptr(h_last), _ptr(hidden_out), _ptr(workspace),
+                                         int(workspace_bytes)))
 
 
 def rp_decode_workspace_bytes(model: int, B: int, cap: int) -> int:

@@ -181,7 +181,7 @@ rp_status check_suffix_cu(const rp_model* m, int32_t B, const int32_t* pcu, cons
 // Shared-prefix suffixes: n_suffix sequences, sequence s scores against prefix
 // prefix_of_suffix[s] of the n_prefix prefixes.
 rp_status check_grouped_cu(const rp_model* m, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
-                           const int32_t* grp, const int32_t* scu) {
+                           const int32_t* grp, const int32_t* scu, const int32_t* rope0 = nullptr) {
   rp_status st = check_prefix_cu(m, n_prefix, pcu, "prefix_cu");
   if (st != RP_OK) return st;
   if (n_suffix < 1 || n_suffix > RP_MAX_SEQS)
@@ -197,17 +197,28 @@ rp_status check_grouped_cu(const rp_model* m, int32_t n_prefix, const int32_t* p
     if (last > m->cfg.max_position)
       return fail(RP_ERR_SHAPE, "suffix %d: prefix + suffix = %lld exceeds max_position %d", s, (long long)last,
                   m->cfg.max_position);
+    if (rope0) {
+      const int64_t r = (int64_t)rope0[grp[s]];
+      if (r < 0 || r + S > m->cfg.max_position)
+        return fail(RP_ERR_SHAPE, "suffix %d: rotary positions %lld .. %lld outside [0, max_position %d)", s,
+                    (long long)r, (long long)(r + S - 1), m->cfg.max_position);
+    }
   }
   return RP_OK;
 }
 
-rp::SeqTable make_table(int32_t B, const int32_t* q_cu, int32_t n_k, const int32_t* k_cu, const int32_t* grp) {
+// Sequence table: query rows q_cu[0..B]; the key segment of sequence b is prefix grp[b]
+// (b when grp is NULL) of the n_k prefixes k_cu[0..n_k] (none when k_cu is NULL).  The
+// first query row after prefix p rotates by position rope0[p] (default: its length).
+rp::SeqTable make_table(int32_t B, const int32_t* q_cu, int32_t n_k, const int32_t* k_cu, const int32_t* grp,
+                        const int32_t* rope0 = nullptr) {
   rp::SeqTable t;
   memset(&t, 0, sizeof t);
   t.n = B;
   for (int b = 0; b <= B; ++b) t.q_cu[b] = q_cu[b];
   for (int p = 0; p <= n_k && k_cu; ++p) t.k_cu[p] = k_cu[p];
-  for (int b = 0; b < B; ++b) t.grp[b] = grp ? grp[b] : b;
+  for (int p = 0; p < n_k && k_cu; ++p) t.rope0[p] = rope0 ? rope0[p] : k_cu[p + 1] - k_cu[p];
+  for (int b = 0; b < B; ++b) t.grp[b] = (uint8_t)(grp ? grp[b] : b);
   return t;
 }
 
@@ -369,7 +380,8 @@ const LayerNames kSuffixNames = {"suffix.rmsnorm", "suffix.gemm_qkv", "suffix.ro
 
 rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, const rp::SeqTable& st,
                     int32_t M, const LayerWS& w, void* k_out, void* v_out, const void* k0, const void* v0,
-                    const LayerPlan& plan, float* gemm_part, const LayerNames& nm) {
+                    const LayerPlan& plan, float* gemm_part, const LayerNames& nm,
+                    const rp::MRope& mr = rp::MRope{nullptr, 0, 0}) {
   const rp_config& c = m->cfg;
   const rp_dtype dt = c.dtype;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
@@ -378,7 +390,7 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
   RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE_F32, plan.qkv, gemm_part));
   RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv(s, dt, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position, w.Q,
-                                   k_out, v_out));
+                                   k_out, v_out, mr));
   rp::AttnArgs a;
   a.q = w.Q;
   a.q_ld = hq;
@@ -408,12 +420,53 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   return RP_OK;
 }
 
+// Prefix pass over B sequences (1-D positions, or multimodal ones when mr.pos is set).
+rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* cu, const int32_t* token_ids,
+                     const void* visual, int64_t n_visual, const rp::MRope& mr, rp_kv kv_out, float* h_last,
+                     float* hidden_out, void* ws, size_t ws_bytes) {
+  if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  rp_status st = check_prefix_cu(m, B, cu, "cu_seqlens");
+  if (st != RP_OK) return st;
+  const int64_t T = cu[B];
+  if (!token_ids || !h_last) return fail(RP_ERR_INVALID_ARG, "token_ids and h_last are required");
+  if (n_visual < 0) return fail(RP_ERR_SHAPE, "n_visual %lld < 0", (long long)n_visual);
+  if (n_visual > 0 && !visual) return fail(RP_ERR_INVALID_ARG, "visual_embeds is NULL with n_visual > 0");
+  if (visual && !aligned16(visual)) return fail(RP_ERR_INVALID_ARG, "visual_embeds must be 16-byte aligned");
+  if ((hidden_out && !aligned16(hidden_out)) || !aligned16(h_last))
+    return fail(RP_ERR_INVALID_ARG, "h_last / hidden_out must be 16-byte aligned");
+  if ((st = check_kv(m, kv_out, T, "kv_out")) != RP_OK) return st;
+  const size_t need = prefix_ws(m, T, nullptr, hidden_out == nullptr, nullptr, nullptr);
+  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
+
+  hipStream_t s = (hipStream_t)stream;
+  const rp_config& c = m->cfg;
+  const rp_dtype dt = c.dtype;
+  LayerWS w;
+  int32_t* vis_idx = nullptr;
+  prefix_ws(m, T, ws, hidden_out == nullptr, &w, &vis_idx);
+  if (hidden_out) w.X = hidden_out;
+  const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
+  const LayerPlan plan = plan_layer(c, (int32_t)T, Pass::kPrefix);
+
+  RP_TRY_LAUNCH_N("prefix.visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
+  RP_TRY_LAUNCH_N("prefix.embed", rp::launch_embed(s, dt, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
+                                 c.d_model, w.X));
+  for (int l = 0; l < c.n_layers; ++l) {
+    void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
+    void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames, mr);
+    if (st != RP_OK) return st;
+  }
+  RP_TRY_LAUNCH_N("prefix.gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
+  return RP_OK;
+}
+
 // Suffix pass over n_suffix sequences; sequence s reads prefix grp[s] (s when grp is
 // NULL) of the n_prefix prefixes: its KV rows pcu[grp[s]].. and boundary state
 // h_last[grp[s]].  Lengths were validated by the caller.
 rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
-                     const int32_t* grp, const int32_t* scu, uint32_t flags, rp_kv kv, const float* h_last,
-                     const int32_t* response_ids, float* logprobs, void* ws, size_t ws_bytes) {
+                     const int32_t* grp, const int32_t* scu, const int32_t* rope0, uint32_t flags, rp_kv kv,
+                     const float* h_last, const int32_t* response_ids, float* logprobs, void* ws, size_t ws_bytes) {
   const int64_t T = pcu[n_prefix], R = scu[n_suffix];
   rp_status st;
   if ((st = check_kv(m, kv, T, "kv")) != RP_OK) return st;
@@ -429,7 +482,7 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   const rp_dtype dt = c.dtype;
   SuffixWS w;
   suffix_ws(m, R, flags, ws, &w);
-  const rp::SeqTable tab = make_table(n_suffix, scu, n_prefix, pcu, grp);
+  const rp::SeqTable tab = make_table(n_suffix, scu, n_prefix, pcu, grp, rope0);
   RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, dt, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
   for (int l = 0; l < c.n_layers; ++l) {
     const void* kl = layer_ptr(m, kv.k, kv.layer_stride, l);
@@ -516,41 +569,24 @@ rp_status rp_prefix_workspace_bytes(const rp_model* m, int32_t B, const int32_t*
 rp_status rp_prefix_forward(const rp_model* m, void* stream, int32_t B, const int32_t* cu, const int32_t* token_ids,
                             const void* visual, int64_t n_visual, rp_kv kv_out, float* h_last, float* hidden_out,
                             void* ws, size_t ws_bytes) {
+  return prefix_run(m, stream, B, cu, token_ids, visual, n_visual, rp::MRope{nullptr, 0, 0}, kv_out, h_last,
+                    hidden_out, ws, ws_bytes);
+}
+
+rp_status rp_prefix_forward_mrope(const rp_model* m, void* stream, int32_t B, const int32_t* cu,
+                                  const int32_t* token_ids, const void* visual, int64_t n_visual,
+                                  const int32_t* positions, const int32_t* mrope_section, rp_kv kv_out,
+                                  float* h_last, float* hidden_out, void* ws, size_t ws_bytes) {
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
-  rp_status st = check_prefix_cu(m, B, cu, "cu_seqlens");
-  if (st != RP_OK) return st;
-  const int64_t T = cu[B];
-  if (!token_ids || !h_last) return fail(RP_ERR_INVALID_ARG, "token_ids and h_last are required");
-  if (n_visual < 0) return fail(RP_ERR_SHAPE, "n_visual %lld < 0", (long long)n_visual);
-  if (n_visual > 0 && !visual) return fail(RP_ERR_INVALID_ARG, "visual_embeds is NULL with n_visual > 0");
-  if (visual && !aligned16(visual)) return fail(RP_ERR_INVALID_ARG, "visual_embeds must be 16-byte aligned");
-  if ((hidden_out && !aligned16(hidden_out)) || !aligned16(h_last))
-    return fail(RP_ERR_INVALID_ARG, "h_last / hidden_out must be 16-byte aligned");
-  if ((st = check_kv(m, kv_out, T, "kv_out")) != RP_OK) return st;
-  const size_t need = prefix_ws(m, T, nullptr, hidden_out == nullptr, nullptr, nullptr);
-  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
-
-  hipStream_t s = (hipStream_t)stream;
-  const rp_config& c = m->cfg;
-  const rp_dtype dt = c.dtype;
-  LayerWS w;
-  int32_t* vis_idx = nullptr;
-  prefix_ws(m, T, ws, hidden_out == nullptr, &w, &vis_idx);
-  if (hidden_out) w.X = hidden_out;
-  const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
-  const LayerPlan plan = plan_layer(c, (int32_t)T, Pass::kPrefix);
-
-  RP_TRY_LAUNCH_N("prefix.visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
-  RP_TRY_LAUNCH_N("prefix.embed", rp::launch_embed(s, dt, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
-                                 c.d_model, w.X));
-  for (int l = 0; l < c.n_layers; ++l) {
-    void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
-    void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames);
-    if (st != RP_OK) return st;
-  }
-  RP_TRY_LAUNCH_N("prefix.gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
-  return RP_OK;
+  if (!positions || !mrope_section) return fail(RP_ERR_INVALID_ARG, "positions and mrope_section are required");
+  if (!aligned16(positions)) return fail(RP_ERR_INVALID_ARG, "positions must be 16-byte aligned");
+  const int half = m->cfg.head_dim / 2;
+  if (mrope_section[0] < 0 || mrope_section[1] < 0 || mrope_section[2] < 0 ||
+      mrope_section[0] + mrope_section[1] + mrope_section[2] != half)
+    return fail(RP_ERR_SHAPE, "mrope_section (%d, %d, %d) must be non-negative and sum to head_dim / 2 = %d",
+                mrope_section[0], mrope_section[1], mrope_section[2], half);
+  const rp::MRope mr = {positions, mrope_section[0], mrope_section[0] + mrope_section[1]};
+  return prefix_run(m, stream, B, cu, token_ids, visual, n_visual, mr, kv_out, h_last, hidden_out, ws, ws_bytes);
 }
 
 rp_status rp_suffix_workspace_bytes(const rp_model* m, int32_t B, const int32_t* pcu, const int32_t* scu,
@@ -568,7 +604,7 @@ rp_status rp_suffix_logprob(const rp_model* m, void* stream, int32_t B, const in
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
   rp_status st = check_suffix_cu(m, B, pcu, scu);
   if (st != RP_OK) return st;
-  return suffix_run(m, stream, B, pcu, B, nullptr, scu, 0u, kv, h_last, response_ids, logprobs, ws, ws_bytes);
+  return suffix_run(m, stream, B, pcu, B, nullptr, scu, nullptr, 0u, kv, h_last, response_ids, logprobs, ws, ws_bytes);
 }
 
 rp_status rp_suffix_grouped_workspace_bytes(const rp_model* m, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
@@ -584,14 +620,14 @@ rp_status rp_suffix_grouped_workspace_bytes(const rp_model* m, int32_t n_prefix,
 
 rp_status rp_suffix_logprob_grouped(const rp_model* m, void* stream, int32_t n_prefix, const int32_t* pcu,
                                     int32_t n_suffix, const int32_t* prefix_of_suffix, const int32_t* scu,
-                                    uint32_t flags, rp_kv kv, const float* h_last, const int32_t* response_ids,
-                                    float* logprobs, void* ws, size_t ws_bytes) {
+                                    const int32_t* rope_pos0, uint32_t flags, rp_kv kv, const float* h_last,
+                                    const int32_t* response_ids, float* logprobs, void* ws, size_t ws_bytes) {
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
   if (flags & ~RP_SUFFIX_FLAGS) return fail(RP_ERR_INVALID_ARG, "unknown suffix flags 0x%x", flags);
-  rp_status st = check_grouped_cu(m, n_prefix, pcu, n_suffix, prefix_of_suffix, scu);
+  rp_status st = check_grouped_cu(m, n_prefix, pcu, n_suffix, prefix_of_suffix, scu, rope_pos0);
   if (st != RP_OK) return st;
-  return suffix_run(m, stream, n_prefix, pcu, n_suffix, prefix_of_suffix, scu, flags, kv, h_last, response_ids,
-                    logprobs, ws, ws_bytes);
+  return suffix_run(m, stream, n_prefix, pcu, n_suffix, prefix_of_suffix, scu, rope_pos0, flags, kv, h_last,
+                    response_ids, logprobs, ws, ws_bytes);
 }
 
 rp_status rp_decode_workspace_bytes(const rp_model* m, int32_t B, int32_t cap, size_t* bytes) {

@@ -168,15 +168,18 @@ hipError_t launch_final_norm_rows(hipStream_t s, rp_dtype dt, const SeqTable& st
 // single rounding to the storage type happen here.  q (rotated) goes to q_dst, k
 // (rotated) and v to k_dst / v_dst.
 // ------------------------------------------------------------------------------------
+// Pair i rotates by position pos[0] for i < sec0, pos[1] for i < sec01, else pos[2]
+// (all equal for 1-D RoPE).
 template <typename T>
-__device__ __forceinline__ void rope_row(const float* __restrict__ row, int pos, int Hq, int Hkv, int D,
-                                         const T* __restrict__ bq, const T* __restrict__ bk,
-                                         const T* __restrict__ bv, const RopeFreq& rf, T* __restrict__ q_dst,
-                                         T* __restrict__ k_dst, T* __restrict__ v_dst, float* cs) {
+__device__ __forceinline__ void rope_row(const float* __restrict__ row, const int (&pos)[3], int sec0, int sec01,
+                                         int Hq, int Hkv, int D, const T* __restrict__ bq,
+                                         const T* __restrict__ bk, const T* __restrict__ bv, const RopeFreq& rf,
+                                         T* __restrict__ q_dst, T* __restrict__ k_dst, T* __restrict__ v_dst,
+                                         float* cs) {
   const int half = D >> 1;
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     float c, s;
-    rope_cs(pos, rf.inv_freq[i], &c, &s);
+    rope_cs(i < sec0 ? pos[0] : i < sec01 ? pos[1] : pos[2], rf.inv_freq[i], &c, &s);
     cs[i] = c;
     cs[64 + i] = s;
   }
@@ -214,27 +217,33 @@ __device__ __forceinline__ void rope_row(const float* __restrict__ row, int pos,
 template <typename T>
 __global__ __launch_bounds__(256) void k_rope_kv(SeqTable st, const float* __restrict__ qkv, int Hq, int Hkv,
                                                  int D, const T* __restrict__ bq, const T* __restrict__ bk,
-                                                 const T* __restrict__ bv, RopeFreq rf, int max_pos,
+                                                 const T* __restrict__ bv, RopeFreq rf, int max_pos, MRope mr, int M,
                                                  T* __restrict__ q_out, T* __restrict__ k_out,
                                                  T* __restrict__ v_out) {
   __shared__ float cs[128];
   const int r = blockIdx.x;
-  const int b = seq_of_row(st, r);
-  const int pos = min(st.pos0(b) + (r - st.q_cu[b]), max_pos - 1);
+  int pos[3];
+  if (mr.pos) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) pos[k] = min(max(mr.pos[(int64_t)k * M + r], 0), max_pos - 1);
+  } else {
+    const int b = seq_of_row(st, r);
+    pos[0] = pos[1] = pos[2] = min(max(st.rpos0(b) + (r - st.q_cu[b]), 0), max_pos - 1);
+  }
   const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
-  rope_row<T>(qkv + r * ld, pos, Hq, Hkv, D, bq, bk, bv, rf, q_out + (int64_t)r * Hq * D,
-              k_out + (int64_t)r * Hkv * D, v_out + (int64_t)r * Hkv * D, cs);
+  rope_row<T>(qkv + r * ld, pos, mr.pos ? mr.sec0 : D, mr.pos ? mr.sec01 : D, Hq, Hkv, D, bq, bk, bv, rf,
+              q_out + (int64_t)r * Hq * D, k_out + (int64_t)r * Hkv * D, v_out + (int64_t)r * Hkv * D, cs);
 }
 
 hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* qkv, int32_t M,
                           int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
                           const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
-                          void* v_out) {
+                          void* v_out, const MRope& mr) {
   if (M <= 0) return hipSuccess;
   with_storage(dt, [&](auto tag_) {
     using E = decltype(tag_);
     k_rope_kv<E><<<M, 256, 0, s>>>(st, qkv, Hq, Hkv, D, (const E*)bq, (const E*)bk,
-                                        (const E*)bv, rf, max_pos, (E*)q_out, (E*)k_out,
+                                        (const E*)bv, rf, max_pos, mr, M, (E*)q_out, (E*)k_out,
                                         (E*)v_out);
   });
   return hipGetLastError();
@@ -252,7 +261,8 @@ __global__ __launch_bounds__(256) void k_decode_rope_kv(const float* __restrict_
   const int slot = min(max(kv_len[b], 0), min(cap, max_pos) - 1);
   const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
   const int64_t dst = ((int64_t)b * cap + slot) * Hkv * D;
-  rope_row<T>(qkv + b * ld, slot, Hq, Hkv, D, bq, bk, bv, rf, q_out + (int64_t)b * Hq * D, ck + dst, cv + dst, cs);
+  const int p3[3] = {slot, slot, slot};
+  rope_row<T>(qkv + b * ld, p3, D, D, Hq, Hkv, D, bq, bk, bv, rf, q_out + (int64_t)b * Hq * D, ck + dst, cv + dst, cs);
 }
 
 hipError_t launch_decode_rope_kv(hipStream_t s, rp_dtype dt, const float* qkv, int32_t B, int32_t Hq, int32_t Hkv,

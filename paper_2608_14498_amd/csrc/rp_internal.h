@@ -16,12 +16,16 @@ struct SeqTable {
   int32_t n;                       // sequences
   int32_t q_cu[RP_MAX_SEQS + 1];   // query rows of sequence b: q_cu[b] .. q_cu[b+1]-1
   int32_t k_cu[RP_MAX_SEQS + 1];   // prefix p's KV rows: k_cu[p] .. k_cu[p+1]-1
-  int32_t grp[RP_MAX_SEQS];        // prefix of sequence b (b itself unless prefixes are shared)
+  int32_t rope0[RP_MAX_SEQS];      // rotary position of the first query row after prefix p
+  uint8_t grp[RP_MAX_SEQS];        // prefix of sequence b (b itself unless prefixes are shared)
   // first row and length of sequence b's first key segment; the length is also the
-  // position of b's first query row
+  // index of b's first query row in its key space (the causal rule)
   __host__ __device__ int32_t k_beg(int b) const { return k_cu[grp[b]]; }
   __host__ __device__ int32_t pos0(int b) const { return k_cu[grp[b] + 1] - k_cu[grp[b]]; }
+  // rotary position of b's first query row (pos0 unless the prefix used multimodal RoPE)
+  __host__ __device__ int32_t rpos0(int b) const { return rope0[grp[b]]; }
 };
+static_assert(RP_MAX_SEQS <= 256, "grp is one byte");
 
 // Row r of the packed queries -> sequence index (binary search over q_cu).
 __host__ __device__ inline int seq_of_row(const SeqTable& t, int r) {
@@ -79,10 +83,17 @@ hipError_t launch_final_norm_rows(hipStream_t s, rp_dtype dt, const SeqTable& st
                                   const float* h_last, const void* w, float eps, int32_t R, int32_t d,
                                   void* out);
 // qkv: fp32 projection rows [M, (Hq+2Hkv)*D]; q_out [M, Hq*D], k_out/v_out [M, Hkv*D] in T.
+// Row r of sequence b rotates by position st.rpos0(b) + (r - q_cu[b]), or, when mpos is
+// given (device int32 [3][M]), pair i by mpos[sec(i)][r] with sec(i) = 0 for i < sec0,
+// 1 for i < sec01, else 2 (multimodal RoPE).  Positions are clamped to [0, max_pos).
+struct MRope {
+  const int32_t* pos;  // NULL: 1-D positions
+  int32_t sec0, sec01;
+};
 hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* qkv, int32_t M,
                           int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
                           const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
-                          void* v_out);
+                          void* v_out, const MRope& mr);
 hipError_t launch_swiglu(hipStream_t s, rp_dtype dt, const void* gu, int32_t M, int32_t F, void* act);
 hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X, int32_t d, float* h_last);
 hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const int32_t* ids, int32_t R,

@@ -79,8 +79,10 @@ class DeviceModel:
 
     # ---------------------------------------------------------------- passes
     def prefix(self, cu: Sequence[int], token_ids: torch.Tensor, visual: Optional[torch.Tensor],
-               kv=None, h_last=None, hidden_out=None, workspace=None, stream=None):
-        """Prefix pass.  Returns (K, V, h_last) with K/V [L, T, Hkv, Dh]."""
+               kv=None, h_last=None, hidden_out=None, workspace=None, stream=None, positions=None,
+               mrope_section=None):
+        """Prefix pass.  Returns (K, V, h_last) with K/V [L, T, Hkv, Dh].  With positions
+        (device int32 [3, T]) and mrope_section, RoPE uses multimodal 3-D positions."""
         m = self.shape
         B, T = len(cu) - 1, int(cu[-1])
         K, V = kv if kv is not None else self.alloc_kv(T)
@@ -89,8 +91,13 @@ class DeviceModel:
         nbytes = rb.rp_prefix_workspace_bytes(self.handle, B, cu)
         ws = workspace if workspace is not None else self.workspace(nbytes)
         n_visual = 0 if visual is None else visual.shape[0]
-        rb.rp_prefix_forward(self.handle, stream_ptr(stream), B, cu, token_ids, visual, n_visual,
-                             rb.make_kv(K, V, K[0].numel()), h_last, hidden_out, ws, ws.numel())
+        if positions is None:
+            rb.rp_prefix_forward(self.handle, stream_ptr(stream), B, cu, token_ids, visual, n_visual,
+                                 rb.make_kv(K, V, K[0].numel()), h_last, hidden_out, ws, ws.numel())
+        else:
+            rb.rp_prefix_forward_mrope(self.handle, stream_ptr(stream), B, cu, token_ids, visual, n_visual,
+                                       positions, mrope_section, rb.make_kv(K, V, K[0].numel()), h_last,
+                                       hidden_out, ws, ws.numel())
         return K, V, h_last
 
     def suffix(self, prefix_cu, suffix_cu, K, V, h_last, response_ids, logprobs=None, workspace=None,
@@ -105,9 +112,10 @@ class DeviceModel:
         return logprobs
 
     def suffix_grouped(self, prefix_cu, prefix_of_suffix, suffix_cu, K, V, h_last, response_ids, logprobs=None,
-                       workspace=None, stream=None, flags: int = 0):
+                       workspace=None, stream=None, flags: int = 0, rope_pos0=None):
         """Suffix pass where suffix s reads prefix prefix_of_suffix[s] (shared prefixes);
-        flags = rb.RP_SUFFIX_FUSED_LOGPROB scores without storing the logits."""
+        flags = rb.RP_SUFFIX_FUSED_LOGPROB scores without storing the logits; rope_pos0[p]
+        is the rotary position of the first response token after prefix p (default P_p)."""
         P, S, R = len(prefix_cu) - 1, len(suffix_cu) - 1, int(suffix_cu[-1])
         if logprobs is None:
             logprobs = torch.empty(max(R, 1), dtype=torch.float32, device=self.device)[:R]
@@ -115,8 +123,8 @@ class DeviceModel:
                                                       flags)
         ws = workspace if workspace is not None else self.workspace(nbytes)
         rb.rp_suffix_logprob_grouped(self.handle, stream_ptr(stream), P, prefix_cu, S, prefix_of_suffix,
-                                     suffix_cu, flags, rb.make_kv(K, V, K[0].numel()), h_last, response_ids,
-                                     logprobs, ws, ws.numel())
+                                     suffix_cu, rope_pos0, flags, rb.make_kv(K, V, K[0].numel()), h_last,
+                                     response_ids, logprobs, ws, ws.numel())
         return logprobs
 
     def decode(self, cache_k, cache_v, kv_len, token_ids, logits=None, next_ids=None, workspace=None,

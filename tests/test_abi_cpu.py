@@ -162,17 +162,36 @@ def test_grouped_suffix_workspace_and_validation(lib):
         assert n == rb.rp_suffix_workspace_bytes(h, 8, list(range(0, 8 * 64 + 1, 64)), list(range(0, 72, 8)))
         m = configs.TINY
         kv = rb.make_kv(FAKE, FAKE + (1 << 30), 512 * m.n_kv_heads * m.head_dim)
-        args = [h, None, 1, [0, 512], 2, [0, 0], [0, 3, 5], 0, kv, None, FAKE + (1 << 31), FAKE + (1 << 32),
-                FAKE + (1 << 33), 1 << 30]
+        args = [h, None, 1, [0, 512], 2, [0, 0], [0, 3, 5], None, 0, kv, None, FAKE + (1 << 31),
+                FAKE + (1 << 32), FAKE + (1 << 33), 1 << 30]
         assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_INVALID_ARG   # h_last NULL
-        args[9] = FAKE + (1 << 34)
+        args[10] = FAKE + (1 << 34)
         need = rb.rp_suffix_grouped_workspace_bytes(h, 1, [0, 512], 2, [0, 0], [0, 3, 5])
-        args[13] = need - 1
+        args[14] = need - 1
         assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_WORKSPACE
-        args[13], args[7] = need, 6                                                        # unknown flag bits
+        args[14], args[8] = need, 6                                                        # unknown flag bits
         assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_INVALID_ARG
+        args[8], args[7] = 0, [1022]                        # rotary positions past max_position
+        assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_SHAPE
+        args[7] = [-1]
+        assert status_of(rb.rp_suffix_logprob_grouped, *args)[0] == rb.RP_ERR_SHAPE
         assert status_of(rb.rp_suffix_grouped_workspace_bytes, h, 1, [0, 512], 2, [0, 0], [0, 3, 5], 2)[0] == \
             rb.RP_ERR_INVALID_ARG
+    finally:
+        rb.rp_destroy(h)
+
+
+def test_prefix_mrope_validation(lib):
+    h, keep = make()
+    try:
+        args = list(_prefix_args(h))
+        base = [args[0], args[1], args[2], args[3], args[4], args[5], args[6]]
+        rest = args[7:]
+        pos = FAKE + (1 << 35)
+        assert status_of(rb.rp_prefix_forward_mrope, *base, None, [8, 12, 12], *rest)[0] == rb.RP_ERR_INVALID_ARG
+        assert status_of(rb.rp_prefix_forward_mrope, *base, pos, [8, 12, 13], *rest)[0] == rb.RP_ERR_SHAPE
+        assert status_of(rb.rp_prefix_forward_mrope, *base, pos, [-1, 17, 16], *rest)[0] == rb.RP_ERR_SHAPE
+        assert status_of(rb.rp_prefix_forward_mrope, *base, pos + 4, [8, 12, 12], *rest)[0] == rb.RP_ERR_INVALID_ARG
     finally:
         rb.rp_destroy(h)
 

@@ -210,3 +210,43 @@ def test_fused_logprob_scoring_matches_plain_and_oracle(model):
     assert d <= 1e-5
     assert err <= 2e-2
     dm.close()
+
+
+@pytest.mark.parametrize("model,sections", [(BF16_SMALL, (16, 24, 24)), (configs.TINY, (8, 12, 12)),
+                                            (F16_SMALL, (16, 24, 24))])
+def test_mrope_prefix_and_suffix_match_oracle(model, sections):
+    """Multimodal RoPE: visual tokens of a video grid at 3-D positions, text after them, the
+    responses continuing at each prefix's next rotary position."""
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+    from tests.test_oracle_pins import video_positions
+    P, Vis, S = [70, 300, 129], [60, 256, 100], [9, 65, 0]
+    grids = [(3, 4, 5), (4, 8, 8), (4, 5, 5)]
+    w = configs.custom(model, P, Vis, S, index=81)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    pos, nxt = zip(*[video_positions(v, p - v, g) for p, v, g in zip(P, Vis, grids)])
+    pos3 = np.concatenate(pos, axis=1).astype(np.int32)              # [3, T]
+    maxp = max(max(int(n) + s for n, s in zip(nxt, S)), max(p + s for p, s in zip(P, S))) + 1
+    dm = DeviceModel(hw, maxp)
+    dev = dm.device
+    cp, cs = [int(x) for x in bt.cu_prefix], [int(x) for x in bt.cu_suffix]
+    K, V, h = dm.prefix(cp, to_device(bt.token_ids, dev), to_device(bt.visual, dev),
+                        positions=torch.as_tensor(pos3, device=dev).contiguous(), mrope_section=list(sections))
+    lp = dm.suffix_grouped(cp, list(range(len(P))), cs, K, V, h, to_device(bt.response_ids, dev),
+                           rope_pos0=[int(n) for n in nxt])
+    torch.cuda.synchronize()
+    W = hw.as_f32()
+    vo = np.concatenate([[0], np.cumsum(Vis)])
+    vis = inputs.to_f32(bt.visual)
+    errs = dict(k=0.0, lp=0.0)
+    for b in range(len(P)):
+        ids = bt.token_ids[cp[b]:cp[b + 1]]
+        k, v, hl, _ = oracle.prefix_forward_one(W, model, ids, vis[vo[b]:vo[b + 1]], mrope=(pos[b], sections))
+        errs["k"] = max(errs["k"], rel_err(K[:, cp[b]:cp[b + 1]].float().cpu().numpy(), k))
+        lpo = oracle.suffix_logprob_one(W, model, k, v, hl, bt.response_ids[cs[b]:cs[b + 1]], rope_start=nxt[b])
+        errs["lp"] = max(errs["lp"], max_abs(lp[cs[b]:cs[b + 1]].cpu().numpy(), lpo))
+    print(f"[parity] mrope {model.dtype} D={model.head_dim}: {errs}", flush=True)
+    f32 = model.dtype == "f32"
+    assert errs["lp"] <= (1e-4 if f32 else 2e-2)
+    assert errs["k"] <= (1e-5 if f32 else 3e-2)
+    dm.close()
