@@ -200,6 +200,26 @@ def prefix_forward_one(weights, cfg, token_ids, visual, mrope=None):
     return np.stack(Ks), np.stack(Vs), x[P - 1].copy(), x
 
 
+def prompt_logprob_one(weights, cfg, token_ids, visual, mrope=None):
+    """Teacher-forced log-probabilities of the prompt's own text tokens (the prefix-side
+    log-probabilities of Section "Cross-Phase Execution": they depend on the prompt and
+    the weights only, so the prefix pass can produce them).
+
+    Entry t is log p(id_t | tokens before t), scored like a response token from the
+    final hidden state one position earlier (row t-1 of the prefix pass), for every
+    text token (id_t >= 0) after position 0.  NaN at position 0 and at visual slots:
+    the model predicts no visual embedding.
+    """
+    ids = np.asarray(token_ids)
+    out = np.full(len(ids), np.nan)
+    t = np.nonzero(ids[1:] >= 0)[0] + 1
+    if len(t) == 0:
+        return out
+    _, _, _, x = prefix_forward_one(weights, cfg, ids, visual, mrope)
+    out[t] = score_rows(weights, cfg, x[t - 1], ids[t])
+    return out
+
+
 def score_rows(weights, cfg, z, ids):
     """Final RMSNorm, lm_head, and log-probability of ids under each row of z."""
     h = rmsnorm(z, weights.final_norm, cfg.rms_eps)
@@ -277,6 +297,20 @@ def prefix_forward(weights, cfg, cu_prefix, token_ids, visual, seqs: Optional[Se
         V[:, cu[b]:cu[b + 1]] = v
         H[b] = h
     return K, V, H
+
+
+def prompt_logprob(weights, cfg, cu_prefix, token_ids, visual, seqs: Optional[Sequence[int]] = None):
+    """Packed prompt-token log-probabilities [T] (prompt_logprob_one per sequence; NaN at
+    each sequence's first token, at visual slots and for sequences not in ``seqs``)."""
+    cu = np.asarray(cu_prefix)
+    B = len(cu) - 1
+    ids = np.asarray(token_ids)
+    out = np.full(int(cu[-1]), np.nan)
+    vis_start = np.concatenate([[0], np.cumsum([(ids[cu[b]:cu[b + 1]] < 0).sum() for b in range(B)])])
+    for b in (range(B) if seqs is None else seqs):
+        out[cu[b]:cu[b + 1]] = prompt_logprob_one(weights, cfg, ids[cu[b]:cu[b + 1]],
+                                                  visual[vis_start[b]:vis_start[b + 1]])
+    return out
 
 
 def suffix_logprob(weights, cfg, cu_prefix, cu_suffix, K, V, h_last, response_ids,

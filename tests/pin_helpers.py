@@ -14,8 +14,9 @@ import numpy as np
 import torch
 
 
-def hf_qwen2(weights, cfg, token_ids, visual, response_ids):
-    """Returns (logprobs [S], keys [L][P+S, Hkv, Dh], values, h_last_prefix [d])."""
+def hf_qwen2(weights, cfg, token_ids, visual, response_ids, full_logp=False):
+    """Returns (logprobs [S], keys [L][P+S, Hkv, Dh], values, h_last_prefix [d]), and with
+    full_logp the library's log-softmax over every position [P+S, V] as a fifth item."""
     from transformers import Qwen2Config, Qwen2ForCausalLM
 
     L = len(weights.layers)
@@ -69,6 +70,8 @@ def hf_qwen2(weights, cfg, token_ids, visual, response_ids):
     vals = [out.past_key_values.layers[l].values[0].transpose(0, 1).numpy() for l in range(L)]
     h = captured["h"]
     h = h[0] if h.dim() == 3 else h
+    if full_logp:
+        return lp, keys, vals, h[P - 1].numpy(), logp.numpy()
     return lp, keys, vals, h[P - 1].numpy()
 
 

@@ -21,7 +21,7 @@ def _pins_hold() -> bool:
     """True iff every pin below still holds."""
     w, W, bt = _setup(P=(19,), Vis=(11,), S=(6,))
     ids, vis, resp = _seq(bt, 0)
-    lp_hf, keys, _, _ = hf_qwen2(W, SMALL, ids, vis, resp)
+    lp_hf, keys, _, _, logp = hf_qwen2(W, SMALL, ids, vis, resp, full_logp=True)
     K, V, h, _ = ob.prefix_forward_one(W, SMALL, ids, vis)
     lp = ob.suffix_logprob_one(W, SMALL, K, V, h, resp)
     lpu = ob.unsplit_logprob_one(W, SMALL, ids, vis, resp)
@@ -50,6 +50,11 @@ def _pins_hold() -> bool:
     lps = ob.suffix_logprob_one(W2, SMALL, K2, V2, h2, resp2, rope_start=nxt)
     lpu2 = ob.unsplit_logprob_one(W2, SMALL, ids2, vis2, resp2, mrope=(p3, MROPE_SMALL), rope_start=nxt)
     ok &= bool(np.max(np.abs(lps - lpu2)) < 1e-10)
+    # prompt-token log-probabilities vs the library's teacher-forced log-softmax
+    lpp = ob.prompt_logprob_one(W, SMALL, ids, vis)
+    t = np.nonzero(ids >= 0)[0]
+    t = t[t > 0]
+    ok &= bool(np.max(np.abs(lpp[t] - logp[t - 1, ids[t]])) < HF_TOL)
     return bool(ok)
 
 
@@ -146,6 +151,15 @@ def _suffix_restarts_at_prefix_length(weights, cfg, K, V, h_last, response_ids, 
     return ORIG["suffix_logprob_one"](weights, cfg, K, V, h_last, response_ids)
 
 
+def _prompt_from_own_row(weights, cfg, token_ids, visual, mrope=None):
+    ids = np.asarray(token_ids)
+    out = np.full(len(ids), np.nan)
+    t = np.nonzero(ids[1:] >= 0)[0] + 1
+    _, _, _, x = ob.prefix_forward_one(weights, cfg, ids, visual, mrope)
+    out[t] = ob.score_rows(weights, cfg, x[t], ids[t])
+    return out
+
+
 ORIG = {n: getattr(ob, n) for n in ("attention", "rmsnorm", "decoder_layer", "apply_rope",
                                     "rope_angles", "rope_angles_mrope", "silu", "suffix_logprob_one")}
 
@@ -164,6 +178,7 @@ MUTATIONS = {
     "suffix_scores_from_own_row": ("suffix_logprob_one", _suffix_no_boundary),
     "mrope_sections_reversed": ("rope_angles_mrope", _mrope_sections_reversed),
     "mrope_suffix_restarts_at_prefix_length": ("suffix_logprob_one", _suffix_restarts_at_prefix_length),
+    "prompt_scored_from_own_row": ("prompt_logprob_one", _prompt_from_own_row),
 }
 
 

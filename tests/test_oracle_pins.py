@@ -314,6 +314,53 @@ def test_shared_prefix_suffixes_equal_unsplit_forward():
     assert np.max(np.abs(lp_wrong[cs[2]:cs[3]] - lp[cs[2]:cs[3]])) > 1e-3
 
 
+# ----------------------------------------------------------------------------------------
+# prompt-token log-probabilities (teacher forcing over the prefix's own text tokens)
+# ----------------------------------------------------------------------------------------
+def _interleaved_prompt(bt, P, n_vis):
+    """The batch's one prompt with its visual slots moved to the middle (text, visual, text),
+    so that text tokens follow visual rows and visual rows follow text."""
+    ids, vis, resp = _seq(bt, 0)
+    text = ids[ids >= 0]
+    a = len(text) // 3
+    return np.concatenate([text[:a], np.full(n_vis, -1, np.int32), text[a:]]).astype(np.int32), vis, resp
+
+
+def test_prompt_logprobs_match_transformers():
+    w, W, bt = _setup(P=(26,), Vis=(9,), S=(3,), index=13)
+    ids, vis, resp = _interleaved_prompt(bt, 26, 9)
+    *_, logp = hf_qwen2(W, SMALL, ids, vis, resp, full_logp=True)
+    lp = oracle.prompt_logprob_one(W, SMALL, ids, vis)
+    scored = np.nonzero((ids >= 0) & (np.arange(26) > 0))[0]
+    assert np.all(np.isnan(lp[np.setdiff1d(np.arange(26), scored)]))
+    ref = np.array([logp[t - 1, ids[t]] for t in scored])
+    assert np.max(np.abs(lp[scored] - ref)) < HF_TOL
+    assert len(scored) == 26 - 9 - 1   # position 0 is text here
+
+
+def test_prompt_logprobs_equal_response_scoring_of_the_same_tokens():
+    # Scoring the prompt's text tail as a response over the shorter prefix gives the same values.
+    w, W, bt = _setup(P=(30,), Vis=(14,), S=(2,), index=17)
+    ids, vis, _ = _seq(bt, 0)
+    lp = oracle.prompt_logprob_one(W, SMALL, ids, vis)
+    for k in (14, 15, 22, 29):
+        K, V, h, _ = oracle.prefix_forward_one(W, SMALL, ids[:k], vis)
+        tail = oracle.suffix_logprob_one(W, SMALL, K, V, h, ids[k:])
+        assert np.max(np.abs(lp[k:] - tail)) < 1e-10
+
+
+def test_prompt_logprobs_packed_and_edge_cases():
+    w, W, bt = _setup(P=(1, 9, 6, 5), Vis=(0, 4, 6, 0), S=(1, 1, 1, 1), index=19)
+    lp = oracle.prompt_logprob(W, SMALL, bt.cu_prefix, bt.token_ids, inputs.to_f32(bt.visual))
+    cu = bt.cu_prefix
+    for b in range(4):
+        ids, vis, _ = _seq(bt, b)
+        np.testing.assert_array_equal(lp[cu[b]:cu[b + 1]], oracle.prompt_logprob_one(W, SMALL, ids, vis))
+    assert np.isnan(lp[cu[0]])                      # a one-token prompt scores nothing
+    assert np.all(np.isnan(lp[cu[2]:cu[3]]))        # an all-visual prompt scores nothing
+    assert np.all(np.isfinite(lp[cu[3] + 1:cu[4]])) and np.all(lp[cu[3] + 1:cu[4]] < 0)
+
+
 def test_prefix_is_response_independent():
     w, W, bt = _setup(P=(12,), Vis=(8,), S=(5,))
     ids, vis, resp = _seq(bt, 0)
