@@ -233,6 +233,8 @@ def main():
                     help="skip timing the fp16 variant of a bf16 workload")
     ap.add_argument("--no-fused-variant", action="store_true",
                     help="skip timing the suffix with the fused lm_head + log-sum-exp scoring")
+    ap.add_argument("--no-prompt-logprobs", action="store_true",
+                    help="skip timing the prompt-token log-probs (rp_prompt_logprob)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -320,6 +322,7 @@ def main():
         "suffix_mfma_frac": sf["total"] / (suf_ms * 1e-3) / peak,
         "roofline": roofline,
         "logsoftmax_roofline": k12,
+        "prompt_logprobs": res["prompt"],
         "kernels": kernels,
     }
     if m.dtype == "bf16" and not args.no_f16_variant:
@@ -435,10 +438,54 @@ def run_passes(w, args, profile: bool, flags: int = 0):
         rb.rp_profile_enable(False)
         kernels = {k: {"launches": n, "avg_ms": ms / max(n, 1), "ms_per_step": ms / args.profile_steps}
                    for k, (n, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1])}
+    prompt = None
+    if profile and not args.no_prompt_logprobs:
+        prompt = time_prompt_logprobs(dm, args, bt, cu_p, ids, vis, (K, V), h_last, ws_p, stream)
     dm.close()
     del K, V, ids, vis, resp, ws_p, ws_s
     torch.cuda.empty_cache()
-    return dict(T=T, R=R, B=B, bt=bt, hw=hw, ms_step=ms_step, pre_ms=pre_ms, suf_ms=suf_ms, kernels=kernels)
+    return dict(T=T, R=R, B=B, bt=bt, hw=hw, ms_step=ms_step, pre_ms=pre_ms, suf_ms=suf_ms, kernels=kernels,
+                prompt=prompt)
+
+
+def time_prompt_logprobs(dm, args, bt, cu_p, ids, vis, kv, h_last, ws_p, stream):
+    """Teacher-forced log-probs of every prompt text token, scored from the prefix pass's
+    hidden states (rp_prompt_logprob), plain and with the fused lm_head scoring."""
+    import numpy as np
+    import torch
+
+    from paper_2608_14498_amd import binding as rb
+    from paper_2608_14498_amd.runtime import prompt_positions, to_device
+
+    m = dm.shape
+    hidden = torch.empty((bt.T, m.d_model), dtype=torch.float32, device=dm.device)
+    dm.prefix(cu_p, ids, vis, kv=kv, h_last=h_last, hidden_out=hidden, workspace=ws_p, stream=stream)
+    pos = to_device(prompt_positions(cu_p, bt.token_ids), dm.device)
+    n = int(pos.numel())
+    out = {"rows": n}
+    variants = [("plain", 0)] + ([("fused", rb.RP_SUFFIX_FUSED_LOGPROB)] if m.dtype != "f32" else [])
+    for name, flags in variants:
+        ws = dm.workspace(rb.rp_prompt_logprob_workspace_bytes(dm.handle, n, flags))
+        lp = torch.empty(max(n, 1), dtype=torch.float32, device=dm.device)[:n]
+        for _ in range(2):
+            dm.prompt_logprobs(cu_p, ids, hidden, pos, logprobs=lp, workspace=ws, stream=stream, flags=flags)
+        reps = max(args.steps, 5)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            dm.prompt_logprobs(cu_p, ids, hidden, pos, logprobs=lp, workspace=ws, stream=stream, flags=flags)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        if not np.all(np.isfinite(lp.cpu().numpy())):
+            raise RuntimeError("non-finite prompt log-probs")
+        out[f"{name}_ms"] = ms
+        out[f"{name}_rows_per_s"] = n / (ms * 1e-3)
+        del ws, lp
+    del hidden
+    log(f"prompt log-probs: {out}")
+    return out
 
 
 if __name__ == "__main__":

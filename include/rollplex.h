@@ -229,6 +229,31 @@ rp_status rp_suffix_logprob_grouped(const rp_model *model, void *stream, int32_t
                                     size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
+ * Prompt-token log-probabilities (the response-independent "prefix log-probs"
+ * of Section "Observation and Opportunity", produced from the prefix pass's
+ * output): teacher-forced log-probabilities of the prompt's own text tokens.
+ * B, cu_seqlens_host and token_ids describe the packed prefixes exactly as in
+ * rp_prefix_forward; hidden is that call's hidden_out (dev fp32 [T, d], the
+ * last-layer residual stream before the final norm, 16-byte aligned).
+ * positions (dev int32 [n_rows]) lists packed prompt positions t; then
+ *   logprobs[i] = log p(token_ids[t] | the tokens of t's sequence before t),
+ * scored like a response token from row t-1 (final norm, lm_head, log-softmax
+ * over the vocabulary).  logprobs[i] is NaN when t is outside [0, T), is the
+ * first token of its sequence, or is a visual slot (token_ids[t] < 0).
+ * Positions may repeat and come in any order.  n_rows >= 0 (else RP_ERR_SHAPE);
+ * n_rows = 0 launches nothing.  flags as in rp_suffix_logprob_grouped
+ * (RP_SUFFIX_FUSED_LOGPROB: never store the [n_rows, V] logits); query the
+ * workspace with the same flags.  Asynchronous on stream; inputs are read only.
+ * ------------------------------------------------------------------------- */
+rp_status rp_prompt_logprob_workspace_bytes(const rp_model *model, int32_t n_rows, uint32_t flags,
+                                            size_t *bytes);
+rp_status rp_prompt_logprob(const rp_model *model, void *stream, int32_t B,
+                            const int32_t *cu_seqlens_host, const int32_t *token_ids,
+                            const float *hidden, int32_t n_rows, const int32_t *positions,
+                            uint32_t flags, float *logprobs, void *workspace,
+                            size_t workspace_bytes);
+
+/* ---------------------------------------------------------------------------
  * Rollout decode step (the memory-bound phase that the prefix pass overlaps
  * with; Section "Observation and Opportunity" and Eq. (1)).  One new token
  * per sequence: token_ids[b] runs at position kv_len[b], its K/V are written

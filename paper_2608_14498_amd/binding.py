@@ -23,7 +23,8 @@ RP_MAX_SEQS = 256
 RP_SUFFIX_FUSED_LOGPROB = 1
 SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_forward", "rp_prefix_forward_mrope",
            "rp_suffix_workspace_bytes", "rp_suffix_logprob", "rp_suffix_grouped_workspace_bytes",
-           "rp_suffix_logprob_grouped", "rp_decode_workspace_bytes",
+           "rp_suffix_logprob_grouped", "rp_prompt_logprob_workspace_bytes", "rp_prompt_logprob",
+           "rp_decode_workspace_bytes",
            "rp_decode_step", "rp_stream_create_cu_masked", "rp_stream_destroy",
            "rp_device_cu_count", "rp_last_error", "rp_status_string", "rp_version",
            "rp_profile_enable", "rp_profile_collect", "rp_profile_count", "rp_profile_read",
@@ -86,6 +87,9 @@ def lib():
             "rp_prefix_forward_mrope": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
                                                 c_int64, c_void_p, POINTER(c_int32), RpKV, c_void_p, c_void_p,
                                                 c_void_p, c_size_t]),
+            "rp_prompt_logprob_workspace_bytes": (c_int, [c_void_p, c_int32, c_uint32, POINTER(c_size_t)]),
+            "rp_prompt_logprob": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
+                                          c_int32, c_void_p, c_uint32, c_void_p, c_void_p, c_size_t]),
             "rp_decode_workspace_bytes": (c_int, [c_void_p, c_int32, c_int32, POINTER(c_size_t)]),
             "rp_decode_step": (c_int, [c_void_p, c_void_p, c_int32, RpKV, c_int32, c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_size_t]),
@@ -209,6 +213,19 @@ def rp_prefix_forward_mrope(model: int, stream, B: int, cu_seqlens, token_ids, v
                                          _ptr(visual_embeds), int(n_visual), _ptr(positions), _i32(mrope_section),
                                          kv_out, _ptr(h_last), _ptr(hidden_out), _ptr(workspace),
                                          int(workspace_bytes)))
+
+
+def rp_prompt_logprob_workspace_bytes(model: int, n_rows: int, flags: int = 0) -> int:
+    n = c_size_t()
+    _check(lib().rp_prompt_logprob_workspace_bytes(model, int(n_rows), int(flags), byref(n)))
+    return n.value
+
+
+def rp_prompt_logprob(model: int, stream, B: int, cu_seqlens, token_ids, hidden, n_rows: int, positions,
+                      flags: int, logprobs, workspace, workspace_bytes: int) -> None:
+    _check(lib().rp_prompt_logprob(model, _ptr(stream), B, _i32(cu_seqlens), _ptr(token_ids), _ptr(hidden),
+                                   int(n_rows), _ptr(positions), int(flags), _ptr(logprobs), _ptr(workspace),
+                                   int(workspace_bytes)))
 
 
 def rp_decode_workspace_bytes(model: int, B: int, cap: int) -> int:

@@ -176,8 +176,6 @@ rp_status check_suffix_cu(const rp_model* m, int32_t B, const int32_t* pcu, cons
   return RP_OK;
 }
 
-// Sequence table: query rows q_cu[0..B]; the key segment of sequence b is prefix grp[b]
-// (b when grp is NULL) of the n_k prefixes k_cu[0..n_k] (none when k_cu is NULL).
 // Shared-prefix suffixes: n_suffix sequences, sequence s scores against prefix
 // prefix_of_suffix[s] of the n_prefix prefixes.
 rp_status check_grouped_cu(const rp_model* m, int32_t n_prefix, const int32_t* pcu, int32_t n_suffix,
@@ -314,6 +312,30 @@ size_t suffix_ws(const rp_model* m, int64_t R, uint32_t flags, void* base, Suffi
     s->logits = (float*)c.take(R * (int64_t)m->cfg.vocab * 4);
   }
   s->gemm_part = (float*)c.take(s->plan.part_floats * 4);
+  return c.off + 256;
+}
+
+struct PromptWS {
+  void* N;        // [n, d] final-norm rows
+  int32_t* tid;   // [n] scored token id, -1 for an invalid position
+  float* logits;  // [n, V] fp32 (unfused scoring)
+  float* lse;     // [n, n_part] float2 and
+  float* tgt;     // [n] (fused scoring)
+};
+
+size_t prompt_ws(const rp_model* m, int64_t n, uint32_t flags, void* base, PromptWS* w) {
+  Carver c(base);
+  PromptWS tmp;
+  PromptWS* p = w ? w : &tmp;
+  p->N = c.take(n * m->cfg.d_model * elem_size(m->cfg));
+  p->tid = (int32_t*)c.take(n * 4);
+  p->logits = p->lse = p->tgt = nullptr;
+  if (fused_scoring(m, flags)) {
+    p->lse = (float*)c.take(n * (int64_t)rp::lse_parts(m->cfg.vocab) * 8);
+    p->tgt = (float*)c.take(n * 4);
+  } else {
+    p->logits = (float*)c.take(n * (int64_t)m->cfg.vocab * 4);
+  }
   return c.off + 256;
 }
 
@@ -628,6 +650,52 @@ rp_status rp_suffix_logprob_grouped(const rp_model* m, void* stream, int32_t n_p
   if (st != RP_OK) return st;
   return suffix_run(m, stream, n_prefix, pcu, n_suffix, prefix_of_suffix, scu, rope_pos0, flags, kv, h_last,
                     response_ids, logprobs, ws, ws_bytes);
+}
+
+rp_status rp_prompt_logprob_workspace_bytes(const rp_model* m, int32_t n_rows, uint32_t flags, size_t* bytes) {
+  if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
+  if (flags & ~RP_SUFFIX_FLAGS) return fail(RP_ERR_INVALID_ARG, "unknown scoring flags 0x%x", flags);
+  if (n_rows < 0) return fail(RP_ERR_SHAPE, "n_rows %d < 0", n_rows);
+  *bytes = prompt_ws(m, n_rows, flags, nullptr, nullptr);
+  return RP_OK;
+}
+
+rp_status rp_prompt_logprob(const rp_model* m, void* stream, int32_t B, const int32_t* cu, const int32_t* token_ids,
+                            const float* hidden, int32_t n_rows, const int32_t* positions, uint32_t flags,
+                            float* logprobs, void* ws, size_t ws_bytes) {
+  if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  if (flags & ~RP_SUFFIX_FLAGS) return fail(RP_ERR_INVALID_ARG, "unknown scoring flags 0x%x", flags);
+  rp_status st = check_prefix_cu(m, B, cu, "cu_seqlens");
+  if (st != RP_OK) return st;
+  if (n_rows < 0) return fail(RP_ERR_SHAPE, "n_rows %d < 0", n_rows);
+  if (n_rows > 0 && (!token_ids || !hidden || !positions || !logprobs))
+    return fail(RP_ERR_INVALID_ARG, "token_ids, hidden, positions and logprobs are required");
+  if (hidden && !aligned16(hidden)) return fail(RP_ERR_INVALID_ARG, "hidden must be 16-byte aligned");
+  if ((st = check_ws(ws, ws_bytes, prompt_ws(m, n_rows, flags, nullptr, nullptr))) != RP_OK) return st;
+  if (n_rows == 0) return RP_OK;
+
+  hipStream_t s = (hipStream_t)stream;
+  const rp_config& c = m->cfg;
+  const rp_dtype dt = c.dtype;
+  PromptWS w;
+  prompt_ws(m, n_rows, flags, ws, &w);
+  const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
+  RP_TRY_LAUNCH_N("prompt.rows", rp::launch_prompt_rows(s, dt, tab, positions, n_rows, token_ids, cu[B], hidden,
+                                                        m->final_norm, c.rms_eps, c.d_model, w.N, w.tid));
+  rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
+  if (fused_scoring(m, flags)) {
+    const rp::LseOut lo = {w.tid, w.lse, w.tgt};
+    RP_TRY_LAUNCH_N("prompt.gemm_lm_head_lse", rp::launch_gemm(s, dt, n_rows, c.vocab, c.d_model, w.N, c.d_model, blm,
+                                                               c.d_model, nullptr, c.vocab, rp::EPI_LSE, 1, nullptr, &lo));
+    RP_TRY_LAUNCH_N("prompt.lse_combine",
+                    rp::launch_lse_combine(s, w.lse, w.tgt, n_rows, rp::lse_parts(c.vocab), logprobs, w.tid));
+    return RP_OK;
+  }
+  RP_TRY_LAUNCH_N("prompt.gemm_lm_head", rp::launch_gemm(s, dt, n_rows, c.vocab, c.d_model, w.N, c.d_model, blm,
+                                                         c.d_model, w.logits, c.vocab, rp::EPI_STORE_F32, 1, nullptr));
+  RP_TRY_LAUNCH_N("prompt.logsoftmax_gather",
+                  rp::launch_logsoftmax_gather(s, w.logits, w.tid, n_rows, c.vocab, logprobs, true));
+  return RP_OK;
 }
 
 rp_status rp_decode_workspace_bytes(const rp_model* m, int32_t B, int32_t cap, size_t* bytes) {

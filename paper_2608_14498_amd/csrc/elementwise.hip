@@ -162,6 +162,47 @@ hipError_t launch_final_norm_rows(hipStream_t s, rp_dtype dt, const SeqTable& st
   return hipGetLastError();
 }
 
+// Prompt scoring rows: row i scores the prompt token at packed position t = pos[i] from
+// the final hidden state at t-1.  Valid iff 0 <= t < T, t is not its sequence's first
+// token and ids[t] >= 0 (a text token); then out[i] = RMSNorm(hidden[t-1]) and tid[i] =
+// ids[t], else out[i] = 0 and tid[i] = -1 (the scoring kernels turn -1 into NaN).
+template <typename T>
+__global__ __launch_bounds__(256) void k_prompt_rows(SeqTable st, const int32_t* __restrict__ pos,
+                                                     const int32_t* __restrict__ ids, int32_t Ttot,
+                                                     const float* __restrict__ hidden,
+                                                     const T* __restrict__ w, float eps, int d,
+                                                     T* __restrict__ out, int32_t* __restrict__ tid) {
+  __shared__ float red[16];
+  const int i = blockIdx.x;
+  const int t = pos[i];
+  bool ok = t > 0 && t < Ttot;
+  int id = -1;
+  if (ok) {
+    const int b = seq_of_row(st, t);
+    id = ids[t];
+    ok = t != st.q_cu[b] && id >= 0;
+  }
+  T* o = out + (int64_t)i * d;
+  if (ok) {
+    rmsnorm_row(hidden + (int64_t)(t - 1) * d, w, eps, d, o, red);
+  } else {
+    float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) store8(o + c, z);
+  }
+  if (threadIdx.x == 0) tid[i] = ok ? id : -1;
+}
+
+hipError_t launch_prompt_rows(hipStream_t s, rp_dtype dt, const SeqTable& st, const int32_t* pos, int32_t n,
+                              const int32_t* ids, int32_t T, const float* hidden, const void* w, float eps,
+                              int32_t d, void* out, int32_t* tid) {
+  if (n <= 0) return hipSuccess;
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_prompt_rows<E><<<n, 256, 0, s>>>(st, pos, ids, T, hidden, (const E*)w, eps, d, (E*)out, tid);
+  });
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------------------------
 // RoPE (rotate-half pairs (i, i+D/2)) + optional q/k/v bias + Q/K/V materialisation.
 // The projection row arrives in fp32 (the GEMM accumulator); bias, rotation and the
@@ -342,7 +383,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 template <int NT>
 __global__ __launch_bounds__(NT) void k_logsoftmax_gather(const float* __restrict__ logits,
                                                           const int32_t* __restrict__ ids, int V,
-                                                          float* __restrict__ lp) {
+                                                          int neg_nan, float* __restrict__ lp) {
   const int r = blockIdx.x;
   const float* row = logits + (int64_t)r * V;
   float m = -INFINITY, s = 0.f;  // in log2 units
@@ -399,21 +440,22 @@ __global__ __launch_bounds__(NT) void k_logsoftmax_gather(const float* __restric
     float M = sm[0], S = ss[0];
     for (int k = 1; k < NT / 64; ++k) lse_merge(M, S, sm[k], ss[k]);
     const int id = min(max(ids[r], 0), V - 1);
-    lp[r] = row[id] - (M + log2f(S)) * kLn2;
+    lp[r] = (neg_nan && ids[r] < 0) ? __builtin_nanf("") : row[id] - (M + log2f(S)) * kLn2;
   }
 }
 
 hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const int32_t* ids, int32_t R,
-                                    int32_t V, float* lp) {
+                                    int32_t V, float* lp, bool neg_nan) {
   if (R <= 0) return hipSuccess;
-  k_logsoftmax_gather<256><<<R, 256, 0, s>>>(logits, ids, V, lp);
+  k_logsoftmax_gather<256><<<R, 256, 0, s>>>(logits, ids, V, neg_nan ? 1 : 0, lp);
   return hipGetLastError();
 }
 
 // Log-probs from the lm_head's online log-sum-exp partials (EPI_LSE): one wave per row
 // merges the row's n_part (max, sum) pairs, lp = tgt - (M + log2 S) ln 2.
 __global__ __launch_bounds__(64) void k_lse_combine(const float2* __restrict__ lse, const float* __restrict__ tgt,
-                                                    int n_part, float* __restrict__ lp) {
+                                                    int n_part, const int32_t* __restrict__ nan_ids,
+                                                    float* __restrict__ lp) {
   const int r = blockIdx.x;
   const float2* p = lse + (int64_t)r * n_part;
   float m = -INFINITY, s = 0.f;
@@ -426,13 +468,14 @@ __global__ __launch_bounds__(64) void k_lse_combine(const float2* __restrict__ l
     const float mo = __shfl_xor(m, o, kWave), so = __shfl_xor(s, o, kWave);
     lse_merge(m, s, mo, so);
   }
-  if (threadIdx.x == 0) lp[r] = tgt[r] - (m + log2f(s)) * kLn2;
+  if (threadIdx.x == 0)
+    lp[r] = (nan_ids && nan_ids[r] < 0) ? __builtin_nanf("") : tgt[r] - (m + log2f(s)) * kLn2;
 }
 
 hipError_t launch_lse_combine(hipStream_t s, const float* lse, const float* tgt, int32_t R, int32_t n_part,
-                              float* lp) {
+                              float* lp, const int32_t* nan_ids) {
   if (R <= 0) return hipSuccess;
-  k_lse_combine<<<R, 64, 0, s>>>(reinterpret_cast<const float2*>(lse), tgt, n_part, lp);
+  k_lse_combine<<<R, 64, 0, s>>>(reinterpret_cast<const float2*>(lse), tgt, n_part, nan_ids, lp);
   return hipGetLastError();
 }
 

@@ -96,8 +96,15 @@ hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const 
                           void* v_out, const MRope& mr);
 hipError_t launch_swiglu(hipStream_t s, rp_dtype dt, const void* gu, int32_t M, int32_t F, void* act);
 hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X, int32_t d, float* h_last);
+// lp[r] = log softmax(logits[r])[ids[r]] (ids clamped to [0, V)); NaN where ids[r] < 0
+// when neg_nan is set.
 hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const int32_t* ids, int32_t R,
-                                    int32_t V, float* lp);
+                                    int32_t V, float* lp, bool neg_nan = false);
+// Prompt scoring rows (see rp_prompt_logprob): out[i] = final-norm(hidden[pos[i] - 1]) and
+// tid[i] = ids[pos[i]] for a valid text position, else a zero row and tid[i] = -1.
+hipError_t launch_prompt_rows(hipStream_t s, rp_dtype dt, const SeqTable& st, const int32_t* pos, int32_t n,
+                              const int32_t* ids, int32_t T, const float* hidden, const void* w, float eps,
+                              int32_t d, void* out, int32_t* tid);
 hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t V, int32_t* out);
 
 // GEMM: C[M,N] (epi)= A[M,K] . B[N,K]^T, fp32 accumulation.  For EPI_SWIGLU, N is the
@@ -106,9 +113,10 @@ hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t 
 hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
                        int32_t splitk, float* partials, const LseOut* lse = nullptr);
-// lp[r] = tgt[r] - log sum_v exp(logit_rv) from the EPI_LSE partials.
+// lp[r] = tgt[r] - log sum_v exp(logit_rv) from the EPI_LSE partials; NaN where
+// nan_ids[r] < 0 (nan_ids nullable).
 hipError_t launch_lse_combine(hipStream_t s, const float* lse, const float* tgt, int32_t R, int32_t n_part,
-                              float* lp);
+                              float* lp, const int32_t* nan_ids = nullptr);
 // Required float count of `partials` for a split-K GEMM.
 size_t gemm_partial_floats(int32_t M, int32_t N, int32_t splitk);
 

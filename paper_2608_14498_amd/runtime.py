@@ -31,6 +31,15 @@ def stream_ptr(stream: Optional[torch.cuda.Stream] = None) -> int:
     return s.cuda_stream
 
 
+def prompt_positions(cu: Sequence[int], token_ids: np.ndarray) -> np.ndarray:
+    """Packed positions of every scorable prompt token: text tokens (id >= 0) that are
+    not the first token of their sequence (host int32)."""
+    ids = np.asarray(token_ids)
+    first = np.zeros(len(ids), bool)
+    first[np.asarray(cu[:-1], np.int64)] = True
+    return np.nonzero((ids >= 0) & ~first)[0].astype(np.int32)
+
+
 class DeviceModel:
     """Weights resident in HBM plus a model handle of the HIP library."""
 
@@ -125,6 +134,19 @@ class DeviceModel:
         rb.rp_suffix_logprob_grouped(self.handle, stream_ptr(stream), P, prefix_cu, S, prefix_of_suffix,
                                      suffix_cu, rope_pos0, flags, rb.make_kv(K, V, K[0].numel()), h_last,
                                      response_ids, logprobs, ws, ws.numel())
+        return logprobs
+
+    def prompt_logprobs(self, cu, token_ids, hidden, positions, logprobs=None, workspace=None, stream=None,
+                        flags: int = 0):
+        """Teacher-forced log-probs of the prompt tokens at packed positions (device int32),
+        scored from the prefix pass's hidden_out (device fp32 [T, d])."""
+        B, n = len(cu) - 1, int(positions.numel())
+        if logprobs is None:
+            logprobs = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)[:n]
+        nbytes = rb.rp_prompt_logprob_workspace_bytes(self.handle, n, flags)
+        ws = workspace if workspace is not None else self.workspace(nbytes)
+        rb.rp_prompt_logprob(self.handle, stream_ptr(stream), B, cu, token_ids, hidden, n, positions, flags,
+                             logprobs, ws, ws.numel())
         return logprobs
 
     def decode(self, cache_k, cache_v, kv_len, token_ids, logits=None, next_ids=None, workspace=None,

@@ -1,6 +1,7 @@
 """Write the oracle's expected values for the full-size parity tests.
 
     python tests/golden/make_fullsize.py WORKLOAD [WORKLOAD ...]
+    python tests/golden/make_fullsize.py --prompt WORKLOAD [WORKLOAD ...]
 
 For each named workload this runs the float64 CPU oracle (oracle/, nothing else
 computes) on one sequence of the seeded synthetic batch, at the workload's real
@@ -16,6 +17,14 @@ shapes, and stores sampled outputs in tests/golden/fullsize_<workload>.npz:
   dec_logits     [len(dec_rows), len(dec_vocab)] oracle logits at dec_vocab
   dec_argmax     [len(dec_rows)] oracle argmax over the whole vocabulary
   dec_top2       [len(dec_rows), 2] the two largest oracle logits of each row
+
+With --prompt it stores prompt-token log-probabilities instead, in
+tests/golden/fullsize_prompt_<workload>.npz:
+
+  seq              index of the sequence in the packed batch
+  prompt_pos       sampled text positions t >= 1 of that prompt (first and last
+                   text token + random)
+  prompt_logprobs  log p(token t | tokens < t) at prompt_pos
 
 Sequences are independent in a packed batch (the oracle has no cross-sequence
 term), so one sequence's oracle values are the expected values of that sequence
@@ -89,6 +98,34 @@ def make(name: str) -> str:
     return path
 
 
+def make_prompt(name: str) -> str:
+    t0 = time.time()
+    w = configs.get(name)
+    m = w.model
+    hw = inputs.make_weights(w)
+    bt = inputs.make_batch(w)
+    P, Vis, _ = inputs.draw_lengths(w)
+    b = pick_sequence(w, P)
+    cp = bt.cu_prefix
+    vo = int(sum(Vis[:b]))
+    ids = bt.token_ids[cp[b]:cp[b + 1]]
+    vis = inputs.to_f32(bt.visual[vo:vo + Vis[b]])
+    lp = oracle.prompt_logprob_one(hw.as_f32(), m, ids, vis)
+    text = np.nonzero(np.isfinite(lp))[0]
+    rng = np.random.default_rng([w.index, 902])
+    pick = rng.choice(text[1:-1], size=min(N_KV_SAMPLES - 2, max(len(text) - 2, 0)), replace=False)
+    pos = np.unique(np.concatenate([text[:1], text[-1:], pick])).astype(np.int64)
+    meta = dict(workload=name, seconds=round(time.time() - t0, 1), prefix=int(P[b]), text=int(len(text)))
+    path = os.path.join(HERE, f"fullsize_prompt_{name}.npz")
+    np.savez_compressed(path, meta=np.array(json.dumps(meta)), seq=np.int64(b), prompt_pos=pos,
+                        prompt_logprobs=lp[pos].astype(np.float64))
+    return path
+
+
 if __name__ == "__main__":
-    for n in sys.argv[1:]:
-        print(make(n), flush=True)
+    args = sys.argv[1:]
+    fn = make
+    if args and args[0] == "--prompt":
+        fn, args = make_prompt, args[1:]
+    for n in args:
+        print(fn(n), flush=True)

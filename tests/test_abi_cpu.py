@@ -209,6 +209,41 @@ def test_fused_scoring_workspace_holds_partials_not_logits(lib):
         rb.rp_destroy(h)
 
 
+def test_prompt_logprob_validation_and_workspace(lib):
+    h, keep = make(configs.QWEN7B_SLICE, max_pos=8192)
+    try:
+        V, d = configs.QWEN7B_SLICE.vocab, configs.QWEN7B_SLICE.d_model
+        plain = rb.rp_prompt_logprob_workspace_bytes(h, 1024)
+        fused = rb.rp_prompt_logprob_workspace_bytes(h, 1024, rb.RP_SUFFIX_FUSED_LOGPROB)
+        assert plain >= 1024 * (V * 4 + d * 2 + 4)
+        assert fused < 1024 * (d * 2 + 4 + 8 * 2 * ((V + 255) // 256) + 4) + 4096
+        assert rb.rp_prompt_logprob_workspace_bytes(h, 0) <= 4096
+        assert status_of(rb.rp_prompt_logprob_workspace_bytes, h, -1)[0] == rb.RP_ERR_SHAPE
+        assert status_of(rb.rp_prompt_logprob_workspace_bytes, h, 4, 2)[0] == rb.RP_ERR_INVALID_ARG
+        need = rb.rp_prompt_logprob_workspace_bytes(h, 8)
+        args = [h, None, 2, [0, 100, 300], FAKE, FAKE + (1 << 31), 8, FAKE + (1 << 32), 0, FAKE + (1 << 33),
+                FAKE + (1 << 34), need]
+        for i, st in ((4, rb.RP_ERR_INVALID_ARG), (5, rb.RP_ERR_INVALID_ARG), (7, rb.RP_ERR_INVALID_ARG),
+                      (9, rb.RP_ERR_INVALID_ARG)):
+            bad = list(args)
+            bad[i] = None
+            assert status_of(rb.rp_prompt_logprob, *bad)[0] == st, i
+        bad = list(args); bad[11] = need - 1
+        assert status_of(rb.rp_prompt_logprob, *bad)[0] == rb.RP_ERR_WORKSPACE
+        bad = list(args); bad[5] = FAKE + 4                       # misaligned hidden
+        assert status_of(rb.rp_prompt_logprob, *bad)[0] == rb.RP_ERR_INVALID_ARG
+        bad = list(args); bad[6] = -3
+        assert status_of(rb.rp_prompt_logprob, *bad)[0] == rb.RP_ERR_SHAPE
+        bad = list(args); bad[3] = [0, 100, 100]                  # an empty prompt
+        assert status_of(rb.rp_prompt_logprob, *bad)[0] == rb.RP_ERR_SHAPE
+        bad = list(args); bad[8] = 4
+        assert status_of(rb.rp_prompt_logprob, *bad)[0] == rb.RP_ERR_INVALID_ARG
+        # no rows: nothing is launched and no pointer is needed
+        rb.rp_prompt_logprob(h, None, 2, [0, 100, 300], None, None, 0, None, 0, None, FAKE, 4096)
+    finally:
+        rb.rp_destroy(h)
+
+
 def _prefix_args(h, T=64, ws_bytes=None, stride=None, tokens=FAKE, ws=FAKE + (1 << 30)):
     m = configs.TINY
     kv = rb.make_kv(FAKE + (1 << 32), FAKE + (1 << 33),

@@ -109,3 +109,47 @@ def test_fullsize_matches_oracle(name, dtype):
         assert res["fused_vs_plain"] <= 1e-4
     if "decode_logits" in res:
         assert res["decode_logits"] <= tol and res["decode_argmax_ok"]
+
+
+PROMPT_NAMES = ["qwen7b_b4_p4096_s256", "qwen7b_ragged_b8"]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("name", PROMPT_NAMES)
+def test_fullsize_prompt_logprobs_match_oracle(name, dtype):
+    """Prompt-token log-probs of every text token of the packed batch (the launch the
+    benchmark times), plain and fused scoring, checked at the stored sampled positions."""
+    from paper_2608_14498_amd.runtime import prompt_positions
+
+    path = os.path.join(GOLDEN, f"fullsize_prompt_{name}.npz")
+    if not os.path.exists(path):
+        pytest.skip(f"no stored oracle values (run tests/golden/make_fullsize.py --prompt {name})")
+    g = np.load(path, allow_pickle=False)
+    w = configs.with_model(configs.get(name), dtype=dtype)
+    m = w.model
+    hw = inputs.make_weights(w)
+    bt = inputs.make_batch(w)
+    dm = DeviceModel(hw, max(bt.prefix_lens) + 1)
+    dev = dm.device
+    cu_p = [int(x) for x in bt.cu_prefix]
+    ids = to_device(bt.token_ids, dev)
+    hidden = torch.empty((cu_p[-1], m.d_model), dtype=torch.float32, device=dev)
+    dm.prefix(cu_p, ids, to_device(bt.visual, dev), hidden_out=hidden)
+    pos = prompt_positions(cu_p, bt.token_ids)
+    print(f"[fullsize] {name} {dtype}: prompt rows {len(pos)}", flush=True)
+    pos_d = to_device(pos, dev)
+    lp = dm.prompt_logprobs(cu_p, ids, hidden, pos_d)
+    lpf = dm.prompt_logprobs(cu_p, ids, hidden, pos_d, flags=rb.RP_SUFFIX_FUSED_LOGPROB)
+    torch.cuda.synchronize()
+    want = cu_p[int(g["seq"])] + g["prompt_pos"]
+    idx = np.searchsorted(pos, want)
+    assert np.array_equal(pos[idx], want)
+    got, gotf = lp.cpu().numpy(), lpf.cpu().numpy()
+    res = dict(prompt=float(np.max(np.abs(got[idx] - g["prompt_logprobs"]))),
+               prompt_fused=float(np.max(np.abs(gotf[idx] - g["prompt_logprobs"]))),
+               fused_vs_plain=float(np.max(np.abs(gotf - got))), finite=bool(np.all(np.isfinite(got))))
+    dm.close()
+    print(f"[fullsize] {name} {dtype}: {json.dumps(res)}", flush=True)
+    assert res["finite"]
+    assert res["prompt"] <= LP_TOL[dtype] and res["prompt_fused"] <= LP_TOL[dtype]
+    assert res["fused_vs_plain"] <= 1e-4

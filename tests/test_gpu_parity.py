@@ -250,3 +250,44 @@ def test_mrope_prefix_and_suffix_match_oracle(model, sections):
     assert errs["lp"] <= (1e-4 if f32 else 2e-2)
     assert errs["k"] <= (1e-5 if f32 else 3e-2)
     dm.close()
+
+
+@pytest.mark.parametrize("model,flags", [(configs.TINY, 0), (BF16_D64, 0), (BF16_D64, 1), (F16_SMALL, 1)])
+def test_prompt_logprobs_match_oracle(model, flags):
+    """Prompt-token log-probs from the prefix pass's hidden states: every text position of
+    ragged prompts laid out text, visual, text (one all-visual), repeated and shuffled, plus
+    positions that score nothing (first tokens, visual slots, out of range: NaN)."""
+    from paper_2608_14498_amd.runtime import DeviceModel, prompt_positions, to_device
+    P, Vis = [1, 70, 300, 129, 40], [0, 60, 256, 100, 40]
+    w = configs.custom(model, P, Vis, [0] * len(P), index=83)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    cp = [int(x) for x in bt.cu_prefix]
+    T = cp[-1]
+    ids = bt.token_ids.copy()
+    for b in range(len(P)):
+        seg = ids[cp[b]:cp[b + 1]]
+        text = seg[seg >= 0]
+        a = len(text) // 3
+        ids[cp[b]:cp[b + 1]] = np.concatenate([text[:a], np.full(Vis[b], -1, np.int32), text[a:]])
+    good = prompt_positions(cp, ids)
+    bad = np.array([0, cp[1], cp[2], cp[1] + 5, cp[4] + 7, T, -1, T + 9], np.int32)
+    pos = np.concatenate([good, bad, good[:7]]).astype(np.int32)
+    np.random.default_rng(5).shuffle(pos)
+    dm = DeviceModel(hw, max(P) + 1)
+    dev = dm.device
+    ids_d = to_device(ids, dev)
+    hidden = torch.empty((T, model.d_model), dtype=torch.float32, device=dev)
+    dm.prefix(cp, ids_d, to_device(bt.visual, dev), hidden_out=hidden)
+    lp = dm.prompt_logprobs(cp, ids_d, hidden, to_device(pos, dev), flags=flags)
+    torch.cuda.synchronize()
+    got = lp.cpu().numpy()
+    full = oracle.prompt_logprob(hw.as_f32(), model, cp, ids, inputs.to_f32(bt.visual))
+    exp = np.array([full[t] if 0 <= t < T else np.nan for t in pos])
+    assert np.array_equal(np.isnan(got), np.isnan(exp))
+    assert np.isfinite(exp).sum() == len(good) + 7
+    err = max_abs(got, exp)
+    print(f"[parity] prompt log-probs {model.dtype} V={model.vocab} flags={flags}: rows {len(pos)} "
+          f"|d lp| {err:.3g}", flush=True)
+    assert err <= (1e-4 if model.dtype == "f32" else 2e-2)
+    dm.close()
