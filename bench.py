@@ -233,6 +233,8 @@ def main():
                     help="skip timing the fp16 variant of a bf16 workload")
     ap.add_argument("--no-fused-variant", action="store_true",
                     help="skip timing the suffix with the fused lm_head + log-sum-exp scoring")
+    ap.add_argument("--no-transposed-variant", action="store_true",
+                    help="skip timing the step with o_proj / down weights stored transposed")
     ap.add_argument("--no-prompt-logprobs", action="store_true",
                     help="skip timing the prompt-token log-probs (rp_prompt_logprob)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -262,7 +264,7 @@ def main():
     if w.decode is not None:
         return colocation(args, w)
     m = w.model
-    res = run_passes(w, args, profile=True)
+    res = run_passes(w, args, profile=True, prompt=True)
     T, R, B, kernels = res["T"], res["R"], res["B"], res["kernels"]
     ms_step, pre_ms, suf_ms = res["ms_step"], res["pre_ms"], res["suf_ms"]
     bt = res["bt"]
@@ -344,14 +346,27 @@ def main():
             "value": (rfu["T"] + rfu["R"]) / (rfu["ms_step"] * 1e-3), "unit": "tokens/s",
             "ms_per_step": rfu["ms_step"], "suffix_ms": rfu["suf_ms"],
             "suffix_tokens_per_s": rfu["R"] / (rfu["suf_ms"] * 1e-3)}
+    if m.dtype != "f32" and not args.no_transposed_variant:
+        # the row-parallel projections (o_proj, down) stored transposed and read in
+        # transpose mode (Case 2 weight sharing), same results bit for bit
+        from paper_2608_14498_amd import binding as rb
+
+        rt = run_passes(w, args, profile=True, weight_layout=rb.RP_WO_TRANSPOSED | rb.RP_W_DOWN_TRANSPOSED)
+        kt = rt["kernels"]
+        out["transposed_weights_variant"] = {
+            "value": (rt["T"] + rt["R"]) / (rt["ms_step"] * 1e-3), "unit": "tokens/s",
+            "ms_per_step": rt["ms_step"], "prefix_ms": rt["pre_ms"], "suffix_ms": rt["suf_ms"],
+            "kernels": {k: kt[k] for k in ("prefix.gemm_o_proj", "prefix.gemm_down", "suffix.gemm_o_proj",
+                                           "suffix.gemm_down") if k in kt}}
     if not args.no_cpu_baseline:
         log("CPU baseline: oracle on sequence 0")
         out["cpu_baseline"] = cpu_baseline(w, res["hw"], bt, args.cpu_prefix_len)
     print(json.dumps(out), flush=True)
 
 
-def run_passes(w, args, profile: bool, flags: int = 0):
-    """Time prefix + suffix steps of workload w; optionally per-kernel durations."""
+def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, prompt: bool = False):
+    """Time prefix + suffix steps of workload w; optionally per-kernel durations and the
+    prompt-token log-probs."""
     import numpy as np
     import torch
 
@@ -368,7 +383,7 @@ def run_passes(w, args, profile: bool, flags: int = 0):
     grp = bt.prefix_of_suffix
     pre_of_suf = bt.prefix_lens if grp is None else [bt.prefix_lens[g] for g in grp]
     maxp = max(p + s for p, s in zip(pre_of_suf, bt.suffix_lens)) + 1
-    dm = DeviceModel(hw, maxp)
+    dm = DeviceModel(hw, maxp, weight_layout=weight_layout)
     dev = dm.device
     ids = to_device(bt.token_ids, dev)
     vis = to_device(bt.visual, dev) if bt.visual.shape[0] else None
@@ -439,7 +454,7 @@ def run_passes(w, args, profile: bool, flags: int = 0):
         kernels = {k: {"launches": n, "avg_ms": ms / max(n, 1), "ms_per_step": ms / args.profile_steps}
                    for k, (n, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1])}
     prompt = None
-    if profile and not args.no_prompt_logprobs:
+    if prompt and not args.no_prompt_logprobs:
         prompt = time_prompt_logprobs(dm, args, bt, cu_p, ids, vis, (K, V), h_last, ws_p, stream)
     dm.close()
     del K, V, ids, vis, resp, ws_p, ws_s

@@ -75,17 +75,29 @@ typedef enum { RP_F32 = 0, RP_BF16 = 1, RP_F16 = 2 } rp_dtype;
  * multiples of 64.
  * rms_eps is the RMSNorm epsilon (1e-6 for the Qwen2 family); rope_theta the
  * RoPE base (1e6).  max_position bounds every position a call may use. */
+/* Storage of the row-parallel projections (Section "Parallelism-Aware Weight
+ * Sharing", Case 2: a logical [O, I] weight sharded along I is kept as [I, O],
+ * so that every tensor-parallel shard of it is one contiguous range shared by
+ * the training and rollout engines; the GEMMs read it in transpose mode and no
+ * copy in the logical orientation is made).  Bits of rp_config.weight_layout;
+ * others are RP_ERR_INVALID_ARG. */
+#define RP_WO_TRANSPOSED 1u     /* wo stored [n_q_heads*head_dim][d_model] */
+#define RP_W_DOWN_TRANSPOSED 2u /* w_down stored [ffn_dim][d_model] */
+#define RP_WEIGHT_LAYOUTS 3u    /* all defined bits */
+
 typedef struct {
   int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab, max_position;
   float rms_eps;
   double rope_theta;
   rp_dtype dtype;
+  uint32_t weight_layout; /* RP_*_TRANSPOSED bits; 0 = nn.Linear layout throughout */
 } rp_config;
 
 /* One decoder layer, device pointers, nn.Linear layout [out, in]:
  * wq [Hq*Dh, d], wk/wv [Hkv*Dh, d], wo [d, Hq*Dh], w_gate/w_up [F, d],
  * w_down [d, F]; attn_norm/mlp_norm [d]; biases bq [Hq*Dh], bk/bv [Hkv*Dh]
- * are optional (NULL = none). */
+ * are optional (NULL = none).  wo and w_down are stored transposed when
+ * rp_config.weight_layout says so. */
 typedef struct {
   const void *attn_norm, *wq, *wk, *wv, *bq, *bk, *bv, *wo;
   const void *mlp_norm, *w_gate, *w_up, *w_down;

@@ -21,6 +21,7 @@ RP_F32, RP_BF16, RP_F16 = 0, 1, 2
 _DTYPES = {"f32": RP_F32, "bf16": RP_BF16, "f16": RP_F16}
 RP_MAX_SEQS = 256
 RP_SUFFIX_FUSED_LOGPROB = 1
+RP_WO_TRANSPOSED, RP_W_DOWN_TRANSPOSED = 1, 2
 SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_forward", "rp_prefix_forward_mrope",
            "rp_suffix_workspace_bytes", "rp_suffix_logprob", "rp_suffix_grouped_workspace_bytes",
            "rp_suffix_logprob_grouped", "rp_prompt_logprob_workspace_bytes", "rp_prompt_logprob",
@@ -41,7 +42,7 @@ class RpConfig(Structure):
     _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_q_heads", c_int32),
                 ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
                 ("vocab", c_int32), ("max_position", c_int32), ("rms_eps", c_float),
-                ("rope_theta", c_double), ("dtype", c_int)]
+                ("rope_theta", c_double), ("dtype", c_int), ("weight_layout", c_uint32)]
 
 
 class RpLayerWeights(Structure):
@@ -140,10 +141,10 @@ def _i32(seq: Optional[Sequence[int]]):
     return (c_int32 * len(vals))(*vals)
 
 
-def make_config(model, max_position: int) -> RpConfig:
+def make_config(model, max_position: int, weight_layout: int = 0) -> RpConfig:
     return RpConfig(model.n_layers, model.d_model, model.n_q_heads, model.n_kv_heads, model.head_dim,
                     model.ffn_dim, model.vocab, int(max_position), float(model.rms_eps),
-                    float(model.rope_theta), _DTYPES[model.dtype])
+                    float(model.rope_theta), _DTYPES[model.dtype], int(weight_layout))
 
 
 def make_kv(k, v, layer_stride: int) -> RpKV:

@@ -127,6 +127,8 @@ rp_status check_config(const rp_config* c) {
   if (!c) return fail(RP_ERR_INVALID_ARG, "config is NULL");
   if (c->dtype != RP_F32 && c->dtype != RP_BF16 && c->dtype != RP_F16)
     return fail(RP_ERR_INVALID_ARG, "bad dtype %d", (int)c->dtype);
+  if (c->weight_layout & ~RP_WEIGHT_LAYOUTS)
+    return fail(RP_ERR_INVALID_ARG, "unknown weight_layout bits 0x%x", c->weight_layout);
   if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn_dim < 1 ||
       c->vocab < 1 || c->max_position < 1)
     return fail(RP_ERR_SHAPE, "config sizes must be positive");
@@ -400,6 +402,14 @@ const LayerNames kSuffixNames = {"suffix.rmsnorm", "suffix.gemm_qkv", "suffix.ro
                                  "suffix.gemm_o_proj", "suffix.rmsnorm", "suffix.gemm_gate_up", "suffix.swiglu",
                                  "suffix.gemm_down"};
 
+// B operands of the row-parallel projections in their stored layout (weight_layout).
+rp::BSeg wo_operand(const rp_config& c, const rp_layer_weights& lw) {
+  return rp::BSeg{lw.wo, lw.wo, lw.wo, c.d_model, c.d_model, (c.weight_layout & RP_WO_TRANSPOSED) != 0};
+}
+rp::BSeg w_down_operand(const rp_config& c, const rp_layer_weights& lw) {
+  return rp::BSeg{lw.w_down, lw.w_down, lw.w_down, c.d_model, c.d_model, (c.weight_layout & RP_W_DOWN_TRANSPOSED) != 0};
+}
+
 rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, const rp::SeqTable& st,
                     int32_t M, const LayerWS& w, void* k_out, void* v_out, const void* k0, const void* v0,
                     const LayerPlan& plan, float* gemm_part, const LayerNames& nm,
@@ -426,8 +436,9 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   a.D = D;
   a.scale = (float)(1.0 / sqrt((double)D));
   RP_TRY_LAUNCH_N(nm.attn, rp::launch_attention(s, dt, st, a, M));
-  rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
-  RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, dt, M, d, hq, w.O, hq, bo, hq, w.X, d, rp::EPI_ADD_F32, plan.o, gemm_part));
+  const rp::BSeg bo = wo_operand(c, lw);
+  RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, dt, M, d, hq, w.O, hq, bo, bo.trans ? d : hq, w.X, d, rp::EPI_ADD_F32,
+                                            plan.o, gemm_part));
   RP_TRY_LAUNCH_N(nm.norm2, rp::launch_rmsnorm(s, dt, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
   if (plan.fused) {
@@ -437,8 +448,9 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
                                                 plan.gu, gemm_part));
     RP_TRY_LAUNCH_N(nm.swiglu, rp::launch_swiglu(s, dt, w.GU, M, F, w.ACT));
   }
-  rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
-  RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, dt, M, d, F, w.ACT, F, bd, F, w.X, d, rp::EPI_ADD_F32, plan.down, gemm_part));
+  const rp::BSeg bd = w_down_operand(c, lw);
+  RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, dt, M, d, F, w.ACT, F, bd, bd.trans ? d : F, w.X, d, rp::EPI_ADD_F32,
+                                           plan.down, gemm_part));
   return RP_OK;
 }
 
@@ -738,17 +750,17 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
                                             c.max_position, w.L.Q, kl, vl));
     RP_TRY_LAUNCH_N("decode.attention", rp::launch_decode_attention(s, dt, w.L.Q, hq, kl, vl, kv_len, cap, c.max_position, B, Hq, Hkv,
                                               D, scale, w.attn_part, w.L.O));
-    rp::BSeg bo = {lw.wo, lw.wo, lw.wo, d, d};
-    RP_TRY_LAUNCH_N("decode.gemm_o_proj", rp::launch_gemm(s, dt, B, d, hq, w.L.O, hq, bo, hq, w.L.X, d, rp::EPI_ADD_F32,
-                                  decode_splitk(c, B, d, hq), w.gemm_part));
+    const rp::BSeg bo = wo_operand(c, lw);
+    RP_TRY_LAUNCH_N("decode.gemm_o_proj", rp::launch_gemm(s, dt, B, d, hq, w.L.O, hq, bo, bo.trans ? d : hq, w.L.X, d,
+                                                          rp::EPI_ADD_F32, decode_splitk(c, B, d, hq), w.gemm_part));
     RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, dt, w.L.X, lw.mlp_norm, c.rms_eps, B, d, w.L.N));
     rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
     RP_TRY_LAUNCH_N("decode.gemm_gate_up", rp::launch_gemm(s, dt, B, 2 * F, d, w.L.N, d, bgu, d, w.L.GU, 2 * F, rp::EPI_STORE,
                                   decode_splitk(c, B, 2 * F, d), w.gemm_part));
     RP_TRY_LAUNCH_N("decode.swiglu", rp::launch_swiglu(s, dt, w.L.GU, B, F, w.L.ACT));
-    rp::BSeg bd = {lw.w_down, lw.w_down, lw.w_down, d, d};
-    RP_TRY_LAUNCH_N("decode.gemm_down", rp::launch_gemm(s, dt, B, d, F, w.L.ACT, F, bd, F, w.L.X, d, rp::EPI_ADD_F32,
-                                  decode_splitk(c, B, d, F), w.gemm_part));
+    const rp::BSeg bd = w_down_operand(c, lw);
+    RP_TRY_LAUNCH_N("decode.gemm_down", rp::launch_gemm(s, dt, B, d, F, w.L.ACT, F, bd, bd.trans ? d : F, w.L.X, d,
+                                                        rp::EPI_ADD_F32, decode_splitk(c, B, d, F), w.gemm_part));
   }
   RP_TRY_LAUNCH_N("decode.final_norm", rp::launch_rmsnorm(s, dt, w.L.X, m->final_norm, c.rms_eps, B, d, w.L.N));
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};

@@ -116,8 +116,6 @@ __device__ __forceinline__ void fa_block(const FaMap& m, int bid, int Hq, int* q
 
 constexpr float kMaskVal = -1e30f;
 constexpr float kLazy = 8.f;  // log2 headroom of the lazily updated softmax max
-typedef short v4i16_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 

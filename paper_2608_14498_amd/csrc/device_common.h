@@ -13,6 +13,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;  // LDS operand of ds_read_b64_tr_b16
 
 // Host-side dispatch on the storage type of a model: calls f(T()) with T = float,
 // bf16_t or f16_t for RP_F32, RP_BF16 and RP_F16.

@@ -66,6 +66,38 @@ __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 constexpr int GB_M = 256, GB_N = 256, GB_K = 64;
 
+// Transposed B (BSeg::trans): the slab is staged as stored, [64 k][256 n] with 32
+// 16-byte chunks per k row, and physical chunk = logical chunk ^ swzt(k).  One
+// transposed fragment read covers 4 consecutive k rows x 4 consecutive chunks per half
+// wave; the XOR gives those 16 (row, chunk) pairs distinct bank groups with 32 or with
+// 64 banks (bits 1-2 and bits 2-3 of the chunk index both differ across the 4 rows).
+__device__ __forceinline__ int swzt(int k) { return (k & 3) * 5; }
+
+// Per-lane element offsets (within a transposed slab) of the B fragments j = 0..NJ-1 at
+// k-step 0; k-step ks adds ks*16 rows and the second read 4 rows (same swizzle: k % 4 is
+// unchanged).  Lane l = 16g + p addresses k row 8(g/2) + p/4 at column
+// n0 + 16(g%2) + 4(p%4), so that ds_read_b64_tr_b16 hands it k = 8(l/32) + 0..3 (then
+// + 4..7 from the second read) of column n0 + l%32: the MFMA operand layout, the same k
+// order as the A fragment.
+template <int NJ>
+__device__ __forceinline__ void bt_offsets(int lane, int n_wave, int (&off)[NJ]) {
+  const int g = lane >> 4, p = lane & 15;
+  const int kr = 8 * (g >> 1) + (p >> 2);
+  const int nb = n_wave + 16 * (g & 1) + 4 * (p & 3);
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) off[j] = kr * GB_N + ((((nb >> 3) + 4 * j) ^ swzt(kr)) << 3) + (nb & 7);
+}
+
+// B fragment from a transposed LDS slab at element offset off (see bt_offsets).
+template <typename T16>
+__device__ __forceinline__ typename Half16<T16>::V8 bt_frag(const void* slab, int off) {
+  const T16* p = reinterpret_cast<const T16*>(slab) + off;
+  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p);
+  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(p + 4 * GB_N));
+  const uint2 l = __builtin_bit_cast(uint2, lo), h = __builtin_bit_cast(uint2, hi);
+  return Half16<T16>::as_v8(make_uint4(l.x, l.y, h.x, h.y));
+}
+
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + expf(-g)) * u; }
 
 // Four consecutive outputs n0..n0+3 of one row: one 8-byte (bf16) or 16-byte (fp32)
@@ -348,7 +380,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&
 // ------------------------------------------------------------------------------------
 // bf16 MFMA GEMM
 // ------------------------------------------------------------------------------------
-template <int EPI, typename T16, int WGM>
+template <int EPI, typename T16, int WGM, bool BT = false>
 __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
   typedef typename Half16<T16>::V8 V8;
   constexpr int NT = WGM * 2 * 64;
@@ -387,19 +419,31 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
   }
 #define G_LDB(i_, kt_)                                                                                 \
   if (i_ < LOADS) {                                                                                    \
-    const int r_ = lr + (NT / 8) * i_;                                                                 \
-    rb##i_ = *reinterpret_cast<const uint4*>(brow<T16>(g.B, b_logical(r_), g.ldb) + kbeg + lc * 8 + \
-                                             (kt_) * GB_K);                                            \
+    if (BT) {                                                                                          \
+      const int kr_ = (tid >> 5) + (NT / 32) * i_;                                                     \
+      rb##i_ = *reinterpret_cast<const uint4*>((const T16*)g.B.b0 +                                    \
+                                               (int64_t)(kbeg + (kt_) * GB_K + kr_) * g.ldb +          \
+                                               min(tn * GB_N + (tid & 31) * 8, g.N - 8));              \
+    } else {                                                                                           \
+      const int r_ = lr + (NT / 8) * i_;                                                               \
+      rb##i_ = *reinterpret_cast<const uint4*>(brow<T16>(g.B, b_logical(r_), g.ldb) + kbeg + lc * 8 + \
+                                               (kt_) * GB_K);                                          \
+    }                                                                                                  \
   }
 #define G_STA(i_, buf_)                                    \
   if (i_ < LOADS) {                                        \
     const int r_ = lr + (NT / 8) * i_;                     \
     As[(buf_)][r_ * 8 + (lc ^ swz(r_))] = ra##i_;          \
   }
-#define G_STB(i_, buf_)                                    \
-  if (i_ < LOADS) {                                        \
-    const int r_ = lr + (NT / 8) * i_;                     \
-    Bs[(buf_)][r_ * 8 + (lc ^ swz(r_))] = rb##i_;          \
+#define G_STB(i_, buf_)                                             \
+  if (i_ < LOADS) {                                                 \
+    if (BT) {                                                       \
+      const int kr_ = (tid >> 5) + (NT / 32) * i_;                  \
+      Bs[(buf_)][kr_ * 32 + ((tid & 31) ^ swzt(kr_))] = rb##i_;     \
+    } else {                                                        \
+      const int r_ = lr + (NT / 8) * i_;                            \
+      Bs[(buf_)][r_ * 8 + (lc ^ swz(r_))] = rb##i_;                 \
+    }                                                               \
   }
 #define G_LOAD_A(kt_) G_LDA(0, kt_) G_LDA(1, kt_) G_LDA(2, kt_) G_LDA(3, kt_) G_LDA(4, kt_) G_LDA(5, kt_) G_LDA(6, kt_) G_LDA(7, kt_)
 #define G_LOAD_B(kt_) G_LDB(0, kt_) G_LDB(1, kt_) G_LDB(2, kt_) G_LDB(3, kt_) G_LDB(4, kt_) G_LDB(5, kt_) G_LDB(6, kt_) G_LDB(7, kt_)
@@ -411,8 +455,12 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
     AF[i] = Half16<T16>::as_v8(As[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
   }                                                                            \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j) {                             \
-    const int r_ = wn * TN + j * 32 + fr;                                      \
-    BF[j] = Half16<T16>::as_v8(Bs[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+    if (BT) {                                                                  \
+      BF[j] = bt_frag<T16>(&Bs[buf][0], btoff[j] + (ks_) * 16 * GB_N);         \
+    } else {                                                                   \
+      const int r_ = wn * TN + j * 32 + fr;                                    \
+      BF[j] = Half16<T16>::as_v8(Bs[buf][r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+    }                                                                          \
   }
 #define G_MMA(AF, BF)                                                           \
   _Pragma("unroll") for (int i = 0; i < MI; ++i)                                \
@@ -442,6 +490,8 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
   __syncthreads();
 
   const int fr = lane & 31, fk = lane >> 5;
+  int btoff[NJ];
+  if (BT) bt_offsets<NJ>(lane, wn * TN, btoff);
   for (int kt = 0; kt < KT; ++kt) {
     const int buf = kt & 1;
     const int ktn = kt + 1 < KT ? kt + 1 : kt;  // the last tile re-loads itself into the idle buffer
@@ -501,7 +551,7 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 // chunk each lane fetches.  The two LDS buffers are separate arrays and the k loop is
 // unrolled by two, so every LDS access names its buffer at compile time.
 // ------------------------------------------------------------------------------------
-template <int EPI, typename T16, int WGM>
+template <int EPI, typename T16, int WGM, bool BT = false>
 __global__ __launch_bounds__(WGM * 128) __attribute__((amdgpu_waves_per_eu(WGM == 2 ? 1 : 2, WGM == 2 ? 1 : 2)))
 void k_gemm_bf16_dma(GemmArgs g) {
 #if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
@@ -510,6 +560,7 @@ void k_gemm_bf16_dma(GemmArgs g) {
   constexpr int MI = TM / 32, NJ = TN / 32;
   constexpr int LOADS = (GB_M * 8) / NT;  // load instructions per matrix per wave: 4
   constexpr int MM = MI * NJ;
+  constexpr int NREAD = MI + (BT ? 2 : 1) * NJ;  // LDS fragment reads per k-step
   typedef __attribute__((address_space(3))) void lds_void;
   typedef typename Half16<T16>::V8 V8;
   // native vector element type: each fragment read is one 16-byte LDS load in the IR
@@ -552,21 +603,32 @@ void k_gemm_bf16_dma(GemmArgs g) {
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) {
     const int r0 = wave * 8 * LOADS + 8 * i;  // first row of the block (wave-uniform)
-    const int br0 = b_logical(r0);
-    const int seg = br0 < g.B.n1 ? 0 : br0 < g.B.n2 ? 1 : 2;
-    rsB[i] = seg == 0 ? rsB0 : seg == 1 ? rsB1 : rsB2;
-    const int sbeg = seg == 0 ? 0 : seg == 1 ? g.B.n1 : g.B.n2;
     const int r = r0 + (lane >> 3);
     const int c = (lane & 7) ^ swz(r);
     aoff[i] = 2u * ((uint32_t)min(m0 + r, g.M - 1) * (uint32_t)g.lda + (uint32_t)(kbeg + c * 8));
-    boff[i] = 2u * ((uint32_t)(b_logical(r) - sbeg) * (uint32_t)g.ldb + (uint32_t)(kbeg + c * 8));
+    if (BT) {
+      // the same 64 LDS chunks hold k rows 2(wave*LOADS + i) and +1 of the transposed slab;
+      // columns past N (N % 8 == 0) re-read the last chunk, and their results are dropped
+      const int kr = 2 * (wave * LOADS + i) + (lane >> 5);
+      const int cb = (lane & 31) ^ swzt(kr);
+      rsB[i] = rsB0;
+      boff[i] = 2u * ((uint32_t)(kbeg + kr) * (uint32_t)g.ldb + (uint32_t)min(tn * GB_N + cb * 8, g.N - 8));
+    } else {
+      const int br0 = b_logical(r0);
+      const int seg = br0 < g.B.n1 ? 0 : br0 < g.B.n2 ? 1 : 2;
+      rsB[i] = seg == 0 ? rsB0 : seg == 1 ? rsB1 : rsB2;
+      const int sbeg = seg == 0 ? 0 : seg == 1 ? g.B.n1 : g.B.n2;
+      boff[i] = 2u * ((uint32_t)(b_logical(r) - sbeg) * (uint32_t)g.ldb + (uint32_t)(kbeg + c * 8));
+    }
   }
+  // byte step of B per slab: 64 elements along a row, or 64 rows of the transposed layout
+  const uint32_t bstep = BT ? (uint32_t)GB_K * 2u * (uint32_t)g.ldb : (uint32_t)GB_K * 2u;
 #define D_LOAD(DA, DB, kt_)                                                                            \
   _Pragma("unroll") for (int i = 0; i < LOADS; ++i) {                                                 \
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)(DA + (wave * LOADS + i) * 64), 16, aoff[i], \
                                              (kt_) * (GB_K * 2), 0, 0);                                \
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB[i], (lds_void*)(DB + (wave * LOADS + i) * 64), 16, boff[i], \
-                                             (kt_) * (GB_K * 2), 0, 0);                                \
+                                             (int)((uint32_t)(kt_) * bstep), 0, 0);                   \
   }
 #define D_FRAGS(AF, BF, SA, SB, ks_)                                          \
   _Pragma("unroll") for (int i = 0; i < MI; ++i) {                            \
@@ -574,8 +636,12 @@ void k_gemm_bf16_dma(GemmArgs g) {
     AF[i] = __builtin_bit_cast(V8, SA[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
   }                                                                           \
   _Pragma("unroll") for (int j = 0; j < NJ; ++j) {                            \
-    const int r_ = wn * TN + j * 32 + fr;                                     \
-    BF[j] = __builtin_bit_cast(V8, SB[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+    if (BT) {                                                                 \
+      BF[j] = bt_frag<T16>(SB, btoff[j] + (ks_) * 16 * GB_N);                 \
+    } else {                                                                  \
+      const int r_ = wn * TN + j * 32 + fr;                                   \
+      BF[j] = __builtin_bit_cast(V8, SB[r_ * 8 + (((ks_) * 2 + fk) ^ swz(r_))]); \
+    }                                                                         \
   }
 #define D_MMA(AF, BF)                                                         \
   _Pragma("unroll") for (int i = 0; i < MI; ++i)                              \
@@ -589,7 +655,7 @@ void k_gemm_bf16_dma(GemmArgs g) {
   // copies have a whole slab of MFMA time to land and each CU keeps L2 misses in flight
   // without a gap (the misses' fabric bandwidth, not the MFMAs, bounds the large GEMMs).
 #define D_REGION(n_mem_, mem_mask_)                                                        \
-  __builtin_amdgcn_sched_group_barrier(0x100, MI + NJ, 0);                                 \
+  __builtin_amdgcn_sched_group_barrier(0x100, NREAD, 0);                                   \
   _Pragma("unroll") for (int q = 0; q < MM; ++q) {                                         \
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                     \
     if (q < (n_mem_)) __builtin_amdgcn_sched_group_barrier((mem_mask_), 1, 0);             \
@@ -625,6 +691,8 @@ void k_gemm_bf16_dma(GemmArgs g) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
   const int fr = lane & 31, fk = lane >> 5;
+  int btoff[NJ];
+  if (BT) bt_offsets<NJ>(lane, wn * TN, btoff);
   V8 af0[MI], bf0[NJ], af1[MI], bf1[NJ];
   if (KT > 0) {
     D_LOAD(As0, Bs0, 0);
@@ -660,7 +728,7 @@ void k_gemm_bf16_dma(GemmArgs g) {
 // ------------------------------------------------------------------------------------
 constexpr int GF_M = 64, GF_N = 64, GF_K = 16;
 
-template <int EPI>
+template <int EPI, bool BT = false>
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs g) {
   __shared__ float As[GF_K][GF_M + 1];
   __shared__ float Bs[GF_K][GF_N + 1];
@@ -677,9 +745,15 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs g) {
     for (int i = 0; i < 4; ++i) {
       const int idx = tid + 256 * i;
       const int r = idx >> 4, kk = idx & 15;
-      const int m = m0 + r, n = n0 + r, k = k0 + kk;
+      const int m = m0 + r, k = k0 + kk;
       As[kk][r] = (m < g.M && k < kend) ? A[(int64_t)m * g.lda + k] : 0.f;
-      Bs[kk][r] = (n < g.N && k < kend) ? brow<float>(g.B, n, g.ldb)[k] : 0.f;
+      if (BT) {  // consecutive threads read consecutive columns of a stored [K][N] row
+        const int rn = idx & 63, kn = idx >> 6, n = n0 + rn, k2 = k0 + kn;
+        Bs[kn][rn] = (n < g.N && k2 < kend) ? ((const float*)g.B.b0)[(int64_t)k2 * g.ldb + n] : 0.f;
+      } else {
+        const int n = n0 + r;
+        Bs[kk][r] = (n < g.N && k < kend) ? brow<float>(g.B, n, g.ldb)[k] : 0.f;
+      }
     }
     __syncthreads();
 #pragma unroll
@@ -753,6 +827,8 @@ static bool dma_setup(const GemmArgs& g, int64_t b_rows, bool swiglu) {
   if (g.M <= 0 || g.K <= 0) return false;
   const uint64_t a_ext = ((uint64_t)(g.M - 1) * (uint64_t)g.lda + (uint64_t)g.K) * 2u;
   if (a_ext > kLim) return false;
+  if (g.B.trans)  // one stored [K][N] matrix; the slab step is a signed 32-bit offset
+    return ((uint64_t)(g.K - 1) * (uint64_t)g.ldb + (uint64_t)g.N) * 2u <= 0x7FFFFF00ull;
   const int64_t start[3] = {0, g.B.n1, g.B.n2};
   const int64_t end[3] = {g.B.n1, g.B.n2, b_rows};
   for (int k = 0; k < 3; ++k) {
@@ -774,16 +850,16 @@ static int gemm_waves() {
 
 // bf16 GEMMs run 8 waves per workgroup (two per SIMD, 64x128 per wave); operands are
 // streamed by the LDS-DMA kernel unless they span more than its 2 GiB buffer window.
-template <int EPI, typename T16>
+template <int EPI, typename T16, bool BT = false>
 static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, bool allow_dma = true) {
   if (allow_dma && dma_setup(g, b_rows, EPI == EPI_SWIGLU)) {
-    if (gemm_waves() == 4)
-      k_gemm_bf16_dma<EPI, T16, 2><<<grid, 256, 0, s>>>(g);
+    if (!BT && gemm_waves() == 4)  // (the 4-wave tile has no registers left for transposed reads)
+      k_gemm_bf16_dma<EPI, T16, 2, false><<<grid, 256, 0, s>>>(g);
     else
-      k_gemm_bf16_dma<EPI, T16, 4><<<grid, 512, 0, s>>>(g);
+      k_gemm_bf16_dma<EPI, T16, 4, BT><<<grid, 512, 0, s>>>(g);
   }
   else
-    k_gemm_bf16<EPI, T16, 4><<<grid, 512, 0, s>>>(g);
+    k_gemm_bf16<EPI, T16, 4, BT><<<grid, 512, 0, s>>>(g);
 }
 
 hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
@@ -793,6 +869,10 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
   const bool half = dt != RP_F32;
   if (epi == EPI_SWIGLU && (!half || splitk > 1)) return hipErrorInvalidValue;
   if (epi == EPI_LSE && (!half || splitk > 1 || !lse)) return hipErrorInvalidValue;
+  // a transposed B serves the row-parallel projections: residual or split-K epilogue
+  if (B.trans && ((epi != EPI_ADD_F32 && splitk <= 1) || ldb < N ||
+                  (half && ((N & 7) || (ldb & 7) || ((uintptr_t)B.b0 & 15)))))
+    return hipErrorInvalidValue;
   GemmArgs g;
   g.M = M;
   g.N = N;
@@ -820,7 +900,11 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
     const int64_t b_rows = epi == EPI_SWIGLU ? (int64_t)B.n1 + N : N;
     with_half16(dt, [&](auto tag_) {
       using H = decltype(tag_);
-      if (split)
+      if (B.trans && split)
+        launch_half<-1, H, true>(s, g, grid, b_rows);
+      else if (B.trans)
+        launch_half<EPI_ADD_F32, H, true>(s, g, grid, b_rows);
+      else if (split)
         launch_half<-1, H>(s, g, grid, b_rows);
       else if (epi == EPI_STORE)
         launch_half<EPI_STORE, H>(s, g, grid, b_rows);
@@ -837,7 +921,11 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
     g.tiles_m = (M + GF_M - 1) / GF_M;
     g.tiles_n = (N + GF_N - 1) / GF_N;
     dim3 grid(g.tiles_m * g.tiles_n, splitk);
-    if (split)
+    if (B.trans && split)
+      k_gemm_f32<-1, true><<<grid, 256, 0, s>>>(g);
+    else if (B.trans)
+      k_gemm_f32<EPI_ADD_F32, true><<<grid, 256, 0, s>>>(g);
+    else if (split)
       k_gemm_f32<-1><<<grid, 256, 0, s>>>(g);
     else if (epi == EPI_ADD_F32)
       k_gemm_f32<EPI_ADD_F32><<<grid, 256, 0, s>>>(g);

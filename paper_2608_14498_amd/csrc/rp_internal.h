@@ -62,11 +62,16 @@ int32_t lse_parts(int32_t N);
 
 // B operand of a GEMM given as up to three row segments of nn.Linear weights:
 // logical row n < n1 -> b0 + n*ldb; n < n2 -> b1 + (n-n1)*ldb; else b2 + (n-n2)*ldb.
+// trans: B is one matrix stored transposed, [K][N] with row stride ldb (element (n, k)
+// at b0 + k*ldb + n): a row-parallel weight kept in the layout whose shards are
+// contiguous (Section "Parallelism-Aware Weight Sharing", Case 2).  Needs N % 8 == 0 and ldb % 8 == 0 for
+// 16-bit types, and the EPI_ADD_F32 or split-K epilogue.
 struct BSeg {
   const void* b0;
   const void* b1;
   const void* b2;
   int32_t n1, n2;
+  bool trans = false;
 };
 
 // ---- launchers (return hipGetLastError() of the launch) ----

@@ -43,7 +43,9 @@ def prompt_positions(cu: Sequence[int], token_ids: np.ndarray) -> np.ndarray:
 class DeviceModel:
     """Weights resident in HBM plus a model handle of the HIP library."""
 
-    def __init__(self, host_weights, max_position: int, device: str = "cuda"):
+    def __init__(self, host_weights, max_position: int, device: str = "cuda", weight_layout: int = 0):
+        """weight_layout (rb.RP_WO_TRANSPOSED | rb.RP_W_DOWN_TRANSPOSED) stores those row-parallel
+        projections transposed, [in, out], as a training engine's shards would lay them out."""
         m: ModelShape = host_weights.model
         self.shape = m
         self.device = torch.device(device)
@@ -53,7 +55,9 @@ class DeviceModel:
         self.embed = up(host_weights.embed)
         self.lm_head = up(host_weights.lm_head)
         self.final_norm = up(host_weights.final_norm)
-        self.layers = [{k: up(v) for k, v in lw.items()} for lw in host_weights.layers]
+        stored_t = {"wo": weight_layout & rb.RP_WO_TRANSPOSED, "w_down": weight_layout & rb.RP_W_DOWN_TRANSPOSED}
+        self.layers = [{k: up(np.ascontiguousarray(v.T) if stored_t.get(k) else v) for k, v in lw.items()}
+                       for lw in host_weights.layers]
         p = rb._ptr
         arr = (rb.RpLayerWeights * m.n_layers)()
         for i, lw in enumerate(self.layers):
@@ -61,7 +65,7 @@ class DeviceModel:
                 setattr(arr[i], name, p(lw.get(name)))
         self._layer_arr = arr
         self._weights = rb.RpWeights(p(self.embed), p(self.final_norm), p(self.lm_head), arr)
-        self.config = rb.make_config(m, self.max_position)
+        self.config = rb.make_config(m, self.max_position, weight_layout)
         self.handle = rb.rp_create(self.config, self._weights)
 
     def close(self):

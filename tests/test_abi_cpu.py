@@ -77,6 +77,7 @@ def status_of(fn, *args):
     ("n_layers", 0, rb.RP_ERR_SHAPE),
     ("rms_eps", 0.0, rb.RP_ERR_SHAPE),
     ("d_model", 100, rb.RP_ERR_UNSUPPORTED),
+    ("weight_layout", 4, rb.RP_ERR_INVALID_ARG),
 ])
 def test_create_rejects_bad_config(lib, field, value, status):
     cfg = rb.make_config(configs.TINY, 1024)

@@ -291,3 +291,42 @@ def test_prompt_logprobs_match_oracle(model, flags):
           f"|d lp| {err:.3g}", flush=True)
     assert err <= (1e-4 if model.dtype == "f32" else 2e-2)
     dm.close()
+
+
+@pytest.mark.parametrize("model", [configs.TINY, BF16_SMALL, BF16_WIDE, F16_D64])
+def test_transposed_row_parallel_weights(model):
+    """Case-2 storage: wo and w_down stored [in, out] and read in transpose mode.  The MFMAs
+    see the same k order, so prefix, suffix (split-K at d = 2048) and decode step are
+    bitwise those of the nn.Linear layout; the suffix also matches the oracle."""
+    from paper_2608_14498_amd import binding as rb
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+    P, Vis, S = [70, 300, 129], [60, 256, 100], [9, 65, 130]
+    w = configs.custom(model, P, Vis, S, index=85)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    cap, lens = 400, [0, 131, 399]
+    dec = inputs.make_decode(w, batch=len(lens), kv_len=np.array(lens, np.int32), cap=cap)
+    cp, cs = [int(x) for x in bt.cu_prefix], [int(x) for x in bt.cu_suffix]
+    outs = []
+    for layout in (0, rb.RP_WO_TRANSPOSED, rb.RP_WO_TRANSPOSED | rb.RP_W_DOWN_TRANSPOSED):
+        dm = DeviceModel(hw, cap + 1, weight_layout=layout)
+        dev = dm.device
+        K, V, h = dm.prefix(cp, to_device(bt.token_ids, dev), to_device(bt.visual, dev))
+        lp = dm.suffix(cp, cs, K, V, h, to_device(bt.response_ids, dev))
+        ck, cv = to_device(dec.cache_k, dev), to_device(dec.cache_v, dev)
+        logits = torch.empty((len(lens), model.vocab), dtype=torch.float32, device=dev)
+        nxt = dm.decode(ck, cv, to_device(dec.kv_len, dev), to_device(dec.token_ids, dev), logits=logits)
+        torch.cuda.synchronize()
+        outs.append([t.cpu() for t in (K, V, h, lp, logits, nxt, ck)])
+        dm.close()
+    names = ("K", "V", "h_last", "logprobs", "decode logits", "next ids", "cache")
+    for o in outs[1:]:
+        for n, a, b in zip(names, outs[0], o):
+            assert torch.equal(a, b), n
+    lpo = oracle.suffix_logprob(hw.as_f32(), model, cp, cs,
+                                *oracle.prefix_forward(hw.as_f32(), model, cp, bt.token_ids,
+                                                       inputs.to_f32(bt.visual))[:3], bt.response_ids)
+    err = max_abs(outs[-1][3].numpy(), lpo)
+    print(f"[parity] transposed wo/w_down {model.dtype} d={model.d_model}: bitwise equal, |d lp| {err:.3g}",
+          flush=True)
+    assert err <= (1e-4 if model.dtype == "f32" else 2e-2)
