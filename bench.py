@@ -235,6 +235,8 @@ def main():
                     help="skip timing the suffix with the fused lm_head + log-sum-exp scoring")
     ap.add_argument("--no-transposed-variant", action="store_true",
                     help="skip timing the step with o_proj / down weights stored transposed")
+    ap.add_argument("--no-last-rows-variant", action="store_true",
+                    help="skip timing the prefix with RP_PREFIX_LAST_ROWS_ONLY")
     ap.add_argument("--no-prompt-logprobs", action="store_true",
                     help="skip timing the prompt-token log-probs (rp_prompt_logprob)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -358,13 +360,31 @@ def main():
             "ms_per_step": rt["ms_step"], "prefix_ms": rt["pre_ms"], "suffix_ms": rt["suf_ms"],
             "kernels": {k: kt[k] for k in ("prefix.gemm_o_proj", "prefix.gemm_down", "suffix.gemm_o_proj",
                                            "suffix.gemm_down") if k in kt}}
+    if not args.no_last_rows_variant:
+        # labelled optimisation: the last layer carries only each sequence's last row past
+        # its K/V projection (all the suffix pass reads); TFLOP/s counts executed flops
+        from paper_2608_14498_amd import binding as rb
+
+        rl = run_passes(w, args, profile=True, prefix_flags=rb.RP_PREFIX_LAST_ROWS_ONLY)
+        pfl = perf.prefix_flops(m, bt.prefix_lens, last_rows_only=True)
+        kl = rl["kernels"]
+        out["last_rows_only_variant"] = {
+            "label": "prefix last layer past K/V only at each sequence's last row (RP_PREFIX_LAST_ROWS_ONLY)",
+            "value": (rl["T"] + rl["R"]) / (rl["ms_step"] * 1e-3), "unit": "tokens/s",
+            "ms_per_step": rl["ms_step"], "prefix_ms": rl["pre_ms"], "suffix_ms": rl["suf_ms"],
+            "prefix_tokens_per_s": rl["T"] / (rl["pre_ms"] * 1e-3),
+            "prefix_executed_tflop": pfl["total"] / 1e12,
+            "prefix_tflops": pfl["total"] / (rl["pre_ms"] * 1e-3) / 1e12,
+            "prefix_mfma_frac": pfl["total"] / (rl["pre_ms"] * 1e-3) / peak,
+            "kernels": {k: v for k, v in kl.items() if k.startswith("prefix.tail")}}
     if not args.no_cpu_baseline:
         log("CPU baseline: oracle on sequence 0")
         out["cpu_baseline"] = cpu_baseline(w, res["hw"], bt, args.cpu_prefix_len)
     print(json.dumps(out), flush=True)
 
 
-def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, prompt: bool = False):
+def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, prompt: bool = False,
+               prefix_flags: int = 0):
     """Time prefix + suffix steps of workload w; optionally per-kernel durations and the
     prompt-token log-probs."""
     import numpy as np
@@ -407,7 +427,7 @@ def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, p
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        dm.prefix(cu_p, ids, vis, kv=(K, V), h_last=h_last, workspace=ws_p, stream=stream)
+        dm.prefix(cu_p, ids, vis, kv=(K, V), h_last=h_last, workspace=ws_p, stream=stream, flags=prefix_flags)
         if ev is not None:
             ev[1].record(stream)
         if not grouped:

@@ -195,6 +195,26 @@ rp_status rp_suffix_logprob(const rp_model *model, void *stream, int32_t B,
                             void *workspace, size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
+ * Prefix pass with options: rp_prefix_forward (positions and mrope_section
+ * NULL) or rp_prefix_forward_mrope (both given), plus flags:
+ *   RP_PREFIX_LAST_ROWS_ONLY  the suffix pass reads every prefix row's K/V but
+ *     only the boundary state h_last (Section "Cross-Phase Execution"), so the
+ *     last layer runs its K/V projection for every row and the rest (attention,
+ *     o-proj, MLP) only at each sequence's last row.  kv_out is exactly that of
+ *     the full pass; h_last equals it up to fp32 summation order (its GEMMs
+ *     split K over the few rows).  hidden_out must be NULL (RP_ERR_INVALID_ARG).
+ * Unknown flag bits are RP_ERR_INVALID_ARG.  Workspace: rp_prefix_workspace_bytes.
+ * ------------------------------------------------------------------------- */
+#define RP_PREFIX_LAST_ROWS_ONLY 1u
+#define RP_PREFIX_FLAGS 1u /* all defined flag bits */
+rp_status rp_prefix_forward_flags(const rp_model *model, void *stream, int32_t B,
+                                  const int32_t *cu_seqlens_host, const int32_t *token_ids,
+                                  const void *visual_embeds, int64_t n_visual,
+                                  const int32_t *positions, const int32_t *mrope_section,
+                                  uint32_t flags, rp_kv kv_out, float *h_last, float *hidden_out,
+                                  void *workspace, size_t workspace_bytes);
+
+/* ---------------------------------------------------------------------------
  * Shared-prefix suffix pass (Section "Prefix Sharing": the N sampled responses
  * of a GRPO prompt group share one video-text prefix, whose prefix pass runs
  * once per group and is reused by every response).  n_suffix sequences score

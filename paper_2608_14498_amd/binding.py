@@ -22,7 +22,9 @@ _DTYPES = {"f32": RP_F32, "bf16": RP_BF16, "f16": RP_F16}
 RP_MAX_SEQS = 256
 RP_SUFFIX_FUSED_LOGPROB = 1
 RP_WO_TRANSPOSED, RP_W_DOWN_TRANSPOSED = 1, 2
+RP_PREFIX_LAST_ROWS_ONLY = 1
 SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_forward", "rp_prefix_forward_mrope",
+           "rp_prefix_forward_flags",
            "rp_suffix_workspace_bytes", "rp_suffix_logprob", "rp_suffix_grouped_workspace_bytes",
            "rp_suffix_logprob_grouped", "rp_prompt_logprob_workspace_bytes", "rp_prompt_logprob",
            "rp_decode_workspace_bytes",
@@ -88,6 +90,9 @@ def lib():
             "rp_prefix_forward_mrope": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
                                                 c_int64, c_void_p, POINTER(c_int32), RpKV, c_void_p, c_void_p,
                                                 c_void_p, c_size_t]),
+            "rp_prefix_forward_flags": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
+                                                c_int64, c_void_p, POINTER(c_int32), c_uint32, RpKV, c_void_p,
+                                                c_void_p, c_void_p, c_size_t]),
             "rp_prompt_logprob_workspace_bytes": (c_int, [c_void_p, c_int32, c_uint32, POINTER(c_size_t)]),
             "rp_prompt_logprob": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
                                           c_int32, c_void_p, c_uint32, c_void_p, c_void_p, c_size_t]),
@@ -227,6 +232,15 @@ def rp_prompt_logprob(model: int, stream, B: int, cu_seqlens, token_ids, hidden,
     _check(lib().rp_prompt_logprob(model, _ptr(stream), B, _i32(cu_seqlens), _ptr(token_ids), _ptr(hidden),
                                    int(n_rows), _ptr(positions), int(flags), _ptr(logprobs), _ptr(workspace),
                                    int(workspace_bytes)))
+
+
+def rp_prefix_forward_flags(model: int, stream, B: int, cu_seqlens, token_ids, visual_embeds, n_visual: int,
+                            positions, mrope_section, flags: int, kv_out: RpKV, h_last, hidden_out, workspace,
+                            workspace_bytes: int) -> None:
+    _check(lib().rp_prefix_forward_flags(model, _ptr(stream), B, _i32(cu_seqlens), _ptr(token_ids),
+                                         _ptr(visual_embeds), int(n_visual), _ptr(positions), _i32(mrope_section),
+                                         int(flags), kv_out, _ptr(h_last), _ptr(hidden_out), _ptr(workspace),
+                                         int(workspace_bytes)))
 
 
 def rp_decode_workspace_bytes(model: int, B: int, cap: int) -> int:

@@ -272,12 +272,40 @@ LayerPlan plan_layer(const rp_config& c, int32_t M, Pass pass) {
   return p;
 }
 
-size_t prefix_ws(const rp_model* m, int64_t T, void* base, bool need_x, LayerWS* w, int32_t** vis_idx) {
+// Buffers of the last layer's last-row tail (RP_PREFIX_LAST_ROWS_ONLY), B rows each.
+struct TailWS {
+  void* Q;      // [B, Hq*D] rotated queries of the last rows
+  void* K;      // [B, Hkv*D] their keys and values
+  void* V;
+  void* O;      // [B, Hq*D] attention output
+  void* N;      // [B, d] normed activations
+  void* GU;     // [B, 2F] (unfused gate/up)
+  void* ACT;    // [B, F]
+  float* part;  // split-K partials
+  LayerPlan plan;
+};
+
+size_t prefix_ws(const rp_model* m, int32_t B, int64_t T, void* base, bool need_x, LayerWS* w, int32_t** vis_idx,
+                 TailWS* tail = nullptr) {
   Carver c(base);
   int32_t* vi = (int32_t*)c.take(T * 4);
   if (vis_idx) *vis_idx = vi;
   LayerWS tmp;
   carve_layer(c, m->cfg, T, need_x, !plan_layer(m->cfg, (int32_t)T, Pass::kPrefix).fused, w ? w : &tmp);
+  const rp_config& cf = m->cfg;
+  const size_t es = elem_size(cf);
+  const int64_t hq = (int64_t)cf.n_q_heads * cf.head_dim, kvr = (int64_t)cf.n_kv_heads * cf.head_dim;
+  TailWS tt;
+  TailWS* t = tail ? tail : &tt;
+  t->plan = plan_layer(cf, B, Pass::kDecode);
+  t->Q = c.take(B * hq * es);
+  t->K = c.take(B * kvr * es);
+  t->V = c.take(B * kvr * es);
+  t->O = c.take(B * hq * es);
+  t->N = c.take(B * (int64_t)cf.d_model * es);
+  t->GU = t->plan.fused ? nullptr : c.take(B * 2 * (int64_t)cf.ffn_dim * es);
+  t->ACT = c.take(B * (int64_t)cf.ffn_dim * es);
+  t->part = (float*)c.take(t->plan.part_floats * 4);
   return c.off + 256;
 }
 
@@ -454,10 +482,67 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   return RP_OK;
 }
 
+// Last layer of a RP_PREFIX_LAST_ROWS_ONLY prefix pass: the suffix reads every row's K/V
+// but only the boundary state, so past the K/V projection only each sequence's last row
+// is carried on.  Its query attends to the sequence's other keys (the first key segment,
+// rows cu[b] .. cu[b+1]-2) and to its own key; its residual row, gathered into h_last,
+// takes the o-proj and the MLP.
+rp_status run_last_rows(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, int32_t B, const int32_t* cu,
+                        const rp::SeqTable& tab, int32_t T, const LayerWS& w, const TailWS& t, void* kl, void* vl,
+                        const rp::MRope& mr, float* h_last) {
+  const rp_config& c = m->cfg;
+  const rp_dtype dt = c.dtype;
+  const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
+  const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
+  const int es = (int)elem_size(c);
+  RP_TRY_LAUNCH_N("prefix.rmsnorm", rp::launch_rmsnorm(s, dt, w.X, lw.attn_norm, c.rms_eps, T, d, w.N));
+  const rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
+  RP_TRY_LAUNCH_N("prefix.gemm_qkv", rp::launch_gemm(s, dt, T, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE_F32, 1,
+                                                     nullptr));
+  RP_TRY_LAUNCH_N("prefix.rope_kv", rp::launch_rope_kv(s, dt, tab, w.QKV, T, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope,
+                                                       c.max_position, w.Q, kl, vl, mr));
+  RP_TRY_LAUNCH_N("prefix.tail_gather", rp::launch_gather_last(s, tab, w.Q, hq * es, kl, vl, Hkv * D * es, w.X, d, t.Q,
+                                                               t.K, t.V, h_last));
+  int32_t one[RP_MAX_SEQS + 1];  // one query row per sequence
+  for (int b = 0; b <= B; ++b) one[b] = b;
+  rp::SeqTable tl = make_table(B, one, B, cu, nullptr);
+  tl.k_drop = 1;
+  rp::AttnArgs a;
+  a.q = t.Q;
+  a.q_ld = hq;
+  a.k0 = kl;
+  a.v0 = vl;
+  a.k1 = t.K;
+  a.v1 = t.V;
+  a.o = t.O;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.D = D;
+  a.scale = (float)(1.0 / sqrt((double)D));
+  RP_TRY_LAUNCH_N("prefix.tail_attention", rp::launch_attention(s, dt, tl, a, B));
+  const rp::BSeg bo = wo_operand(c, lw);
+  RP_TRY_LAUNCH_N("prefix.tail_gemm_o_proj", rp::launch_gemm(s, dt, B, d, hq, t.O, hq, bo, bo.trans ? d : hq, h_last, d,
+                                                             rp::EPI_ADD_F32, t.plan.o, t.part));
+  RP_TRY_LAUNCH_N("prefix.tail_rmsnorm", rp::launch_rmsnorm(s, dt, h_last, lw.mlp_norm, c.rms_eps, B, d, t.N));
+  const rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
+  if (t.plan.fused) {
+    RP_TRY_LAUNCH_N("prefix.tail_gemm_gate_up", rp::launch_gemm(s, dt, B, F, d, t.N, d, bgu, d, t.ACT, F, rp::EPI_SWIGLU, 1,
+                                                                nullptr));
+  } else {
+    RP_TRY_LAUNCH_N("prefix.tail_gemm_gate_up", rp::launch_gemm(s, dt, B, 2 * F, d, t.N, d, bgu, d, t.GU, 2 * F,
+                                                                rp::EPI_STORE, t.plan.gu, t.part));
+    RP_TRY_LAUNCH_N("prefix.tail_swiglu", rp::launch_swiglu(s, dt, t.GU, B, F, t.ACT));
+  }
+  const rp::BSeg bd = w_down_operand(c, lw);
+  RP_TRY_LAUNCH_N("prefix.tail_gemm_down", rp::launch_gemm(s, dt, B, d, F, t.ACT, F, bd, bd.trans ? d : F, h_last, d,
+                                                           rp::EPI_ADD_F32, t.plan.down, t.part));
+  return RP_OK;
+}
+
 // Prefix pass over B sequences (1-D positions, or multimodal ones when mr.pos is set).
 rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* cu, const int32_t* token_ids,
-                     const void* visual, int64_t n_visual, const rp::MRope& mr, rp_kv kv_out, float* h_last,
-                     float* hidden_out, void* ws, size_t ws_bytes) {
+                     const void* visual, int64_t n_visual, const rp::MRope& mr, uint32_t flags, rp_kv kv_out,
+                     float* h_last, float* hidden_out, void* ws, size_t ws_bytes) {
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
   rp_status st = check_prefix_cu(m, B, cu, "cu_seqlens");
   if (st != RP_OK) return st;
@@ -469,15 +554,20 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
   if ((hidden_out && !aligned16(hidden_out)) || !aligned16(h_last))
     return fail(RP_ERR_INVALID_ARG, "h_last / hidden_out must be 16-byte aligned");
   if ((st = check_kv(m, kv_out, T, "kv_out")) != RP_OK) return st;
-  const size_t need = prefix_ws(m, T, nullptr, hidden_out == nullptr, nullptr, nullptr);
+  if (flags & ~RP_PREFIX_FLAGS) return fail(RP_ERR_INVALID_ARG, "unknown prefix flags 0x%x", flags);
+  const bool last_rows = (flags & RP_PREFIX_LAST_ROWS_ONLY) != 0;
+  if (last_rows && hidden_out)
+    return fail(RP_ERR_INVALID_ARG, "RP_PREFIX_LAST_ROWS_ONLY computes no full hidden state (hidden_out must be NULL)");
+  const size_t need = prefix_ws(m, B, T, nullptr, hidden_out == nullptr, nullptr, nullptr);
   if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
 
   hipStream_t s = (hipStream_t)stream;
   const rp_config& c = m->cfg;
   const rp_dtype dt = c.dtype;
   LayerWS w;
+  TailWS tail;
   int32_t* vis_idx = nullptr;
-  prefix_ws(m, T, ws, hidden_out == nullptr, &w, &vis_idx);
+  prefix_ws(m, B, T, ws, hidden_out == nullptr, &w, &vis_idx, &tail);
   if (hidden_out) w.X = hidden_out;
   const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
   const LayerPlan plan = plan_layer(c, (int32_t)T, Pass::kPrefix);
@@ -488,6 +578,8 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
   for (int l = 0; l < c.n_layers; ++l) {
     void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
     void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
+    if (last_rows && l == c.n_layers - 1)
+      return run_last_rows(m, s, m->layers[l], B, cu, tab, (int32_t)T, w, tail, kl, vl, mr, h_last);
     st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames, mr);
     if (st != RP_OK) return st;
   }
@@ -596,14 +688,14 @@ rp_status rp_prefix_workspace_bytes(const rp_model* m, int32_t B, const int32_t*
   if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
   rp_status s = check_prefix_cu(m, B, cu, "cu_seqlens");
   if (s != RP_OK) return s;
-  *bytes = prefix_ws(m, cu[B], nullptr, true, nullptr, nullptr);
+  *bytes = prefix_ws(m, B, cu[B], nullptr, true, nullptr, nullptr);
   return RP_OK;
 }
 
 rp_status rp_prefix_forward(const rp_model* m, void* stream, int32_t B, const int32_t* cu, const int32_t* token_ids,
                             const void* visual, int64_t n_visual, rp_kv kv_out, float* h_last, float* hidden_out,
                             void* ws, size_t ws_bytes) {
-  return prefix_run(m, stream, B, cu, token_ids, visual, n_visual, rp::MRope{nullptr, 0, 0}, kv_out, h_last,
+  return prefix_run(m, stream, B, cu, token_ids, visual, n_visual, rp::MRope{nullptr, 0, 0}, 0u, kv_out, h_last,
                     hidden_out, ws, ws_bytes);
 }
 
@@ -613,6 +705,20 @@ rp_status rp_prefix_forward_mrope(const rp_model* m, void* stream, int32_t B, co
                                   float* h_last, float* hidden_out, void* ws, size_t ws_bytes) {
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
   if (!positions || !mrope_section) return fail(RP_ERR_INVALID_ARG, "positions and mrope_section are required");
+  return rp_prefix_forward_flags(m, stream, B, cu, token_ids, visual, n_visual, positions, mrope_section, 0u, kv_out,
+                                 h_last, hidden_out, ws, ws_bytes);
+}
+
+rp_status rp_prefix_forward_flags(const rp_model* m, void* stream, int32_t B, const int32_t* cu,
+                                  const int32_t* token_ids, const void* visual, int64_t n_visual,
+                                  const int32_t* positions, const int32_t* mrope_section, uint32_t flags,
+                                  rp_kv kv_out, float* h_last, float* hidden_out, void* ws, size_t ws_bytes) {
+  if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
+  if (!positions != !mrope_section)
+    return fail(RP_ERR_INVALID_ARG, "positions and mrope_section go together (both NULL: 1-D positions)");
+  if (!positions)
+    return prefix_run(m, stream, B, cu, token_ids, visual, n_visual, rp::MRope{nullptr, 0, 0}, flags, kv_out, h_last,
+                      hidden_out, ws, ws_bytes);
   if (!aligned16(positions)) return fail(RP_ERR_INVALID_ARG, "positions must be 16-byte aligned");
   const int half = m->cfg.head_dim / 2;
   if (mrope_section[0] < 0 || mrope_section[1] < 0 || mrope_section[2] < 0 ||
@@ -620,7 +726,8 @@ rp_status rp_prefix_forward_mrope(const rp_model* m, void* stream, int32_t B, co
     return fail(RP_ERR_SHAPE, "mrope_section (%d, %d, %d) must be non-negative and sum to head_dim / 2 = %d",
                 mrope_section[0], mrope_section[1], mrope_section[2], half);
   const rp::MRope mr = {positions, mrope_section[0], mrope_section[0] + mrope_section[1]};
-  return prefix_run(m, stream, B, cu, token_ids, visual, n_visual, mr, kv_out, h_last, hidden_out, ws, ws_bytes);
+  return prefix_run(m, stream, B, cu, token_ids, visual, n_visual, mr, flags, kv_out, h_last, hidden_out, ws,
+                    ws_bytes);
 }
 
 rp_status rp_suffix_workspace_bytes(const rp_model* m, int32_t B, const int32_t* pcu, const int32_t* scu,

@@ -366,6 +366,33 @@ hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X,
   return hipGetLastError();
 }
 
+__device__ __forceinline__ void copy_row16(char* __restrict__ dst, const char* __restrict__ src, int bytes) {
+  for (int c = threadIdx.x * 16; c < bytes; c += blockDim.x * 16)
+    *reinterpret_cast<uint4*>(dst + c) = *reinterpret_cast<const uint4*>(src + c);
+}
+
+__global__ __launch_bounds__(256) void k_gather_last(SeqTable st, const char* __restrict__ q, int q_bytes,
+                                                     const char* __restrict__ k, const char* __restrict__ v,
+                                                     int kv_bytes, const float* __restrict__ X, int d,
+                                                     char* __restrict__ qs, char* __restrict__ ks,
+                                                     char* __restrict__ vs, float* __restrict__ h) {
+  const int b = blockIdx.x;
+  const int64_t r = st.q_cu[b + 1] - 1;
+  copy_row16(qs + (int64_t)b * q_bytes, q + r * q_bytes, q_bytes);
+  copy_row16(ks + (int64_t)b * kv_bytes, k + r * kv_bytes, kv_bytes);
+  copy_row16(vs + (int64_t)b * kv_bytes, v + r * kv_bytes, kv_bytes);
+  copy_row16((char*)(h + (int64_t)b * d), (const char*)(X + r * d), d * 4);
+}
+
+hipError_t launch_gather_last(hipStream_t s, const SeqTable& st, const void* q, int32_t q_bytes, const void* k,
+                              const void* v, int32_t kv_bytes, const float* X, int32_t d, void* qs, void* ks,
+                              void* vs, float* h) {
+  if ((q_bytes | kv_bytes | (d * 4)) & 15) return hipErrorInvalidValue;
+  k_gather_last<<<st.n, 256, 0, s>>>(st, (const char*)q, q_bytes, (const char*)k, (const char*)v, kv_bytes, X, d,
+                                     (char*)qs, (char*)ks, (char*)vs, h);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------------------------
 // Fused log-softmax + gather: lp[r] = l[r, id_r] - (m + log sum exp(l - m)), one pass
 // over the row with a running (max, scaled sum) per thread, merged across the block.

@@ -18,10 +18,11 @@ struct SeqTable {
   int32_t k_cu[RP_MAX_SEQS + 1];   // prefix p's KV rows: k_cu[p] .. k_cu[p+1]-1
   int32_t rope0[RP_MAX_SEQS];      // rotary position of the first query row after prefix p
   uint8_t grp[RP_MAX_SEQS];        // prefix of sequence b (b itself unless prefixes are shared)
+  int32_t k_drop;                  // rows left out at the end of every first key segment
   // first row and length of sequence b's first key segment; the length is also the
   // index of b's first query row in its key space (the causal rule)
   __host__ __device__ int32_t k_beg(int b) const { return k_cu[grp[b]]; }
-  __host__ __device__ int32_t pos0(int b) const { return k_cu[grp[b] + 1] - k_cu[grp[b]]; }
+  __host__ __device__ int32_t pos0(int b) const { return k_cu[grp[b] + 1] - k_cu[grp[b]] - k_drop; }
   // rotary position of b's first query row (pos0 unless the prefix used multimodal RoPE)
   __host__ __device__ int32_t rpos0(int b) const { return rope0[grp[b]]; }
 };
@@ -101,6 +102,11 @@ hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const 
                           void* v_out, const MRope& mr);
 hipError_t launch_swiglu(hipStream_t s, rp_dtype dt, const void* gu, int32_t M, int32_t F, void* act);
 hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X, int32_t d, float* h_last);
+// Last row r = q_cu[b+1]-1 of every sequence b: qs[b] = q[r] (q_bytes), ks[b] = k[r] and
+// vs[b] = v[r] (kv_bytes each), h[b] = X[r] (d floats).  Byte counts are multiples of 16.
+hipError_t launch_gather_last(hipStream_t s, const SeqTable& st, const void* q, int32_t q_bytes, const void* k,
+                              const void* v, int32_t kv_bytes, const float* X, int32_t d, void* qs, void* ks,
+                              void* vs, float* h);
 // lp[r] = log softmax(logits[r])[ids[r]] (ids clamped to [0, V)); NaN where ids[r] < 0
 // when neg_nan is set.
 hipError_t launch_logsoftmax_gather(hipStream_t s, const float* logits, const int32_t* ids, int32_t R,

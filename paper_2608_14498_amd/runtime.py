@@ -93,9 +93,10 @@ class DeviceModel:
     # ---------------------------------------------------------------- passes
     def prefix(self, cu: Sequence[int], token_ids: torch.Tensor, visual: Optional[torch.Tensor],
                kv=None, h_last=None, hidden_out=None, workspace=None, stream=None, positions=None,
-               mrope_section=None):
+               mrope_section=None, flags: int = 0):
         """Prefix pass.  Returns (K, V, h_last) with K/V [L, T, Hkv, Dh].  With positions
-        (device int32 [3, T]) and mrope_section, RoPE uses multimodal 3-D positions."""
+        (device int32 [3, T]) and mrope_section, RoPE uses multimodal 3-D positions; flags
+        (rb.RP_PREFIX_LAST_ROWS_ONLY) select options of rp_prefix_forward_flags."""
         m = self.shape
         B, T = len(cu) - 1, int(cu[-1])
         K, V = kv if kv is not None else self.alloc_kv(T)
@@ -104,7 +105,11 @@ class DeviceModel:
         nbytes = rb.rp_prefix_workspace_bytes(self.handle, B, cu)
         ws = workspace if workspace is not None else self.workspace(nbytes)
         n_visual = 0 if visual is None else visual.shape[0]
-        if positions is None:
+        if flags:
+            rb.rp_prefix_forward_flags(self.handle, stream_ptr(stream), B, cu, token_ids, visual, n_visual,
+                                       positions, mrope_section, flags, rb.make_kv(K, V, K[0].numel()), h_last,
+                                       hidden_out, ws, ws.numel())
+        elif positions is None:
             rb.rp_prefix_forward(self.handle, stream_ptr(stream), B, cu, token_ids, visual, n_visual,
                                  rb.make_kv(K, V, K[0].numel()), h_last, hidden_out, ws, ws.numel())
         else:

@@ -197,6 +197,26 @@ def test_prefix_mrope_validation(lib):
         rb.rp_destroy(h)
 
 
+def test_prefix_flags_validation(lib):
+    h, keep = make()
+    try:
+        args = list(_prefix_args(h))
+        base, rest = args[:7], args[7:]
+        last = rb.RP_PREFIX_LAST_ROWS_ONLY
+        assert status_of(rb.rp_prefix_forward_flags, *base, None, None, 2, *rest)[0] == rb.RP_ERR_INVALID_ARG
+        with_hidden = list(rest)
+        with_hidden[2] = FAKE + (1 << 36)                       # hidden_out
+        assert status_of(rb.rp_prefix_forward_flags, *base, None, None, last, *with_hidden)[0] == \
+            rb.RP_ERR_INVALID_ARG
+        assert status_of(rb.rp_prefix_forward_flags, *base, FAKE + (1 << 35), None, last, *rest)[0] == \
+            rb.RP_ERR_INVALID_ARG
+        bad_ws = list(rest)
+        bad_ws[4] = 1000
+        assert status_of(rb.rp_prefix_forward_flags, *base, None, None, last, *bad_ws)[0] == rb.RP_ERR_WORKSPACE
+    finally:
+        rb.rp_destroy(h)
+
+
 def test_fused_scoring_workspace_holds_partials_not_logits(lib):
     h, keep = make(configs.QWEN7B_SLICE, max_pos=8192)
     try:

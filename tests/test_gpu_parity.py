@@ -330,3 +330,58 @@ def test_transposed_row_parallel_weights(model):
     print(f"[parity] transposed wo/w_down {model.dtype} d={model.d_model}: bitwise equal, |d lp| {err:.3g}",
           flush=True)
     assert err <= (1e-4 if model.dtype == "f32" else 2e-2)
+
+
+@pytest.mark.parametrize("model,mrope", [(configs.TINY, False), (BF16_SMALL, False), (BF16_D64, True),
+                                         (F16_SMALL, False), (BF16_WIDE, False)])
+def test_prefix_last_rows_only(model, mrope):
+    """RP_PREFIX_LAST_ROWS_ONLY: the last layer past its K/V projection runs only at each
+    sequence's last row.  K/V are bitwise those of the full pass, h_last equals the full
+    pass's up to summation order, and both meet the oracle bar (so do the suffix log-probs
+    scored from them).  P = 1 leaves the last row's query with only its own key."""
+    from paper_2608_14498_amd import binding as rb
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+    from tests.test_oracle_pins import video_positions
+    P, Vis, S = [1, 70, 300, 129], [0, 60, 256, 100], [3, 9, 65, 130]
+    w = configs.custom(model, P, Vis, S, index=87)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    cp, cs = [int(x) for x in bt.cu_prefix], [int(x) for x in bt.cu_suffix]
+    dm = DeviceModel(hw, max(p + s for p, s in zip(P, S)) + 1)
+    dev = dm.device
+    ids, vis = to_device(bt.token_ids, dev), to_device(bt.visual, dev)
+    kw, rope0 = {}, None
+    sec = (8, 12, 12) if model.head_dim == 64 else (16, 24, 24)
+    if mrope:
+        grids = [(1, 1, 1), (3, 4, 5), (4, 8, 8), (4, 5, 5)]
+        pos, nxt = zip(*[video_positions(v, p - v, g) if v else (np.zeros((3, p), np.int64), p)
+                         for p, v, g in zip(P, Vis, grids)])
+        kw = dict(positions=torch.as_tensor(np.concatenate(pos, axis=1).astype(np.int32), device=dev).contiguous(),
+                  mrope_section=list(sec))
+        rope0 = [int(n) for n in nxt]
+    Kf, Vf, hf = dm.prefix(cp, ids, vis, **kw)
+    Kt, Vt, ht = dm.prefix(cp, ids, vis, flags=rb.RP_PREFIX_LAST_ROWS_ONLY, **kw)
+    lp = dm.suffix_grouped(cp, list(range(len(P))), cs, Kt, Vt, ht, to_device(bt.response_ids, dev),
+                           rope_pos0=rope0)
+    torch.cuda.synchronize()
+    assert torch.equal(Kf, Kt) and torch.equal(Vf, Vt)
+    f32 = model.dtype == "f32"
+    d_full = rel_err(ht.cpu().numpy(), hf.cpu().numpy())
+    W = hw.as_f32()
+    vo = np.concatenate([[0], np.cumsum(Vis)])
+    visf = inputs.to_f32(bt.visual)
+    e_h, e_lp = 0.0, 0.0
+    for b in range(len(P)):
+        idb = bt.token_ids[cp[b]:cp[b + 1]]
+        mr = (pos[b], sec) if mrope else None
+        k, v, hl, _ = oracle.prefix_forward_one(W, model, idb, visf[vo[b]:vo[b + 1]], mrope=mr)
+        e_h = max(e_h, rel_err(ht[b].cpu().numpy(), hl))
+        lpo = oracle.suffix_logprob_one(W, model, k, v, hl, bt.response_ids[cs[b]:cs[b + 1]],
+                                        rope_start=None if rope0 is None else rope0[b])
+        e_lp = max(e_lp, max_abs(lp[cs[b]:cs[b + 1]].cpu().numpy(), lpo))
+    print(f"[parity] last-rows-only prefix {model.dtype} d={model.d_model} mrope={mrope}: h vs full {d_full:.3g}, "
+          f"h vs oracle {e_h:.3g}, |d lp| {e_lp:.3g}", flush=True)
+    assert d_full <= (1e-5 if f32 else 1e-2)
+    assert e_h <= (1e-5 if f32 else 3e-2)
+    assert e_lp <= (1e-4 if f32 else 2e-2)
+    dm.close()
