@@ -274,6 +274,7 @@ LayerPlan plan_layer(const rp_config& c, int32_t M, Pass pass) {
 
 // Buffers of the last layer's last-row tail (RP_PREFIX_LAST_ROWS_ONLY), B rows each.
 struct TailWS {
+  float* Qf;    // [B, Hq*D] fp32 query projections of the last rows
   void* Q;      // [B, Hq*D] rotated queries of the last rows
   void* K;      // [B, Hkv*D] their keys and values
   void* V;
@@ -298,6 +299,9 @@ size_t prefix_ws(const rp_model* m, int32_t B, int64_t T, void* base, bool need_
   TailWS tt;
   TailWS* t = tail ? tail : &tt;
   t->plan = plan_layer(cf, B, Pass::kDecode);
+  const size_t qpart = rp::gemm_partial_floats(B, (int32_t)hq, decode_splitk(cf, B, (int32_t)hq, cf.d_model));
+  if (qpart > t->plan.part_floats) t->plan.part_floats = qpart;
+  t->Qf = (float*)c.take(B * hq * 4);
   t->Q = c.take(B * hq * es);
   t->K = c.take(B * kvr * es);
   t->V = c.take(B * kvr * es);
@@ -483,10 +487,12 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
 }
 
 // Last layer of a RP_PREFIX_LAST_ROWS_ONLY prefix pass: the suffix reads every row's K/V
-// but only the boundary state, so past the K/V projection only each sequence's last row
-// is carried on.  Its query attends to the sequence's other keys (the first key segment,
-// rows cu[b] .. cu[b+1]-2) and to its own key; its residual row, gathered into h_last,
-// takes the o-proj and the MLP.
+// but only the boundary state, so beyond the K/V projection only each sequence's last row
+// is carried on.  Keys and values are projected for every row, the query for the last
+// rows only (scattered into the projection buffer, where RoPE rotates it).  The last
+// row's query attends to the sequence's other keys (the first key segment, rows cu[b] ..
+// cu[b+1]-2) and to its own key; its residual row, gathered into h_last, takes the o-proj
+// and the MLP.
 rp_status run_last_rows(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, int32_t B, const int32_t* cu,
                         const rp::SeqTable& tab, int32_t T, const LayerWS& w, const TailWS& t, void* kl, void* vl,
                         const rp::MRope& mr, float* h_last) {
@@ -495,12 +501,20 @@ rp_status run_last_rows(const rp_model* m, hipStream_t s, const rp_layer_weights
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
   const int es = (int)elem_size(c);
+  const int kvr = Hkv * D;
   RP_TRY_LAUNCH_N("prefix.rmsnorm", rp::launch_rmsnorm(s, dt, w.X, lw.attn_norm, c.rms_eps, T, d, w.N));
-  const rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
-  RP_TRY_LAUNCH_N("prefix.gemm_qkv", rp::launch_gemm(s, dt, T, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE_F32, 1,
-                                                     nullptr));
+  const rp::BSeg bkv = {lw.wk, lw.wv, lw.wv, kvr, 2 * kvr};
+  RP_TRY_LAUNCH_N("prefix.gemm_kv", rp::launch_gemm(s, dt, T, 2 * kvr, d, w.N, d, bkv, d, w.QKV + hq, qkv,
+                                                    rp::EPI_STORE_F32, 1, nullptr));
+  RP_TRY_LAUNCH_N("prefix.tail_gather_n", rp::launch_copy_last_rows(s, tab, w.N, (int64_t)d * es, t.N, (int64_t)d * es,
+                                                                    d * es, false));
+  const rp::BSeg bq = {lw.wq, lw.wq, lw.wq, hq, hq};
+  RP_TRY_LAUNCH_N("prefix.tail_gemm_q", rp::launch_gemm(s, dt, B, hq, d, t.N, d, bq, d, t.Qf, hq, rp::EPI_STORE_F32,
+                                                        decode_splitk(c, B, hq, d), t.part));
+  RP_TRY_LAUNCH_N("prefix.tail_scatter_q", rp::launch_copy_last_rows(s, tab, t.Qf, (int64_t)hq * 4, w.QKV,
+                                                                     (int64_t)qkv * 4, hq * 4, true));
   RP_TRY_LAUNCH_N("prefix.rope_kv", rp::launch_rope_kv(s, dt, tab, w.QKV, T, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope,
-                                                       c.max_position, w.Q, kl, vl, mr));
+                                                       c.max_position, w.Q, kl, vl, mr, true));
   RP_TRY_LAUNCH_N("prefix.tail_gather", rp::launch_gather_last(s, tab, w.Q, hq * es, kl, vl, Hkv * D * es, w.X, d, t.Q,
                                                                t.K, t.V, h_last));
   int32_t one[RP_MAX_SEQS + 1];  // one query row per sequence

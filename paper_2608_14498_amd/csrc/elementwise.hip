@@ -216,7 +216,7 @@ __device__ __forceinline__ void rope_row(const float* __restrict__ row, const in
                                          int Hq, int Hkv, int D, const T* __restrict__ bq,
                                          const T* __restrict__ bk, const T* __restrict__ bv, const RopeFreq& rf,
                                          T* __restrict__ q_dst, T* __restrict__ k_dst, T* __restrict__ v_dst,
-                                         float* cs) {
+                                         float* cs, bool do_q = true) {
   const int half = D >> 1;
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     float c, s;
@@ -225,7 +225,7 @@ __device__ __forceinline__ void rope_row(const float* __restrict__ row, const in
     cs[64 + i] = s;
   }
   __syncthreads();
-  const int nq = Hq * half, nk = Hkv * half;
+  const int nq = do_q ? Hq * half : 0, nk = Hkv * half;
   for (int p = threadIdx.x; p < nq + nk; p += blockDim.x) {
     const bool isq = p < nq;
     const int pp = isq ? p : p - nq;
@@ -259,10 +259,15 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_rope_kv(SeqTable st, const float* __restrict__ qkv, int Hq, int Hkv,
                                                  int D, const T* __restrict__ bq, const T* __restrict__ bk,
                                                  const T* __restrict__ bv, RopeFreq rf, int max_pos, MRope mr, int M,
-                                                 T* __restrict__ q_out, T* __restrict__ k_out,
+                                                 int q_last_only, T* __restrict__ q_out, T* __restrict__ k_out,
                                                  T* __restrict__ v_out) {
   __shared__ float cs[128];
   const int r = blockIdx.x;
+  bool do_q = true;
+  if (q_last_only) {
+    const int b = seq_of_row(st, r);
+    do_q = r == st.q_cu[b + 1] - 1;
+  }
   int pos[3];
   if (mr.pos) {
 #pragma unroll
@@ -273,19 +278,19 @@ __global__ __launch_bounds__(256) void k_rope_kv(SeqTable st, const float* __res
   }
   const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
   rope_row<T>(qkv + r * ld, pos, mr.pos ? mr.sec0 : D, mr.pos ? mr.sec01 : D, Hq, Hkv, D, bq, bk, bv, rf,
-              q_out + (int64_t)r * Hq * D, k_out + (int64_t)r * Hkv * D, v_out + (int64_t)r * Hkv * D, cs);
+              q_out + (int64_t)r * Hq * D, k_out + (int64_t)r * Hkv * D, v_out + (int64_t)r * Hkv * D, cs, do_q);
 }
 
 hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* qkv, int32_t M,
                           int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
                           const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
-                          void* v_out, const MRope& mr) {
+                          void* v_out, const MRope& mr, bool q_last_only) {
   if (M <= 0) return hipSuccess;
   with_storage(dt, [&](auto tag_) {
     using E = decltype(tag_);
     k_rope_kv<E><<<M, 256, 0, s>>>(st, qkv, Hq, Hkv, D, (const E*)bq, (const E*)bk,
-                                        (const E*)bv, rf, max_pos, mr, M, (E*)q_out, (E*)k_out,
-                                        (E*)v_out);
+                                        (const E*)bv, rf, max_pos, mr, M, q_last_only ? 1 : 0, (E*)q_out,
+                                        (E*)k_out, (E*)v_out);
   });
   return hipGetLastError();
 }
@@ -382,6 +387,20 @@ __global__ __launch_bounds__(256) void k_gather_last(SeqTable st, const char* __
   copy_row16(ks + (int64_t)b * kv_bytes, k + r * kv_bytes, kv_bytes);
   copy_row16(vs + (int64_t)b * kv_bytes, v + r * kv_bytes, kv_bytes);
   copy_row16((char*)(h + (int64_t)b * d), (const char*)(X + r * d), d * 4);
+}
+
+__global__ __launch_bounds__(256) void k_copy_last_rows(SeqTable st, const char* __restrict__ src, int64_t sld,
+                                                        char* __restrict__ dst, int64_t dld, int bytes, int scatter) {
+  const int b = blockIdx.x;
+  const int64_t last = st.q_cu[b + 1] - 1;
+  copy_row16(dst + (scatter ? last : b) * dld, src + (scatter ? b : last) * sld, bytes);
+}
+
+hipError_t launch_copy_last_rows(hipStream_t s, const SeqTable& st, const void* src, int64_t src_ld, void* dst,
+                                 int64_t dst_ld, int32_t bytes, bool scatter) {
+  if ((bytes | src_ld | dst_ld) & 15) return hipErrorInvalidValue;
+  k_copy_last_rows<<<st.n, 256, 0, s>>>(st, (const char*)src, src_ld, (char*)dst, dst_ld, bytes, scatter ? 1 : 0);
+  return hipGetLastError();
 }
 
 hipError_t launch_gather_last(hipStream_t s, const SeqTable& st, const void* q, int32_t q_bytes, const void* k,

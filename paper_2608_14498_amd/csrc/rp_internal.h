@@ -96,12 +96,19 @@ struct MRope {
   const int32_t* pos;  // NULL: 1-D positions
   int32_t sec0, sec01;
 };
+// q_last_only: rotate and store the queries of each sequence's last row only (the other
+// rows' query columns are not read).
 hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* qkv, int32_t M,
                           int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
                           const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
-                          void* v_out, const MRope& mr);
+                          void* v_out, const MRope& mr, bool q_last_only = false);
 hipError_t launch_swiglu(hipStream_t s, rp_dtype dt, const void* gu, int32_t M, int32_t F, void* act);
 hipError_t launch_gather_rows(hipStream_t s, const SeqTable& st, const float* X, int32_t d, float* h_last);
+// Row copies between the packed rows and one row per sequence b (last(b) = q_cu[b+1]-1):
+// gather: dst row b = src row last(b); scatter: dst row last(b) = src row b.  Row strides
+// in bytes; bytes per row, strides and pointers 16-byte aligned.
+hipError_t launch_copy_last_rows(hipStream_t s, const SeqTable& st, const void* src, int64_t src_ld, void* dst,
+                                 int64_t dst_ld, int32_t bytes, bool scatter);
 // Last row r = q_cu[b+1]-1 of every sequence b: qs[b] = q[r] (q_bytes), ks[b] = k[r] and
 // vs[b] = v[r] (kv_bytes each), h[b] = X[r] (d floats).  Byte counts are multiples of 16.
 hipError_t launch_gather_last(hipStream_t s, const SeqTable& st, const void* q, int32_t q_bytes, const void* k,

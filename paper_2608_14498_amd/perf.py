@@ -20,16 +20,16 @@ def layer_gemm_flops_per_token(m) -> float:
 
 def prefix_flops(m, prefix_lens: Sequence[int], last_rows_only: bool = False) -> Dict[str, float]:
     """GEMM and attention flops of the prefix pass (all layers).  last_rows_only: the last
-    layer runs its q/k/v projection for every row, and attention (one query over P keys),
-    o-proj and MLP only for each sequence's last row."""
+    layer runs its k/v projection for every row, and the q projection, attention (one
+    query over P keys), o-proj and MLP only for each sequence's last row."""
     T = sum(prefix_lens)
     full = m.n_layers - (1 if last_rows_only else 0)
     gemm = full * T * layer_gemm_flops_per_token(m)
     # QK^T and PV over the causal half: 2 * (2 Hq Dh P(P+1)/2) per sequence per layer
     attn = full * sum(2.0 * m.n_q_heads * m.head_dim * P * (P + 1) for P in prefix_lens)
     if last_rows_only:
-        qkv = 2.0 * (m.n_q_heads + 2 * m.n_kv_heads) * m.head_dim * m.d_model
-        gemm += T * qkv + len(prefix_lens) * (layer_gemm_flops_per_token(m) - qkv)
+        kv = 2.0 * 2 * m.n_kv_heads * m.head_dim * m.d_model
+        gemm += T * kv + len(prefix_lens) * (layer_gemm_flops_per_token(m) - kv)
         attn += sum(4.0 * m.n_q_heads * m.head_dim * P for P in prefix_lens)
     return {"gemm": gemm, "attention": attn, "total": gemm + attn}
 
