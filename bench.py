@@ -473,14 +473,14 @@ def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, p
         rb.rp_profile_enable(False)
         kernels = {k: {"launches": n, "avg_ms": ms / max(n, 1), "ms_per_step": ms / args.profile_steps}
                    for k, (n, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1])}
-    prompt = None
+    prompt_res = None
     if prompt and not args.no_prompt_logprobs:
-        prompt = time_prompt_logprobs(dm, args, bt, cu_p, ids, vis, (K, V), h_last, ws_p, stream)
+        prompt_res = time_prompt_logprobs(dm, args, bt, cu_p, ids, vis, (K, V), h_last, ws_p, stream)
     dm.close()
     del K, V, ids, vis, resp, ws_p, ws_s
     torch.cuda.empty_cache()
     return dict(T=T, R=R, B=B, bt=bt, hw=hw, ms_step=ms_step, pre_ms=pre_ms, suf_ms=suf_ms, kernels=kernels,
-                prompt=prompt)
+                prompt=prompt_res)
 
 
 def time_prompt_logprobs(dm, args, bt, cu_p, ids, vis, kv, h_last, ws_p, stream):

@@ -385,3 +385,40 @@ def test_prefix_last_rows_only(model, mrope):
     assert e_h <= (1e-5 if f32 else 3e-2)
     assert e_lp <= (1e-4 if f32 else 2e-2)
     dm.close()
+
+
+@pytest.mark.parametrize("model", [configs.TINY, BF16_D64])
+def test_maximum_batch_of_256_sequences(model):
+    """RP_MAX_SEQS sequences in one call (the kernel-argument sequence table at capacity):
+    prefixes of 1..40 tokens, suffixes of 0..8, plus a shared-prefix call whose 256
+    responses read 32 of those prefixes."""
+    from paper_2608_14498_amd import binding as rb
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+    n = rb.RP_MAX_SEQS
+    P = [1 + (b * 7) % 40 for b in range(n)]
+    Vis = [p // 2 for p in P]
+    S = [b % 9 for b in range(n)]
+    w = configs.custom(model, P, Vis, S, index=89)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    got = gpu_run(w, hw, bt)
+    ref = oracle_run(w, hw, bt)
+    r = _report(f"{n} sequences {model.dtype}", *got, *ref)
+    f32 = model.dtype == "f32"
+    assert r["lp"] <= (1e-4 if f32 else 2e-2)
+    assert r["kv"] <= (1e-5 if f32 else 3e-2) and r["h"] <= (1e-5 if f32 else 3e-2)
+    # 256 responses over the first 32 prefixes (8 each), read through the grouped call
+    grp = [b // 8 for b in range(n)]
+    cp = [int(x) for x in bt.cu_prefix]
+    cs = [int(x) for x in bt.cu_suffix]
+    dm = DeviceModel(hw, max(P) + max(S) + 1)
+    dev = dm.device
+    K, V, h = dm.prefix(cp, to_device(bt.token_ids, dev), to_device(bt.visual, dev))
+    lp = dm.suffix_grouped(cp, grp, cs, K, V, h, to_device(bt.response_ids, dev)).cpu().numpy()
+    dm.close()
+    Ko, Vo, Ho = ref[0], ref[1], ref[2]
+    lpo = oracle.suffix_logprob_grouped(hw.as_f32(), model, bt.cu_prefix, grp, bt.cu_suffix, Ko, Vo, Ho,
+                                        bt.response_ids)
+    err = max_abs(lp, lpo)
+    print(f"[parity] {n} grouped responses {model.dtype}: |d lp| {err:.3g}", flush=True)
+    assert err <= (1e-4 if f32 else 2e-2)
