@@ -130,6 +130,28 @@ __device__ __forceinline__ void store4(float* row, int n0, int N, const float (&
   }
 }
 
+#ifndef RP_GEMM_NT_STORE
+#define RP_GEMM_NT_STORE 1
+#endif
+// 16-byte global store of the epilogue.  Outputs that no later step of the kernel reads
+// (16-bit stores, fp32 stores) are written non-temporally, so that they do not evict the
+// A/B slab lines the other workgroups of the XCD are still reading from L2; residual and
+// split-K outputs, re-read soon, are stored normally.
+template <bool NT>
+__device__ __forceinline__ void st_out16(void* p, uint4 v) {
+  if (NT && RP_GEMM_NT_STORE) {
+    typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
+    u4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, reinterpret_cast<u4_t*>(p));
+  } else {
+    *reinterpret_cast<uint4*>(p) = v;
+  }
+}
+template <bool NT>
+__device__ __forceinline__ void st_out16(float* p, float4 v) {
+  st_out16<NT>((void*)p, make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)));
+}
+
 // Epilogue of the bf16 kernels.  The MFMAs take the B fragment as their first operand,
 // so a lane holds rows of C^T: acc[i][j][e] = C(row i*32 + fr, col j*32 + 8(e/4) + 4 fk
 // + e%4) of the wave tile, i.e. four consecutive columns of one row per e/4.
@@ -278,7 +300,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&
       if (m >= g.M) continue;
       T16* dst = (T16*)g.C + (int64_t)m * g.ldc + n;
       if (vec && n + 7 < g.N) {
-        *reinterpret_cast<uint4*>(dst) = v;
+        st_out16<true>((void*)dst, v);
       } else {
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -345,7 +367,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&
             o.z += c[s].z;
             o.w += c[s].w;
           }
-          if (m < g.M) *reinterpret_cast<float4*>(out + (int64_t)m * ld + ncol0 + k * 4) = o;
+          if (m < g.M) st_out16<EPI == EPI_STORE_F32>(out + (int64_t)m * ld + ncol0 + k * 4, o);
         }
       }
       continue;
@@ -366,7 +388,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&
           o.z += c.z;
           o.w += c.w;
         }
-        *reinterpret_cast<float4*>(dst) = o;
+        st_out16<EPI == EPI_STORE_F32>(dst, o);
       } else {
         const float w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
