@@ -220,7 +220,7 @@ def measured_traffic(kernel_src: str, path: str):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen7b_b4_p4096_s256")
     ap.add_argument("--profile-steps", type=int, default=3)
@@ -237,6 +237,8 @@ def main():
                     help="skip timing the step with o_proj / down weights stored transposed")
     ap.add_argument("--no-last-rows-variant", action="store_true",
                     help="skip timing the prefix with RP_PREFIX_LAST_ROWS_ONLY")
+    ap.add_argument("--no-measured-peaks", action="store_true",
+                    help="skip the matrix-core probe and the device-copy bandwidth measurement")
     ap.add_argument("--no-prompt-logprobs", action="store_true",
                     help="skip timing the prompt-token log-probs (rp_prompt_logprob)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -324,6 +326,7 @@ def main():
         "prefix_mfma_frac": pf["total"] / (pre_ms * 1e-3) / peak,
         "suffix_tflops": sf["total"] / (suf_ms * 1e-3) / 1e12,
         "suffix_mfma_frac": sf["total"] / (suf_ms * 1e-3) / peak,
+        "step_ms": res["step_stats"],
         "roofline": roofline,
         "logsoftmax_roofline": k12,
         "prompt_logprobs": res["prompt"],
@@ -377,6 +380,13 @@ def main():
             "prefix_tflops": pfl["total"] / (rl["pre_ms"] * 1e-3) / 1e12,
             "prefix_mfma_frac": pfl["total"] / (rl["pre_ms"] * 1e-3) / peak,
             "kernels": {k: v for k, v in kl.items() if k.startswith("prefix.tail")}}
+    if not args.no_measured_peaks:
+        mp = measured_peaks()
+        out["measured_peaks"] = mp
+        if roofline and m.dtype == "bf16":
+            roofline["frac_of_measured_peak"] = roofline["achieved"] / mp["mfma_bf16_tflops"]
+        if k12:
+            k12["frac_of_measured_read"] = k12["achieved"] / mp["hbm_read_gbps"]
     if not args.no_cpu_baseline:
         log("CPU baseline: oracle on sequence 0")
         out["cpu_baseline"] = cpu_baseline(w, res["hw"], bt, args.cpu_prefix_len)
@@ -456,6 +466,8 @@ def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, p
     ms_step = total_ms / args.steps
     pre_ms = sorted(e[0].elapsed_time(e[1]) for e in evs)[args.steps // 2]
     suf_ms = sorted(e[1].elapsed_time(e[2]) for e in evs)[args.steps // 2]
+    st = sorted(e[0].elapsed_time(e[2]) for e in evs)
+    step_stats = {"median": st[len(st) // 2], "mean": sum(st) / len(st), "min": st[0]}
     if not np.all(np.isfinite(lp[:R].cpu().numpy())):
         raise RuntimeError("non-finite log-probs")
 
@@ -480,7 +492,47 @@ def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, p
     del K, V, ids, vis, resp, ws_p, ws_s
     torch.cuda.empty_cache()
     return dict(T=T, R=R, B=B, bt=bt, hw=hw, ms_step=ms_step, pre_ms=pre_ms, suf_ms=suf_ms, kernels=kernels,
+                step_stats=step_stats,
                 prompt=prompt_res)
+
+
+def measured_peaks():
+    """Matrix-core rate of the MFMA probe (random bf16 operands, two waves per SIMD, about
+    25 ms) and the HBM read bandwidth of a 4 GiB streaming read, on this GPU: the practical
+    ceilings beside the published peaks."""
+    import torch
+
+    from paper_2608_14498_amd import binding as rb
+
+    log("measured peaks: MFMA probe and HBM read probe")
+    stream = torch.cuda.current_stream()
+    cus = rb.rp_device_cu_count(0)
+    blocks = 2 * cus
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    rb.rp_calibrate_mfma(stream.cuda_stream, "bf16", blocks, 2000, sink, sink.numel() * 4)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    flops = rb.rp_calibrate_mfma(stream.cuda_stream, "bf16", blocks, 100000, sink, sink.numel() * 4)
+    b.record(stream)
+    torch.cuda.synchronize()
+    mfma = flops / (a.elapsed_time(b) * 1e-3) / 1e12
+    if not bool(torch.isfinite(sink).all()):
+        raise RuntimeError("MFMA probe produced non-finite sums")
+    n = 4 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    rblocks = 16 * cus
+    rsink = torch.empty(rblocks * 256, dtype=torch.int32, device="cuda")
+    rb.rp_calibrate_read(stream.cuda_stream, src, n, rblocks, rsink, rsink.numel() * 4)
+    a.record(stream)
+    for _ in range(3):
+        rb.rp_calibrate_read(stream.cuda_stream, src, n, rblocks, rsink, rsink.numel() * 4)
+    b.record(stream)
+    torch.cuda.synchronize()
+    read = 3.0 * n / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, rsink, sink
+    torch.cuda.empty_cache()
+    return {"mfma_bf16_tflops": mfma, "mfma_probe": f"{blocks} workgroups x 4 waves, 100000 x 8 MFMA 32x32x16 each",
+            "hbm_read_gbps": read, "read_probe": f"4 GiB streamed by {rblocks} workgroups, 16-byte loads"}
 
 
 def time_prompt_logprobs(dm, args, bt, cu_p, ids, vis, kv, h_last, ws_p, stream):

@@ -326,6 +326,24 @@ int32_t rp_profile_count(void);
 rp_status rp_profile_read(int32_t i, const char **name, int64_t *launches, double *total_ms);
 void rp_profile_reset(void);
 
+/* ---------------------------------------------------------------------------
+ * Matrix-core probe (measurement aid): launches blocks workgroups of 256
+ * threads on stream; every wave issues iters x 8 independent 32x32x16 MFMAs of
+ * dtype (RP_BF16 or RP_F16) on random register operands and writes one float
+ * per thread to sink (device, >= blocks*256*4 bytes, else RP_ERR_WORKSPACE).
+ * *flops (nullable) receives the launch's matrix flop count; the caller times
+ * the launch (e.g. with events on the same stream).  Asynchronous.
+ * ------------------------------------------------------------------------- */
+rp_status rp_calibrate_mfma(void *stream, rp_dtype dtype, int32_t blocks, int32_t iters, float *sink,
+                            size_t sink_bytes, double *flops);
+
+/* HBM read probe (measurement aid): blocks workgroups of 256 threads stream bytes
+ * (a positive multiple of 16) of device memory src once with 16-byte loads and
+ * write one word per thread to sink (>= blocks*256*4 bytes).  Asynchronous; the
+ * caller times it. */
+rp_status rp_calibrate_read(void *stream, const void *src, int64_t bytes, int32_t blocks, uint32_t *sink,
+                            size_t sink_bytes);
+
 const char *rp_last_error(void);
 const char *rp_status_string(rp_status status);
 const char *rp_version(void);

@@ -29,7 +29,7 @@ SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_fo
            "rp_suffix_logprob_grouped", "rp_prompt_logprob_workspace_bytes", "rp_prompt_logprob",
            "rp_decode_workspace_bytes",
            "rp_decode_step", "rp_stream_create_cu_masked", "rp_stream_destroy",
-           "rp_device_cu_count", "rp_last_error", "rp_status_string", "rp_version",
+           "rp_device_cu_count", "rp_calibrate_mfma", "rp_calibrate_read", "rp_last_error", "rp_status_string", "rp_version",
            "rp_profile_enable", "rp_profile_collect", "rp_profile_count", "rp_profile_read",
            "rp_profile_reset"]
 
@@ -97,6 +97,9 @@ def lib():
             "rp_prompt_logprob": (c_int, [c_void_p, c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p,
                                           c_int32, c_void_p, c_uint32, c_void_p, c_void_p, c_size_t]),
             "rp_decode_workspace_bytes": (c_int, [c_void_p, c_int32, c_int32, POINTER(c_size_t)]),
+            "rp_calibrate_mfma": (c_int, [c_void_p, c_int, c_int32, c_int32, c_void_p, c_size_t,
+                                          POINTER(c_double)]),
+            "rp_calibrate_read": (c_int, [c_void_p, c_void_p, c_int64, c_int32, c_void_p, c_size_t]),
             "rp_decode_step": (c_int, [c_void_p, c_void_p, c_int32, RpKV, c_int32, c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_size_t]),
             "rp_stream_create_cu_masked": (c_int, [c_int, POINTER(c_uint32), c_uint32, POINTER(c_void_p)]),
@@ -264,6 +267,19 @@ def rp_stream_create_cu_masked(device: int, mask_words: Sequence[int]) -> int:
 
 def rp_stream_destroy(stream: int) -> None:
     _check(lib().rp_stream_destroy(stream))
+
+
+def rp_calibrate_mfma(stream, dtype: str, blocks: int, iters: int, sink, sink_bytes: int) -> float:
+    """Launch the matrix-core probe; returns its flop count (time it on the same stream)."""
+    f = c_double()
+    _check(lib().rp_calibrate_mfma(_ptr(stream), _DTYPES[dtype], int(blocks), int(iters), _ptr(sink),
+                                   int(sink_bytes), byref(f)))
+    return f.value
+
+
+def rp_calibrate_read(stream, src, nbytes: int, blocks: int, sink, sink_bytes: int) -> None:
+    _check(lib().rp_calibrate_read(_ptr(stream), _ptr(src), int(nbytes), int(blocks), _ptr(sink),
+                                   int(sink_bytes)))
 
 
 def rp_device_cu_count(device: int = 0) -> int:

@@ -975,6 +975,31 @@ rp_status rp_stream_destroy(void* stream) {
   return RP_OK;
 }
 
+rp_status rp_calibrate_mfma(void* stream, rp_dtype dtype, int32_t blocks, int32_t iters, float* sink,
+                            size_t sink_bytes, double* flops) {
+  if (dtype != RP_BF16 && dtype != RP_F16) return fail(RP_ERR_INVALID_ARG, "dtype must be RP_BF16 or RP_F16");
+  if (blocks < 1 || iters < 1) return fail(RP_ERR_SHAPE, "blocks and iters must be >= 1");
+  if (!sink || !aligned16(sink)) return fail(RP_ERR_INVALID_ARG, "sink must be a 16-byte aligned device buffer");
+  if (sink_bytes < (size_t)blocks * 256 * 4)
+    return fail(RP_ERR_WORKSPACE, "sink holds %zu bytes, needs %zu", sink_bytes, (size_t)blocks * 256 * 4);
+  if (flops) *flops = (double)blocks * 4.0 * (double)iters * 8.0 * 32.0 * 32.0 * 16.0 * 2.0;
+  const hipError_t e = rp::launch_mfma_probe((hipStream_t)stream, dtype, blocks, iters, sink);
+  if (e != hipSuccess) return fail(RP_ERR_HIP, "mfma probe launch: %s", hipGetErrorString(e));
+  return RP_OK;
+}
+
+rp_status rp_calibrate_read(void* stream, const void* src, int64_t bytes, int32_t blocks, uint32_t* sink,
+                            size_t sink_bytes) {
+  if (!src || !sink || !aligned16(src) || !aligned16(sink))
+    return fail(RP_ERR_INVALID_ARG, "src and sink must be 16-byte aligned device buffers");
+  if (bytes < 16 || (bytes & 15) || blocks < 1) return fail(RP_ERR_SHAPE, "bytes must be a positive multiple of 16");
+  if (sink_bytes < (size_t)blocks * 256 * 4)
+    return fail(RP_ERR_WORKSPACE, "sink holds %zu bytes, needs %zu", sink_bytes, (size_t)blocks * 256 * 4);
+  const hipError_t e = rp::launch_read_probe((hipStream_t)stream, src, bytes, blocks, sink);
+  if (e != hipSuccess) return fail(RP_ERR_HIP, "read probe launch: %s", hipGetErrorString(e));
+  return RP_OK;
+}
+
 int rp_device_cu_count(int device) {
   int n = 0;
   if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) return -1;

@@ -157,6 +157,12 @@ struct AttnArgs {
 hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, const AttnArgs& a,
                             int32_t total_q);
 
+// Matrix-core probe: blocks x 256 threads, each wave iters x 8 MFMAs of 32x32x16;
+// sink receives blocks * 256 floats.
+hipError_t launch_mfma_probe(hipStream_t s, rp_dtype dt, int32_t blocks, int32_t iters, float* sink);
+// HBM read probe over bytes (a multiple of 16) of src; sink receives blocks * 256 words.
+hipError_t launch_read_probe(hipStream_t s, const void* src, int64_t bytes, int32_t blocks, uint32_t* sink);
+
 // Decode step pieces.
 hipError_t launch_decode_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const void* embed,
                                int32_t vocab, int32_t B, int32_t d, float* X);

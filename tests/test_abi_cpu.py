@@ -217,6 +217,16 @@ def test_prefix_flags_validation(lib):
         rb.rp_destroy(h)
 
 
+def test_mfma_probe_validation(lib):
+    assert status_of(rb.rp_calibrate_mfma, None, "f32", 1, 1, FAKE, 1 << 20)[0] == rb.RP_ERR_INVALID_ARG
+    assert status_of(rb.rp_calibrate_mfma, None, "bf16", 0, 1, FAKE, 1 << 20)[0] == rb.RP_ERR_SHAPE
+    assert status_of(rb.rp_calibrate_mfma, None, "bf16", 4, 1, FAKE, 4 * 256 * 4 - 1)[0] == rb.RP_ERR_WORKSPACE
+    assert status_of(rb.rp_calibrate_mfma, None, "bf16", 4, 1, FAKE + 4, 1 << 20)[0] == rb.RP_ERR_INVALID_ARG
+    assert status_of(rb.rp_calibrate_read, None, FAKE, 100, 4, FAKE, 1 << 20)[0] == rb.RP_ERR_SHAPE
+    assert status_of(rb.rp_calibrate_read, None, FAKE, 1 << 20, 4, FAKE, 100)[0] == rb.RP_ERR_WORKSPACE
+    assert status_of(rb.rp_calibrate_read, None, None, 1 << 20, 4, FAKE, 1 << 20)[0] == rb.RP_ERR_INVALID_ARG
+
+
 def test_fused_scoring_workspace_holds_partials_not_logits(lib):
     h, keep = make(configs.QWEN7B_SLICE, max_pos=8192)
     try:
