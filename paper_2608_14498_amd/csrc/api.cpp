@@ -228,7 +228,7 @@ int decode_splitk(const rp_config& cfg, int32_t M, int32_t N, int32_t K) {
   const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
   int s = (512 + tiles - 1) / tiles;
   s = s < 1 ? 1 : s;
-  s = s > 8 ? 8 : s;
+  s = s > 16 ? 16 : s;
   const int kb = K / 64;
   return s > kb ? kb : s;
 }

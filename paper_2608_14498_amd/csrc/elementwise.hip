@@ -225,33 +225,45 @@ __device__ __forceinline__ void rope_row(const float* __restrict__ row, const in
     cs[64 + i] = s;
   }
   __syncthreads();
-  const int nq = do_q ? Hq * half : 0, nk = Hkv * half;
+  // four consecutive rotary pairs (i .. i+3) per thread: 16-byte loads of x1 and x2 and
+  // 4-wide stores (D/2 is a multiple of 4; rows start 16-byte aligned)
+  const int quads = half >> 2;
+  const int nq = do_q ? Hq * quads : 0, nk = Hkv * quads;
   for (int p = threadIdx.x; p < nq + nk; p += blockDim.x) {
     const bool isq = p < nq;
     const int pp = isq ? p : p - nq;
-    const int h = pp / half, i = pp - h * half;
+    const int h = pp / quads, i = (pp - h * quads) * 4;
     const int col = (isq ? 0 : Hq * D) + h * D + i;
-    float x1 = row[col], x2 = row[col + half];
+    float x1[4], x2[4], y1[4], y2[4];
+    load4(row + col, x1);
+    load4(row + col + half, x2);
     const T* b = isq ? bq : bk;
     if (b) {
-      x1 += ldf(b + h * D + i);
-      x2 += ldf(b + h * D + i + half);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        x1[u] += ldf(b + h * D + i + u);
+        x2[u] += ldf(b + h * D + i + half + u);
+      }
     }
-    const float c = cs[i], s = cs[64 + i];
-    const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
-    if (isq) {
-      stf(q_dst + h * D + i, y1);
-      stf(q_dst + h * D + i + half, y2);
-    } else {
-      stf(k_dst + h * D + i, y1);
-      stf(k_dst + h * D + i + half, y2);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float c = cs[i + u], s = cs[64 + i + u];
+      y1[u] = x1[u] * c - x2[u] * s;
+      y2[u] = x2[u] * c + x1[u] * s;
     }
+    T* dst = (isq ? q_dst : k_dst) + h * D + i;
+    store4(dst, y1);
+    store4(dst + half, y2);
   }
   const int vbase = (Hq + Hkv) * D;
-  for (int e = threadIdx.x; e < Hkv * D; e += blockDim.x) {
-    float v = row[vbase + e];
-    if (bv) v += ldf(bv + e);
-    stf(v_dst + e, v);
+  for (int e = threadIdx.x * 4; e < Hkv * D; e += blockDim.x * 4) {
+    float v[4];
+    load4(row + vbase + e, v);
+    if (bv) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] += ldf(bv + e + u);
+    }
+    store4(v_dst + e, v);
   }
 }
 
