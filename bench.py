@@ -46,12 +46,21 @@ def cpu_baseline(w, hw, bt, prefix_len: int):
     t1 = time.perf_counter()
     oracle.suffix_logprob_one(W, w.model, K, V, h, resp)
     t2 = time.perf_counter()
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    pools = threadpool_info()
+    threads = max([p.get("num_threads", 1) for p in pools] or [1])
+    blas = ", ".join(sorted({f"{p.get('internal_api')} {p.get('version')}" for p in pools if p.get("user_api") == "blas"}))
+    cpu = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     n_tok = P + len(resp)
     return {"value": n_tok / (t2 - t0), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"sequence 0 of the workload: prefix {P} + suffix {len(resp)} tokens, all "
                       f"{w.model.n_layers} layers, float64 numpy oracle; prefix {t1 - t0:.1f} s, "
-                      f"suffix {t2 - t1:.1f} s"}
+                      f"suffix {t2 - t1:.1f} s",
+            "prefix_s": t1 - t0, "suffix_s": t2 - t1, "cpu_model": cpu, "numpy": np.__version__, "blas": blas}
 
 
 def colocation(args, w):
@@ -204,9 +213,9 @@ def colocation(args, w):
     print(json.dumps(out), flush=True)
 
 
-def measured_traffic(kernel_src: str, path: str):
-    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter runs,
-    or None when the kernel source has changed since those counters were taken."""
+def measured_traffic(kernel_src: str, path: str, sha_key: str = "gemm_source_sha1"):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 counter runs, or None
+    when the kernel source has changed since those counters were taken."""
     import hashlib
 
     try:
@@ -214,7 +223,7 @@ def measured_traffic(kernel_src: str, path: str):
         cur = hashlib.sha1(open(os.path.join(ROOT, kernel_src), "rb").read()).hexdigest()
     except (OSError, ValueError):
         return None
-    return rec["traffic_bytes_per_launch"] if rec.get("gemm_source_sha1") == cur else None
+    return rec["traffic_bytes_per_launch"] if rec.get(sha_key) == cur else None
 
 
 def main():
@@ -297,7 +306,12 @@ def main():
     if ls:
         gbs = perf.logsoftmax_bytes(R, m.vocab) / (ls["avg_ms"] * 1e-3) / 1e9
         k12 = {"bound": "hbm", "achieved": gbs, "peak": perf.PEAK_HBM_BPS / 1e9, "unit": "GB/s",
-               "frac": gbs / (perf.PEAK_HBM_BPS / 1e9)}
+               "frac": gbs / (perf.PEAK_HBM_BPS / 1e9), "algorithmic_bytes_per_launch": perf.logsoftmax_bytes(R, m.vocab),
+               "traffic": None}
+        if w.name == "qwen7b_b4_p4096_s256" and m.dtype == "bf16":
+            k12["traffic"] = measured_traffic("paper_2608_14498_amd/csrc/elementwise.hip",
+                                              "profiles/logsoftmax_gather_qwen7b_b4_p4096_s256_traffic.json",
+                                              "elementwise_source_sha1")
 
     out = {
         "metric": "prefix prefill tokens/s + suffix logprob tokens/s; % bf16 MFMA peak",
