@@ -555,12 +555,21 @@ __global__ __launch_bounds__(1024) void k_argmax(const float* __restrict__ logit
   int bi = 0x7fffffff;
   if ((V & 3) == 0) {
     const f32x4_t* row4 = reinterpret_cast<const f32x4_t*>(row);
-    for (int i = threadIdx.x; i < V / 4; i += blockDim.x) {  // i increases: strict > keeps the lowest index
+    const int n4 = V / 4, bd = blockDim.x;
+    int i = threadIdx.x;
+    for (; i + 3 * bd < n4; i += 4 * bd) {  // four independent loads in flight per thread
+      f32x4_t x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = row4[i + u * bd];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) argmax_merge(best, bi, x[u][c], 4 * (i + u * bd) + c);
+    }
+    for (; i < n4; i += bd) {
       const f32x4_t x = row4[i];
-      argmax_merge(best, bi, x[0], 4 * i);
-      argmax_merge(best, bi, x[1], 4 * i + 1);
-      argmax_merge(best, bi, x[2], 4 * i + 2);
-      argmax_merge(best, bi, x[3], 4 * i + 3);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) argmax_merge(best, bi, x[c], 4 * i + c);
     }
   } else {
     for (int i = threadIdx.x; i < V; i += blockDim.x) argmax_merge(best, bi, row[i], i);
