@@ -390,12 +390,17 @@ size_t decode_ws(const rp_model* m, int32_t B, int32_t cap, void* base, DecodeWS
   s->attn_part = (float*)c.take(rp::decode_attn_partial_floats(B, cfg.n_q_heads, cfg.head_dim, cap) * 4);
   const int64_t d = cfg.d_model, F = cfg.ffn_dim, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
   const int64_t hq = (int64_t)cfg.n_q_heads * cfg.head_dim;
+  // the layer GEMMs write split-K partials (one split included) that the next kernel sums
   size_t need = 0;
   const int64_t shapes[4][2] = {{qkv, d}, {d, hq}, {2 * F, d}, {d, F}};
   for (auto& sh : shapes) {
-    size_t f = rp::gemm_partial_floats(B, (int32_t)sh[0], decode_splitk(cfg, B, (int32_t)sh[0], (int32_t)sh[1]));
+    const int32_t sk = rp::gemm_effective_splitk(cfg.dtype, (int32_t)sh[1],
+                                                 decode_splitk(cfg, B, (int32_t)sh[0], (int32_t)sh[1]));
+    const size_t f = (size_t)sk * B * sh[0];
     need = f > need ? f : need;
   }
+  const size_t lm = rp::gemm_partial_floats(B, cfg.vocab, decode_splitk(cfg, B, cfg.vocab, (int32_t)d));
+  need = lm > need ? lm : need;
   s->gemm_part = (float*)c.take(need * 4);
   return c.off + 256;
 }
@@ -846,6 +851,8 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
   rp_status st = check_kv(m, cache, (int64_t)B * cap, "cache");
   if (st != RP_OK) return st;
   if (!kv_len || !token_ids || !next_ids) return fail(RP_ERR_INVALID_ARG, "kv_len, token_ids and next_ids are required");
+  if ((int64_t)(m->cfg.n_q_heads + 2 * m->cfg.n_kv_heads) * m->cfg.head_dim * 4 > 65536)
+    return fail(RP_ERR_UNSUPPORTED, "decode step: a q/k/v row must fit 64 KiB of LDS");
   const size_t need = decode_ws(m, B, cap, nullptr, nullptr);
   if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
 
@@ -858,32 +865,47 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
   const float scale = (float)(1.0 / sqrt((double)D));
-  RP_TRY_LAUNCH_N("decode.embed", rp::launch_decode_embed(s, dt, token_ids, m->embed, c.vocab, B, d, w.L.X));
+  // Each layer GEMM writes split-K partials (EPI_PARTIALS) and the kernel that consumes
+  // its output sums them: RoPE + cache write, residual add + the next RMSNorm, SwiGLU.
+  // The last layer's down projection is followed by the final norm the same way.
+  RP_TRY_LAUNCH_N("decode.embed_norm", rp::launch_decode_embed_norm(s, dt, token_ids, m->embed, c.vocab, B, d, w.L.X,
+                                                                    m->layers[0].attn_norm, c.rms_eps, w.L.N));
   for (int l = 0; l < c.n_layers; ++l) {
     const rp_layer_weights& lw = m->layers[l];
     void* kl = layer_ptr(m, cache.k, cache.layer_stride, l);
     void* vl = layer_ptr(m, cache.v, cache.layer_stride, l);
-    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, dt, w.L.X, lw.attn_norm, c.rms_eps, B, d, w.L.N));
+    const void* next_norm = l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : m->final_norm;
     rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
-    RP_TRY_LAUNCH_N("decode.gemm_qkv", rp::launch_gemm(s, dt, B, qkv, d, w.L.N, d, bqkv, d, w.L.QKV, qkv, rp::EPI_STORE_F32,
-                                  decode_splitk(c, B, qkv, d), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode.rope_kv", rp::launch_decode_rope_kv(s, dt, w.L.QKV, B, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, kv_len, cap,
-                                            c.max_position, w.L.Q, kl, vl));
+    const int s_qkv = decode_splitk(c, B, qkv, d);
+    RP_TRY_LAUNCH_N("decode.gemm_qkv", rp::launch_gemm(s, dt, B, qkv, d, w.L.N, d, bqkv, d, nullptr, qkv,
+                                                       rp::EPI_PARTIALS, s_qkv, w.gemm_part));
+    RP_TRY_LAUNCH_N("decode.rope_kv", rp::launch_decode_rope_kv_splitk(s, dt, w.gemm_part,
+                                                                       rp::gemm_effective_splitk(dt, d, s_qkv), B, Hq,
+                                                                       Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, kv_len,
+                                                                       cap, c.max_position, w.L.Q, kl, vl));
     RP_TRY_LAUNCH_N("decode.attention", rp::launch_decode_attention(s, dt, w.L.Q, hq, kl, vl, kv_len, cap, c.max_position, B, Hq, Hkv,
                                               D, scale, w.attn_part, w.L.O));
     const rp::BSeg bo = wo_operand(c, lw);
-    RP_TRY_LAUNCH_N("decode.gemm_o_proj", rp::launch_gemm(s, dt, B, d, hq, w.L.O, hq, bo, bo.trans ? d : hq, w.L.X, d,
-                                                          rp::EPI_ADD_F32, decode_splitk(c, B, d, hq), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode.rmsnorm", rp::launch_rmsnorm(s, dt, w.L.X, lw.mlp_norm, c.rms_eps, B, d, w.L.N));
+    const int s_o = decode_splitk(c, B, d, hq);
+    RP_TRY_LAUNCH_N("decode.gemm_o_proj", rp::launch_gemm(s, dt, B, d, hq, w.L.O, hq, bo, bo.trans ? d : hq, nullptr,
+                                                          d, rp::EPI_PARTIALS, s_o, w.gemm_part));
+    RP_TRY_LAUNCH_N("decode.add_rmsnorm", rp::launch_splitk_add_rmsnorm(s, dt, w.gemm_part,
+                                                                        rp::gemm_effective_splitk(dt, hq, s_o), B, d,
+                                                                        w.L.X, lw.mlp_norm, c.rms_eps, w.L.N));
     rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
-    RP_TRY_LAUNCH_N("decode.gemm_gate_up", rp::launch_gemm(s, dt, B, 2 * F, d, w.L.N, d, bgu, d, w.L.GU, 2 * F, rp::EPI_STORE,
-                                  decode_splitk(c, B, 2 * F, d), w.gemm_part));
-    RP_TRY_LAUNCH_N("decode.swiglu", rp::launch_swiglu(s, dt, w.L.GU, B, F, w.L.ACT));
+    const int s_gu = decode_splitk(c, B, 2 * F, d);
+    RP_TRY_LAUNCH_N("decode.gemm_gate_up", rp::launch_gemm(s, dt, B, 2 * F, d, w.L.N, d, bgu, d, nullptr, 2 * F,
+                                                           rp::EPI_PARTIALS, s_gu, w.gemm_part));
+    RP_TRY_LAUNCH_N("decode.swiglu", rp::launch_splitk_swiglu(s, dt, w.gemm_part, rp::gemm_effective_splitk(dt, d, s_gu),
+                                                              B, F, w.L.ACT));
     const rp::BSeg bd = w_down_operand(c, lw);
-    RP_TRY_LAUNCH_N("decode.gemm_down", rp::launch_gemm(s, dt, B, d, F, w.L.ACT, F, bd, bd.trans ? d : F, w.L.X, d,
-                                                        rp::EPI_ADD_F32, decode_splitk(c, B, d, F), w.gemm_part));
+    const int s_down = decode_splitk(c, B, d, F);
+    RP_TRY_LAUNCH_N("decode.gemm_down", rp::launch_gemm(s, dt, B, d, F, w.L.ACT, F, bd, bd.trans ? d : F, nullptr, d,
+                                                        rp::EPI_PARTIALS, s_down, w.gemm_part));
+    RP_TRY_LAUNCH_N("decode.add_rmsnorm", rp::launch_splitk_add_rmsnorm(s, dt, w.gemm_part,
+                                                                        rp::gemm_effective_splitk(dt, F, s_down), B, d,
+                                                                        w.L.X, next_norm, c.rms_eps, w.L.N));
   }
-  RP_TRY_LAUNCH_N("decode.final_norm", rp::launch_rmsnorm(s, dt, w.L.X, m->final_norm, c.rms_eps, B, d, w.L.N));
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
   RP_TRY_LAUNCH_N("decode.gemm_lm_head", rp::launch_gemm(s, dt, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
                                 decode_splitk(c, B, c.vocab, d), w.gemm_part));

@@ -599,4 +599,163 @@ hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------------
+// Decode-step kernels that fold a split-K reduction (partials [splitk][M][N] fp32, summed
+// in split order as k_splitk_reduce does) into the next step, saving a launch and a
+// round trip of the reduced rows.
+// ------------------------------------------------------------------------------------
+// Sum over z < splitk of part[z*zstride + 0..3], four splits in flight (the rows come from
+// few workgroups, so each thread keeps several loads outstanding).
+__device__ __forceinline__ void splitk_sum4(const float* __restrict__ part, int64_t zstride, int splitk, float* a) {
+  float b[4][4] = {};
+  int z = 0;
+  for (; z + 4 <= splitk; z += 4) {
+    float p[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) load4(part + (int64_t)(z + u) * zstride, p[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) b[u][e] += p[u][e];
+  }
+  for (; z < splitk; ++z) {
+    float p[4];
+    load4(part + (int64_t)z * zstride, p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) b[0][e] += p[e];
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) a[e] = (b[0][e] + b[1][e]) + (b[2][e] + b[3][e]);
+}
+
+// X[m] += sum_z part[z][m]; out[m] = RMSNorm(X[m]) * w (one block of 1024 per row).
+template <typename T>
+__global__ __launch_bounds__(1024) void k_splitk_add_rmsnorm(const float* __restrict__ part, int splitk, int M,
+                                                            int d, float* __restrict__ X, const T* __restrict__ w,
+                                                            float eps, T* __restrict__ out) {
+  __shared__ float red[16];
+  const int m = blockIdx.x;
+  float* x = X + (int64_t)m * d;
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    float a[4], v[4];
+    splitk_sum4(part + (int64_t)m * d + c, (int64_t)M * d, splitk, a);
+    load4(x + c, v);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] += a[u];
+    store4(x + c, v);
+  }
+  __syncthreads();  // the row is re-read below with another thread mapping
+  rmsnorm_row(x, w, eps, d, out + (int64_t)m * d, red);
+}
+
+hipError_t launch_splitk_add_rmsnorm(hipStream_t s, rp_dtype dt, const float* part, int32_t splitk, int32_t M,
+                                     int32_t d, float* X, const void* w, float eps, void* out) {
+  if (M <= 0) return hipSuccess;
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_splitk_add_rmsnorm<E><<<M, 1024, 0, s>>>(part, splitk, M, d, X, (const E*)w, eps, (E*)out);
+  });
+  return hipGetLastError();
+}
+
+// act[m][f] = silu(g) * u with g, u the split-K sums of columns f and F + f of [M][2F].
+template <typename T>
+__global__ __launch_bounds__(256) void k_splitk_swiglu(const float* __restrict__ part, int splitk, int M, int F,
+                                                       T* __restrict__ act) {
+  const int64_t per_row = F / 4;
+  const int64_t n = (int64_t)M * per_row;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t m = i / per_row;
+    const int f = (int)(i - m * per_row) * 4;
+    float g[4], u[4], o[4];
+    const float* row = part + m * 2 * F;
+    splitk_sum4(row + f, (int64_t)M * 2 * F, splitk, g);
+    splitk_sum4(row + F + f, (int64_t)M * 2 * F, splitk, u);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = g[e] / (1.0f + expf(-g[e])) * u[e];
+    store4(act + m * F + f, o);
+  }
+}
+
+hipError_t launch_splitk_swiglu(hipStream_t s, rp_dtype dt, const float* part, int32_t splitk, int32_t M, int32_t F,
+                                void* act) {
+  if (M <= 0) return hipSuccess;
+  const int64_t n = (int64_t)M * (F / 4);
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 256 * 16);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_splitk_swiglu<E><<<blocks, 256, 0, s>>>(part, splitk, M, F, (E*)act);
+  });
+  return hipGetLastError();
+}
+
+// Decode RoPE + cache write from the split-K partials of the q/k/v projection: the row is
+// summed into LDS (dynamic, qkv floats), then rotated as k_decode_rope_kv does.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_decode_rope_kv_splitk(const float* __restrict__ part, int splitk, int Hq,
+                                                               int Hkv, int D, const T* __restrict__ bq,
+                                                               const T* __restrict__ bk, const T* __restrict__ bv,
+                                                               RopeFreq rf, const int32_t* __restrict__ kv_len,
+                                                               int cap, int max_pos, int B, T* __restrict__ q_out,
+                                                               T* __restrict__ ck, T* __restrict__ cv) {
+  extern __shared__ float4 rowsh4[];
+  float* row = reinterpret_cast<float*>(rowsh4);
+  __shared__ float cs[128];
+  const int b = blockIdx.x;
+  const int ld = (Hq + 2 * Hkv) * D;
+  for (int c = threadIdx.x * 4; c < ld; c += blockDim.x * 4) {
+    float a[4];
+    splitk_sum4(part + (int64_t)b * ld + c, (int64_t)B * ld, splitk, a);
+    *reinterpret_cast<float4*>(row + c) = make_float4(a[0], a[1], a[2], a[3]);
+  }
+  __syncthreads();
+  const int slot = min(max(kv_len[b], 0), min(cap, max_pos) - 1);
+  const int64_t dst = ((int64_t)b * cap + slot) * Hkv * D;
+  const int p3[3] = {slot, slot, slot};
+  rope_row<T>(row, p3, D, D, Hq, Hkv, D, bq, bk, bv, rf, q_out + (int64_t)b * Hq * D, ck + dst, cv + dst, cs);
+}
+
+hipError_t launch_decode_rope_kv_splitk(hipStream_t s, rp_dtype dt, const float* part, int32_t splitk, int32_t B,
+                                        int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
+                                        const void* bv, const RopeFreq& rf, const int32_t* kv_len, int32_t cap,
+                                        int32_t max_pos, void* q_out, void* cache_k, void* cache_v) {
+  if (B <= 0) return hipSuccess;
+  const size_t lds = (size_t)(Hq + 2 * Hkv) * D * sizeof(float);
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_decode_rope_kv_splitk<E><<<B, 1024, lds, s>>>(part, splitk, Hq, Hkv, D, (const E*)bq, (const E*)bk,
+                                                   (const E*)bv, rf, kv_len, cap, max_pos, B, (E*)q_out,
+                                                   (E*)cache_k, (E*)cache_v);
+  });
+  return hipGetLastError();
+}
+
+// Decode embedding + the first layer's RMSNorm (one block per sequence).
+template <typename T>
+__global__ __launch_bounds__(256) void k_decode_embed_norm(const int32_t* __restrict__ ids,
+                                                           const T* __restrict__ embed, int vocab, int d,
+                                                           float* __restrict__ X, const T* __restrict__ w,
+                                                           float eps, T* __restrict__ out) {
+  __shared__ float red[16];
+  const int b = blockIdx.x;
+  const T* src = embed + (int64_t)min(max(ids[b], 0), vocab - 1) * d;
+  float* x = X + (int64_t)b * d;
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8];
+    load8(src + c, v);
+    store8(x + c, v);
+  }
+  __syncthreads();
+  rmsnorm_row(x, w, eps, d, out + (int64_t)b * d, red);
+}
+
+hipError_t launch_decode_embed_norm(hipStream_t s, rp_dtype dt, const int32_t* ids, const void* embed, int32_t vocab,
+                                    int32_t B, int32_t d, float* X, const void* w, float eps, void* out) {
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_decode_embed_norm<E><<<B, 256, 0, s>>>(ids, (const E*)embed, vocab, d, X, (const E*)w, eps, (E*)out);
+  });
+  return hipGetLastError();
+}
+
 }  // namespace rp

@@ -884,6 +884,15 @@ static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, b
     k_gemm_bf16<EPI, T16, 4, BT><<<grid, 512, 0, s>>>(g);
 }
 
+int32_t gemm_effective_splitk(rp_dtype dt, int32_t K, int32_t splitk) {
+  const int bk = dt != RP_F32 ? GB_K : GF_K;
+  const int kblocks = (K + bk - 1) / bk;
+  if (splitk < 1) splitk = 1;
+  if (splitk > kblocks) splitk = kblocks;
+  const int k_chunk = ((kblocks + splitk - 1) / splitk) * bk;
+  return (K + k_chunk - 1) / k_chunk;
+}
+
 hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
                        int32_t splitk, float* partials, const LseOut* lse) {
@@ -891,8 +900,9 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
   const bool half = dt != RP_F32;
   if (epi == EPI_SWIGLU && (!half || splitk > 1)) return hipErrorInvalidValue;
   if (epi == EPI_LSE && (!half || splitk > 1 || !lse)) return hipErrorInvalidValue;
+  if (epi == EPI_PARTIALS && !partials) return hipErrorInvalidValue;
   // a transposed B serves the row-parallel projections: residual or split-K epilogue
-  if (B.trans && ((epi != EPI_ADD_F32 && splitk <= 1) || ldb < N ||
+  if (B.trans && ((epi != EPI_ADD_F32 && epi != EPI_PARTIALS && splitk <= 1) || ldb < N ||
                   (half && ((N & 7) || (ldb & 7) || ((uintptr_t)B.b0 & 15)))))
     return hipErrorInvalidValue;
   GemmArgs g;
@@ -914,7 +924,8 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
   if (splitk > kblocks) splitk = kblocks;
   g.k_chunk = ((kblocks + splitk - 1) / splitk) * bk;
   splitk = (K + g.k_chunk - 1) / g.k_chunk;
-  const bool split = splitk > 1;
+  // EPI_PARTIALS: the partials epilogue even for one split, and no reduction here
+  const bool split = splitk > 1 || epi == EPI_PARTIALS;
   if (half) {
     g.tiles_m = (M + GB_M - 1) / GB_M;
     g.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB_N - 1) / GB_N;
@@ -955,7 +966,7 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
       k_gemm_f32<EPI_STORE_F32><<<grid, 256, 0, s>>>(g);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !split) return e;
+  if (e != hipSuccess || !split || epi == EPI_PARTIALS) return e;
   const int64_t total = (int64_t)M * N;
   const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
   if (epi == EPI_STORE && dt == RP_BF16)

@@ -48,7 +48,10 @@ enum Epi : int {
   EPI_ADD_F32 = 2,    // C[f32] += acc  (residual stream)
   EPI_SWIGLU = 3,     // C[T][m, f] = silu(gate) * up; B = {gate rows, up rows}, N = ffn features
   EPI_LSE = 4,        // no C: per-row log-sum-exp partials and the target logit (LseOut)
+  EPI_PARTIALS = 5,   // split-K partials [splitk][M][N] only (also for splitk 1); the caller reduces
 };
+// Number of K splits launch_gemm actually uses for a requested splitk.
+int32_t gemm_effective_splitk(rp_dtype dt, int32_t K, int32_t splitk);
 
 // Outputs of the EPI_LSE epilogue (an lm_head GEMM whose logits are never stored):
 // lse[m * n_part + p] = (max, sum of 2^(x log2 e - max)) over column block p of row m, in
@@ -171,6 +174,21 @@ hipError_t launch_decode_rope_kv(hipStream_t s, rp_dtype dt, const float* qkv, i
                                  const RopeFreq& rf, const int32_t* kv_len, int32_t cap, int32_t max_pos,
                                  void* q_out, void* cache_k, void* cache_v);
 size_t decode_attn_partial_floats(int32_t B, int32_t Hq, int32_t D, int32_t cap);
+// Decode kernels that consume split-K partials part[splitk][M][N] (EPI_PARTIALS):
+// X[m] += sum; out[m] = RMSNorm(X[m]) * w.
+hipError_t launch_splitk_add_rmsnorm(hipStream_t s, rp_dtype dt, const float* part, int32_t splitk, int32_t M,
+                                     int32_t d, float* X, const void* w, float eps, void* out);
+// act[m][f] = silu(sum of column f) * (sum of column F + f), N = 2F.
+hipError_t launch_splitk_swiglu(hipStream_t s, rp_dtype dt, const float* part, int32_t splitk, int32_t M, int32_t F,
+                                void* act);
+// launch_decode_rope_kv on the summed q/k/v projection rows.
+hipError_t launch_decode_rope_kv_splitk(hipStream_t s, rp_dtype dt, const float* part, int32_t splitk, int32_t B,
+                                        int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
+                                        const void* bv, const RopeFreq& rf, const int32_t* kv_len, int32_t cap,
+                                        int32_t max_pos, void* q_out, void* cache_k, void* cache_v);
+// X[b] = E[ids[b]] (clamped); out[b] = RMSNorm(X[b]) * w.
+hipError_t launch_decode_embed_norm(hipStream_t s, rp_dtype dt, const int32_t* ids, const void* embed, int32_t vocab,
+                                    int32_t B, int32_t d, float* X, const void* w, float eps, void* out);
 hipError_t launch_decode_attention(hipStream_t s, rp_dtype dt, const void* q, int32_t q_ld,
                                    const void* cache_k, const void* cache_v, const int32_t* kv_len,
                                    int32_t cap, int32_t max_pos, int32_t B, int32_t Hq, int32_t Hkv,
