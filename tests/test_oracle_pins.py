@@ -99,6 +99,17 @@ def test_zero_lm_head_gives_uniform():
     assert abs(-math.log(2048) - (-7.6246189861593985)) < 1e-15
 
 
+def test_scored_distribution_sums_to_one():
+    # scoring every vocabulary id from the same boundary state gives a distribution
+    w, W, bt = _setup(P=(9,), Vis=(4,), S=(1,))
+    ids, vis, _ = _seq(bt, 0)
+    _, _, h, _ = oracle.prefix_forward_one(W, SMALL, ids, vis)
+    z = np.repeat(np.asarray(h)[None, :], SMALL.vocab, axis=0)
+    lp = oracle.score_rows(W, SMALL, z, np.arange(SMALL.vocab))
+    assert abs(np.exp(lp).sum() - 1.0) < 1e-12
+    assert np.all(lp < 0)
+
+
 def test_identity_layers_reduce_to_log_softmax():
     """Wo = Wd = 0 make every layer the identity on the residual stream."""
     w, W, bt = _setup(P=(9,), Vis=(4,), S=(6,))
