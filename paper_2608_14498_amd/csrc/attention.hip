@@ -123,19 +123,19 @@ template <int D>
 __device__ __forceinline__ int kswz(int key) { return D == 128 ? (key & 15) : (key & 7); }
 __device__ __forceinline__ int vswz(int key) { return (key & 3) << 1; }
 
-template <typename T16, int D, int QW, int KT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QW == 1 ? 2 : 1, QW == 1 ? 2 : 1)))
+template <typename T16, int D, int QW, int KT, int NW = 4>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(QW == 1 ? 2 : 1, QW == 1 ? 2 : 1)))
 void k_attn_bf16(SeqTable st, AttnArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
   typedef Half16<T16> H;
   typedef typename H::V8 V8;
-  constexpr int BQ = 4 * 32 * QW;
+  constexpr int BQ = NW * 32 * QW;
   constexpr int CH = D / 8;               // 16-byte chunks per K/V row
   constexpr int KSTEPS = D / 16;          // MFMA k-steps of S^T (over Dh)
   constexpr int DB = D / 32;              // 32-row blocks of O^T
   constexpr int KB = KT / 32;             // 32-key blocks per tile
-  constexpr int LOADS = (KT * CH) / 256;  // load instructions per wave per matrix
-  static_assert(LOADS >= 1 && (KT * CH) % 256 == 0 && 64 % CH == 0, "tile loader");
+  constexpr int LOADS = (KT * CH) / (NW * 64);  // load instructions per wave per matrix
+  static_assert(LOADS >= 1 && (KT * CH) % (NW * 64) == 0 && 64 % CH == 0, "tile loader");
   __shared__ u32x4_t Ks0[KT * CH], Ks1[KT * CH], Vs0[KT * CH], Vs1[KT * CH];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -468,11 +468,25 @@ hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, cons
     }
     with_half16(dt, [&](auto tag_) {
       using H = decltype(tag_);
-      const int grid = fa_grid(fa_map(a.Hq, a.Hkv), count_qblocks(st, 128), a.Hq);
-      if (a.D == 128)
-        k_attn_bf16<H, 128, 1, 64><<<grid, 256, 0, s>>>(st, a);
-      else
-        k_attn_bf16<H, 64, 1, 64><<<grid, 256, 0, s>>>(st, a);
+      // Long sequences: 8 waves (256 queries) share each K/V tile, halving the tile loads
+      // per query; shorter ones keep 4 waves, whose smaller blocks balance better.  Each
+      // query sees the same key tiles in the same order either way (same results).
+      int max_q = 0;
+      for (int b = 0; b < st.n; ++b) max_q = std::max(max_q, st.q_cu[b + 1] - st.q_cu[b]);
+      const FaMap fm = fa_map(a.Hq, a.Hkv);
+      if (max_q >= 8192) {
+        const int grid = fa_grid(fm, count_qblocks(st, 256), a.Hq);
+        if (a.D == 128)
+          k_attn_bf16<H, 128, 1, 64, 8><<<grid, 512, 0, s>>>(st, a);
+        else
+          k_attn_bf16<H, 64, 1, 64, 8><<<grid, 512, 0, s>>>(st, a);
+      } else {
+        const int grid = fa_grid(fm, count_qblocks(st, 128), a.Hq);
+        if (a.D == 128)
+          k_attn_bf16<H, 128, 1, 64><<<grid, 256, 0, s>>>(st, a);
+        else
+          k_attn_bf16<H, 64, 1, 64><<<grid, 256, 0, s>>>(st, a);
+      }
     });
   } else {
     const int nqb = count_qblocks(st, 64);
