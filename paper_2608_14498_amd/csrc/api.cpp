@@ -450,12 +450,21 @@ rp::BSeg w_down_operand(const rp_config& c, const rp_layer_weights& lw) {
 rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw, const rp::SeqTable& st,
                     int32_t M, const LayerWS& w, void* k_out, void* v_out, const void* k0, const void* v0,
                     const LayerPlan& plan, float* gemm_part, const LayerNames& nm,
-                    const rp::MRope& mr = rp::MRope{nullptr, 0, 0}) {
+                    const rp::MRope& mr = rp::MRope{nullptr, 0, 0}, bool norm1_done = false,
+                    const void* next_norm = nullptr, bool* next_normed = nullptr) {
   const rp_config& c = m->cfg;
   const rp_dtype dt = c.dtype;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
-  RP_TRY_LAUNCH_N(nm.norm1, rp::launch_rmsnorm(s, dt, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
+  // Split-K partials of the o-proj, gate/up and down projections are summed by the kernel
+  // that consumes them (residual add + RMSNorm, SwiGLU), not by a separate reduction; the
+  // down projection's consumer applies the next layer's attention norm (next_norm), which
+  // that layer then skips (norm1_done).
+  const int s_o = gemm_part ? rp::gemm_effective_splitk(dt, hq, plan.o) : 1;
+  const int s_gu = gemm_part ? rp::gemm_effective_splitk(dt, d, plan.gu) : 1;
+  const int s_down = gemm_part ? rp::gemm_effective_splitk(dt, F, plan.down) : 1;
+  if (next_normed) *next_normed = next_norm != nullptr && s_down > 1;
+  if (!norm1_done) RP_TRY_LAUNCH_N(nm.norm1, rp::launch_rmsnorm(s, dt, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
   RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE_F32, plan.qkv, gemm_part));
   RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv(s, dt, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position, w.Q,
@@ -474,20 +483,38 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   a.scale = (float)(1.0 / sqrt((double)D));
   RP_TRY_LAUNCH_N(nm.attn, rp::launch_attention(s, dt, st, a, M));
   const rp::BSeg bo = wo_operand(c, lw);
-  RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, dt, M, d, hq, w.O, hq, bo, bo.trans ? d : hq, w.X, d, rp::EPI_ADD_F32,
-                                            plan.o, gemm_part));
-  RP_TRY_LAUNCH_N(nm.norm2, rp::launch_rmsnorm(s, dt, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
+  if (s_o > 1) {
+    RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, dt, M, d, hq, w.O, hq, bo, bo.trans ? d : hq, nullptr, d,
+                                              rp::EPI_PARTIALS, plan.o, gemm_part));
+    RP_TRY_LAUNCH_N(nm.norm2, rp::launch_splitk_add_rmsnorm(s, dt, gemm_part, s_o, M, d, w.X, lw.mlp_norm, c.rms_eps,
+                                                            w.N));
+  } else {
+    RP_TRY_LAUNCH_N(nm.oproj, rp::launch_gemm(s, dt, M, d, hq, w.O, hq, bo, bo.trans ? d : hq, w.X, d, rp::EPI_ADD_F32,
+                                              plan.o, gemm_part));
+    RP_TRY_LAUNCH_N(nm.norm2, rp::launch_rmsnorm(s, dt, w.X, lw.mlp_norm, c.rms_eps, M, d, w.N));
+  }
   rp::BSeg bgu = {lw.w_gate, lw.w_up, lw.w_up, F, 2 * F};
   if (plan.fused) {
     RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, dt, M, F, d, w.N, d, bgu, d, w.ACT, F, rp::EPI_SWIGLU, 1, nullptr));
+  } else if (s_gu > 1) {
+    RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, dt, M, 2 * F, d, w.N, d, bgu, d, nullptr, 2 * F, rp::EPI_PARTIALS,
+                                                plan.gu, gemm_part));
+    RP_TRY_LAUNCH_N(nm.swiglu, rp::launch_splitk_swiglu(s, dt, gemm_part, s_gu, M, F, w.ACT));
   } else {
     RP_TRY_LAUNCH_N(nm.gate_up, rp::launch_gemm(s, dt, M, 2 * F, d, w.N, d, bgu, d, w.GU, 2 * F, rp::EPI_STORE,
                                                 plan.gu, gemm_part));
     RP_TRY_LAUNCH_N(nm.swiglu, rp::launch_swiglu(s, dt, w.GU, M, F, w.ACT));
   }
   const rp::BSeg bd = w_down_operand(c, lw);
-  RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, dt, M, d, F, w.ACT, F, bd, bd.trans ? d : F, w.X, d, rp::EPI_ADD_F32,
-                                           plan.down, gemm_part));
+  if (s_down > 1 && next_norm) {
+    RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, dt, M, d, F, w.ACT, F, bd, bd.trans ? d : F, nullptr, d,
+                                             rp::EPI_PARTIALS, plan.down, gemm_part));
+    RP_TRY_LAUNCH_N(nm.norm1, rp::launch_splitk_add_rmsnorm(s, dt, gemm_part, s_down, M, d, w.X, next_norm,
+                                                            c.rms_eps, w.N));
+  } else {
+    RP_TRY_LAUNCH_N(nm.down, rp::launch_gemm(s, dt, M, d, F, w.ACT, F, bd, bd.trans ? d : F, w.X, d, rp::EPI_ADD_F32,
+                                             plan.down, gemm_part));
+  }
   return RP_OK;
 }
 
@@ -629,11 +656,16 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   suffix_ws(m, R, flags, ws, &w);
   const rp::SeqTable tab = make_table(n_suffix, scu, n_prefix, pcu, grp, rope0);
   RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, dt, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
+  bool norm1_done = false;
   for (int l = 0; l < c.n_layers; ++l) {
     const void* kl = layer_ptr(m, kv.k, kv.layer_stride, l);
     const void* vl = layer_ptr(m, kv.v, kv.layer_stride, l);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, w.plan, w.gemm_part, kSuffixNames);
+    const void* next_norm = l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : nullptr;
+    bool normed = false;
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)R, w.L, w.Ks, w.Vs, kl, vl, w.plan, w.gemm_part, kSuffixNames,
+                   rp::MRope{nullptr, 0, 0}, norm1_done, next_norm, &normed);
     if (st != RP_OK) return st;
+    norm1_done = normed;
   }
   RP_TRY_LAUNCH_N("suffix.final_norm", rp::launch_final_norm_rows(s, dt, tab, w.L.X, h_last, m->final_norm, c.rms_eps, (int32_t)R,
                                            c.d_model, w.L.N));
