@@ -40,8 +40,9 @@ BF16_SMALL = configs.ModelShape(n_layers=2, d_model=384, n_q_heads=6, n_kv_heads
                                 ffn_dim=768, vocab=1000, dtype="bf16")
 BF16_D64 = configs.ModelShape(n_layers=2, d_model=256, n_q_heads=8, n_kv_heads=2, head_dim=64,
                               ffn_dim=512, vocab=2051, dtype="bf16")
-# wide enough (K >= 2048) that the suffix GEMMs split K and SwiGLU runs unfused
-BF16_WIDE = configs.ModelShape(n_layers=1, d_model=2048, n_q_heads=16, n_kv_heads=2, head_dim=128,
+# wide enough (K >= 2048) that the suffix GEMMs split K and SwiGLU runs unfused; two layers,
+# so that the down projection's partials are summed by the next layer's attention norm
+BF16_WIDE = configs.ModelShape(n_layers=2, d_model=2048, n_q_heads=16, n_kv_heads=2, head_dim=128,
                                ffn_dim=4096, vocab=1000, dtype="bf16")
 # the same models stored in fp16 (same kernels, fp16 MFMA)
 F16_SMALL = replace(BF16_SMALL, dtype="f16")
