@@ -11,7 +11,10 @@ shapes, and stores sampled outputs in tests/golden/fullsize_<workload>.npz:
   kv_pos         sampled prefix positions (first, second, middle, last + random)
   k, v           [L, len(kv_pos), Hkv, Dh] post-RoPE keys / values at kv_pos
   h_last         [d] residual stream at the last prefix position
-  logprobs       [S] log-probabilities of the sequence's response tokens
+  logprobs       [S] log-probabilities of the sequence's response tokens; for a
+                 workload of grouped responses, [2, S]: the first and the last
+                 response of sequence seq's group
+  resp_idx       (grouped responses only) the indices of those two responses
   dec_rows       decode-step batch rows checked (co-location workload only)
   dec_vocab      sampled vocabulary ids of the decode logits
   dec_logits     [len(dec_rows), len(dec_vocab)] oracle logits at dec_vocab
@@ -77,12 +80,19 @@ def make(name: str) -> str:
     vo = int(sum(Vis[:b]))
     ids = bt.token_ids[cp[b]:cp[b + 1]]
     vis = inputs.to_f32(bt.visual[vo:vo + Vis[b]])
-    resp = bt.response_ids[cs[b]:cs[b + 1]]
     K, V, h_last, _ = oracle.prefix_forward_one(W, m, ids, vis)
-    lp = oracle.suffix_logprob_one(W, m, K, V, h_last, resp)
     pos = kv_positions(P[b], w.index)
     out = dict(seq=np.int64(b), kv_pos=pos, k=K[:, pos].astype(np.float32), v=V[:, pos].astype(np.float32),
-               h_last=h_last.astype(np.float64), logprobs=lp.astype(np.float64))
+               h_last=h_last.astype(np.float64))
+    if w.group:
+        # grouped responses: the first and the last response of prompt b's group, both
+        # scored over that prompt's one prefix
+        ridx = np.asarray([b * w.group, b * w.group + w.group - 1], np.int64)
+        lps = [oracle.suffix_logprob_one(W, m, K, V, h_last, bt.response_ids[cs[r]:cs[r + 1]]) for r in ridx]
+        out.update(resp_idx=ridx, logprobs=np.stack(lps).astype(np.float64))
+    else:
+        lp = oracle.suffix_logprob_one(W, m, K, V, h_last, bt.response_ids[cs[b]:cs[b + 1]])
+        out.update(logprobs=lp.astype(np.float64))
     del K, V
     if w.decode is not None:
         dec = inputs.make_decode(w)

@@ -111,6 +111,49 @@ def test_fullsize_matches_oracle(name, dtype):
         assert res["decode_logits"] <= tol and res["decode_argmax_ok"]
 
 
+GROUPED_NAME = "qwen7b_grpo_g4_p4096_n8_s256"
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_fullsize_grouped_responses_match_oracle(dtype):
+    """GRPO groups at full size: 4 prompts of 4096 tokens run once, then 32 responses of
+    256 tokens (8 per prompt) are scored in one grouped suffix launch over the shared
+    prefix KV, stored logits and fused scoring both, as the benchmark runs them."""
+    name = GROUPED_NAME
+    g = _golden(name)
+    w = configs.with_model(configs.get(name), dtype=dtype)
+    tol = LP_TOL[dtype]
+    print(f"[fullsize] {name} {dtype}: generating inputs", flush=True)
+    hw = inputs.make_weights(w)
+    bt = inputs.make_batch(w)
+    maxp = max(bt.prefix_lens) + max(bt.suffix_lens) + 1
+    dm = DeviceModel(hw, maxp)
+    dev = dm.device
+    cu_p, cu_s = [int(x) for x in bt.cu_prefix], [int(x) for x in bt.cu_suffix]
+    grp = [int(x) for x in bt.prefix_of_suffix]
+    print(f"[fullsize] {name}: prefix T={cu_p[-1]} suffix R={cu_s[-1]} ({len(grp)} responses)", flush=True)
+    K, V, h = dm.prefix(cu_p, to_device(bt.token_ids, dev), to_device(bt.visual, dev))
+    b = int(g["seq"])
+    rows = cu_p[b] + g["kv_pos"]
+    k = K[:, torch.as_tensor(rows, device=dev)].float().cpu().numpy()
+    v = V[:, torch.as_tensor(rows, device=dev)].float().cpu().numpy()
+    res = dict(k=_rel(k, g["k"]), v=_rel(v, g["v"]), h_last=_rel(h[b].cpu().numpy(), g["h_last"]))
+    rid = to_device(bt.response_ids, dev)
+    lp = dm.suffix_grouped(cu_p, grp, cu_s, K, V, h, rid)
+    lpf = dm.suffix_grouped(cu_p, grp, cu_s, K, V, h, rid, flags=rb.RP_SUFFIX_FUSED_LOGPROB)
+    torch.cuda.synchronize()
+    for tag, out in (("logprob", lp), ("logprob_fused", lpf)):
+        res[tag] = max(float(np.max(np.abs(out[cu_s[r]:cu_s[r + 1]].cpu().numpy() - g["logprobs"][i])))
+                       for i, r in enumerate(g["resp_idx"]))
+    res["fused_vs_plain"] = float((lpf - lp).abs().max().item())
+    del K, V
+    dm.close()
+    print(f"[fullsize] {name} {dtype}: {json.dumps(res)}", flush=True)
+    assert res["k"] <= REL_TOL and res["v"] <= REL_TOL and res["h_last"] <= REL_TOL
+    assert res["logprob"] <= tol and res["logprob_fused"] <= tol
+    assert res["fused_vs_plain"] <= 1e-4
+
+
 PROMPT_NAMES = ["qwen7b_b4_p4096_s256", "qwen7b_ragged_b8"]
 
 
