@@ -456,8 +456,9 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   const rp_dtype dt = c.dtype;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
-  // Split-K partials of the o-proj, gate/up and down projections are summed by the kernel
-  // that consumes them (residual add + RMSNorm, SwiGLU), not by a separate reduction; the
+  // Split-K partials of the q/k/v, o-proj, gate/up and down projections are summed by the
+  // kernel that consumes them (RoPE, residual add + RMSNorm, SwiGLU), not by a separate
+  // reduction; the
   // down projection's consumer applies the next layer's attention norm (next_norm), which
   // that layer then skips (norm1_done).
   const int s_o = gemm_part ? rp::gemm_effective_splitk(dt, hq, plan.o) : 1;
@@ -466,9 +467,18 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   if (next_normed) *next_normed = next_norm != nullptr && s_down > 1;
   if (!norm1_done) RP_TRY_LAUNCH_N(nm.norm1, rp::launch_rmsnorm(s, dt, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
-  RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE_F32, plan.qkv, gemm_part));
-  RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv(s, dt, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope, c.max_position, w.Q,
-                                   k_out, v_out, mr));
+  const int s_qkv = gemm_part ? rp::gemm_effective_splitk(dt, d, plan.qkv) : 1;
+  if (s_qkv > 1 && !mr.pos && (size_t)qkv * sizeof(float) <= 65536) {
+    RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, nullptr, qkv, rp::EPI_PARTIALS, plan.qkv,
+                                            gemm_part));
+    RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv_splitk(s, dt, st, gemm_part, s_qkv, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv,
+                                                       m->rope, c.max_position, w.Q, k_out, v_out));
+  } else {
+    RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, w.QKV, qkv, rp::EPI_STORE_F32, plan.qkv,
+                                            gemm_part));
+    RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv(s, dt, st, w.QKV, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv, m->rope,
+                                                c.max_position, w.Q, k_out, v_out, mr));
+  }
   rp::AttnArgs a;
   a.q = w.Q;
   a.q_ld = hq;

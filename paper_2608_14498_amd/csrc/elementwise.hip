@@ -689,6 +689,48 @@ hipError_t launch_splitk_swiglu(hipStream_t s, rp_dtype dt, const float* part, i
   return hipGetLastError();
 }
 
+// RoPE + K/V store from the split-K partials of the q/k/v projection, for rows at 1-D
+// positions (the suffix): the row is summed into LDS (dynamic, (Hq + 2 Hkv) D floats), then
+// rotated at its sequence position as k_rope_kv does.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_rope_kv_splitk(SeqTable st, const float* __restrict__ part, int splitk,
+                                                        int M, int Hq, int Hkv, int D, const T* __restrict__ bq,
+                                                        const T* __restrict__ bk, const T* __restrict__ bv,
+                                                        RopeFreq rf, int max_pos, T* __restrict__ q_out,
+                                                        T* __restrict__ k_out, T* __restrict__ v_out) {
+  extern __shared__ float4 rowsh4[];
+  float* row = reinterpret_cast<float*>(rowsh4);
+  __shared__ float cs[128];
+  const int r = blockIdx.x;
+  const int ld = (Hq + 2 * Hkv) * D;
+  for (int c = threadIdx.x * 4; c < ld; c += blockDim.x * 4) {
+    float a[4];
+    splitk_sum4(part + (int64_t)r * ld + c, (int64_t)M * ld, splitk, a);
+    *reinterpret_cast<float4*>(row + c) = make_float4(a[0], a[1], a[2], a[3]);
+  }
+  __syncthreads();
+  const int b = seq_of_row(st, r);
+  const int p = min(max(st.rpos0(b) + (r - st.q_cu[b]), 0), max_pos - 1);
+  const int p3[3] = {p, p, p};
+  rope_row<T>(row, p3, D, D, Hq, Hkv, D, bq, bk, bv, rf, q_out + (int64_t)r * Hq * D, k_out + (int64_t)r * Hkv * D,
+              v_out + (int64_t)r * Hkv * D, cs);
+}
+
+hipError_t launch_rope_kv_splitk(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* part, int32_t splitk,
+                                 int32_t M, int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
+                                 const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
+                                 void* v_out) {
+  if (M <= 0) return hipSuccess;
+  const size_t lds = (size_t)(Hq + 2 * Hkv) * D * sizeof(float);
+  if (lds > 65536 || ((Hq + 2 * Hkv) * D) % 4) return hipErrorInvalidValue;
+  with_storage(dt, [&](auto tag_) {
+    using E = decltype(tag_);
+    k_rope_kv_splitk<E><<<M, 1024, lds, s>>>(st, part, splitk, M, Hq, Hkv, D, (const E*)bq, (const E*)bk,
+                                             (const E*)bv, rf, max_pos, (E*)q_out, (E*)k_out, (E*)v_out);
+  });
+  return hipGetLastError();
+}
+
 // Decode RoPE + cache write from the split-K partials of the q/k/v projection: the row is
 // summed into LDS (dynamic, qkv floats), then rotated as k_decode_rope_kv does.
 template <typename T>

@@ -186,6 +186,13 @@ hipError_t launch_decode_rope_kv_splitk(hipStream_t s, rp_dtype dt, const float*
                                         int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
                                         const void* bv, const RopeFreq& rf, const int32_t* kv_len, int32_t cap,
                                         int32_t max_pos, void* q_out, void* cache_k, void* cache_v);
+// launch_rope_kv (1-D positions from the table, all rows) on the q/k/v projection rows
+// summed from their split-K partials [splitk][M][(Hq + 2 Hkv) D]; hipErrorInvalidValue when
+// a row does not fit 64 KiB of LDS.
+hipError_t launch_rope_kv_splitk(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* part, int32_t splitk,
+                                 int32_t M, int32_t Hq, int32_t Hkv, int32_t D, const void* bq, const void* bk,
+                                 const void* bv, const RopeFreq& rf, int32_t max_pos, void* q_out, void* k_out,
+                                 void* v_out);
 // X[b] = E[ids[b]] (clamped); out[b] = RMSNorm(X[b]) * w.
 hipError_t launch_decode_embed_norm(hipStream_t s, rp_dtype dt, const int32_t* ids, const void* embed, int32_t vocab,
                                     int32_t B, int32_t d, float* X, const void* w, float eps, void* out);
