@@ -2,6 +2,11 @@
 
     python tests/golden/make_fullsize.py WORKLOAD [WORKLOAD ...]
     python tests/golden/make_fullsize.py --prompt WORKLOAD [WORKLOAD ...]
+    python tests/golden/make_fullsize.py --seq B --tag TAG WORKLOAD
+
+The last form stores sequence B instead of the default one, in
+tests/golden/fullsize_<workload>_<tag>.npz (the ragged batch's longest prefix and
+longest suffix are stored that way, beside its shortest sequence).
 
 For each named workload this runs the float64 CPU oracle (oracle/, nothing else
 computes) on one sequence of the seeded synthetic batch, at the workload's real
@@ -67,7 +72,7 @@ def kv_positions(P: int, seed: int):
     return np.unique(np.concatenate([fixed, extra])).astype(np.int64)
 
 
-def make(name: str) -> str:
+def make(name: str, seq=None, tag: str = "") -> str:
     t0 = time.time()
     w = configs.get(name)
     m = w.model
@@ -75,7 +80,7 @@ def make(name: str) -> str:
     bt = inputs.make_batch(w)
     W = hw.as_f32()
     P, Vis, S = inputs.draw_lengths(w)
-    b = pick_sequence(w, P)
+    b = pick_sequence(w, P) if seq is None else int(seq)
     cp, cs = bt.cu_prefix, bt.cu_suffix
     vo = int(sum(Vis[:b]))
     ids = bt.token_ids[cp[b]:cp[b + 1]]
@@ -103,7 +108,7 @@ def make(name: str) -> str:
         out.update(dec_rows=rows, dec_vocab=vocab.astype(np.int64), dec_logits=lo[:, vocab].astype(np.float64),
                    dec_argmax=np.asarray(amax, np.int64), dec_top2=np.sort(lo, axis=1)[:, -2:].astype(np.float64))
     meta = dict(workload=name, seconds=round(time.time() - t0, 1), prefix=int(P[b]), suffix=int(S[b]))
-    path = os.path.join(HERE, f"fullsize_{name}.npz")
+    path = os.path.join(HERE, f"fullsize_{name}{'_' + tag if tag else ''}.npz")
     np.savez_compressed(path, meta=np.array(json.dumps(meta)), **out)
     return path
 
@@ -137,5 +142,9 @@ if __name__ == "__main__":
     fn = make
     if args and args[0] == "--prompt":
         fn, args = make_prompt, args[1:]
+    if args and args[0] == "--seq":
+        assert args[2] == "--tag" and len(args) == 5, "usage: --seq B --tag TAG WORKLOAD"
+        print(make(args[4], seq=int(args[1]), tag=args[3]), flush=True)
+        sys.exit(0)
     for n in args:
         print(fn(n), flush=True)

@@ -1,8 +1,10 @@
 """GPU parity: the HIP path (through the C ABI) against the float64 CPU oracle.
 
 Tolerances: |d logprob| <= 1e-4 for the fp32 model and <= 2e-2 for the 16-bit models
-(fp32 accumulation), as required of the path; bf16 models of width 2048 and more, whose
-bf16 rounding floor alone reaches 2e-2, are held to twice that floor (lp_bar).  KV and h_last are compared as
+(fp32 accumulation), as required of the path.  A bf16 case that misses 2e-2 must stay
+within the error of an ideal bf16 implementation of the same tokens (TargetCheck in
+tests/gpu_helpers.py, computed by tests/bf16_emulation.py) and is then reported as an
+expected failure naming both values.  KV and h_last are compared as
 max error relative to the largest reference magnitude: bf16 storage of K/V alone
 contributes up to 2^-9 relative per element, and activations are rounded to bf16
 between kernels, so 3e-2 bounds the bf16 cases; the fp32 model must match to 1e-5.
@@ -15,7 +17,7 @@ import torch
 
 import oracle
 from paper_2608_14498_amd import configs, inputs
-from tests.gpu_helpers import gpu_run, max_abs, oracle_run, rel_err
+from tests.gpu_helpers import TargetCheck, emulated_suffix, gpu_run, max_abs, oracle_run, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -51,16 +53,6 @@ F16_D64 = replace(BF16_D64, dtype="f16")
 F16_WIDE = replace(BF16_WIDE, dtype="f16")
 
 
-def lp_bar(model) -> float:
-    """Log-prob bar against the float64 oracle.  The error that bf16 storage rounding alone
-    leaves grows with the logit scale (sigma_w * sqrt(d)): at d = 2048 it measures 0.019-0.020
-    while the same model stored in fp16 (3 more mantissa bits, same kernels) stays at
-    0.002-0.003, so bf16 models that wide are held to twice that floor, as at full size."""
-    if model.dtype == "f32":
-        return 1e-4
-    return 4e-2 if model.dtype == "bf16" and model.d_model >= 2048 else 2e-2
-
-
 @pytest.mark.parametrize("model,norm,bias", [(BF16_SMALL, "ones", False), (BF16_SMALL, "random", True),
                                              (BF16_D64, "random", True), (BF16_WIDE, "random", True),
                                              (F16_SMALL, "random", True), (F16_D64, "random", True),
@@ -72,9 +64,12 @@ def test_bf16_ragged_batch_matches_oracle(model, norm, bias):
     bt = inputs.make_batch(w)
     got = gpu_run(w, hw, bt)
     ref = oracle_run(w, hw, bt)
-    r = _report(f"{model.dtype} d={model.d_model} D={model.head_dim} {norm} bias={bias}", *got, *ref)
-    assert r["lp"] <= lp_bar(model)
+    name = f"{model.dtype} d={model.d_model} D={model.head_dim} {norm} bias={bias}"
+    r = _report(name, *got, *ref)
     assert r["kv"] <= 3e-2 and r["h"] <= 3e-2
+    chk = TargetCheck(model.dtype)
+    chk.check(name, got[3], ref[3], lambda: emulated_suffix(w, hw, bt))
+    chk.finish()
 
 
 def test_fp32_ragged_edges_match_oracle():
@@ -110,12 +105,22 @@ def test_packing_is_bitwise_invariant(model):
         assert np.array_equal(lp[cs[b]:cs[b + 1]], lp1)
 
 
+# A GPU run that included the bf16 decode step at head_dim 64 and the last-rows-only
+# prefix at head_dim 64 with 1-D positions faulted (illegal memory access) and no cause has
+# been shown; the library returns RP_ERR_UNSUPPORTED for both until one is, and these cases
+# stay skipped (they must not run on a GPU before a cause is found and fixed).
+UNEXPLAINED_FAULT = pytest.mark.skip(reason="disabled in the library (RP_ERR_UNSUPPORTED): a GPU memory fault "
+                                            "in a run that included this combination has no known cause")
+
+
 @pytest.mark.parametrize("model,cap,lens", [(BF16_SMALL, 300, [0, 1, 63, 256, 299]),
                                             (configs.TINY, 300, [0, 1, 63, 256, 299]),
                                             (F16_SMALL, 300, [0, 1, 63, 256, 299]),
                                             # several 512-key chunks per sequence, chunk edges
                                             (BF16_SMALL, 1100, [511, 512, 1023, 700, 1099]),
-                                            (configs.TINY, 1100, [0, 513, 1024, 1099, 5])])
+                                            (configs.TINY, 1100, [0, 513, 1024, 1099, 5]),
+                                            (F16_D64, 400, [0, 131, 399]),
+                                            pytest.param(BF16_D64, 400, [0, 131, 399], marks=UNEXPLAINED_FAULT)])
 def test_decode_step_matches_oracle(model, cap, lens):
     from paper_2608_14498_amd.runtime import DeviceModel, to_device
     w = configs.custom(model, [1], [0], [1], index=53)
@@ -188,10 +193,16 @@ def test_shared_prefix_suffix_matches_oracle_and_duplicated_prefix(model):
     W = hw.as_f32()
     Ko, Vo, Ho = oracle.prefix_forward(W, model, bt.cu_prefix, bt.token_ids, inputs.to_f32(bt.visual))
     lpo = oracle.suffix_logprob_grouped(W, model, bt.cu_prefix, grp, cs, Ko, Vo, Ho, resp)
-    err = max_abs(lp.cpu().numpy(), lpo)
-    print(f"[parity] shared prefix {model.dtype}: max|d logprob| = {err}", flush=True)
-    assert err <= lp_bar(model)
+    got = lp.cpu().numpy()
     dm.close()
+    print(f"[parity] shared prefix {model.dtype}: max|d logprob| = {max_abs(got, lpo)}", flush=True)
+    from types import SimpleNamespace
+    grouped = SimpleNamespace(cu_prefix=bt.cu_prefix, token_ids=bt.token_ids, visual=bt.visual, cu_suffix=cs,
+                              response_ids=resp)
+    chk = TargetCheck(model.dtype)
+    chk.check(f"shared prefix {model.dtype} d={model.d_model}", got, lpo,
+              lambda: emulated_suffix(w, hw, grouped, prefix_of_suffix=grp))
+    chk.finish()
 
 
 @pytest.mark.parametrize("model", [BF16_SMALL, BF16_D64, F16_SMALL])
@@ -301,7 +312,7 @@ def test_prompt_logprobs_match_oracle(model, flags):
     err = max_abs(got, exp)
     print(f"[parity] prompt log-probs {model.dtype} V={model.vocab} flags={flags}: rows {len(pos)} "
           f"|d lp| {err:.3g}", flush=True)
-    assert err <= lp_bar(model)
+    assert err <= (1e-4 if model.dtype == "f32" else 2e-2)
     dm.close()
 
 
@@ -341,11 +352,15 @@ def test_transposed_row_parallel_weights(model):
     err = max_abs(outs[-1][3].numpy(), lpo)
     print(f"[parity] transposed wo/w_down {model.dtype} d={model.d_model}: bitwise equal, |d lp| {err:.3g}",
           flush=True)
-    assert err <= lp_bar(model)
+    chk = TargetCheck(model.dtype)
+    chk.check(f"transposed wo/w_down {model.dtype} d={model.d_model}", outs[-1][3].numpy(), lpo,
+              lambda: emulated_suffix(w, hw, bt))
+    chk.finish()
 
 
 @pytest.mark.parametrize("model,mrope", [(configs.TINY, False), (BF16_SMALL, False), (BF16_D64, True),
-                                         (F16_SMALL, False), (BF16_WIDE, False)])
+                                         (F16_SMALL, False), (BF16_WIDE, False),
+                                         pytest.param(BF16_D64, False, marks=UNEXPLAINED_FAULT)])
 def test_prefix_last_rows_only(model, mrope):
     """RP_PREFIX_LAST_ROWS_ONLY: the last layer past its K/V projection runs only at each
     sequence's last row.  K/V are bitwise those of the full pass, h_last equals the full
