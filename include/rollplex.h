@@ -203,6 +203,9 @@ rp_status rp_suffix_logprob(const rp_model *model, void *stream, int32_t B,
  *     o-proj, MLP) only at each sequence's last row.  kv_out is exactly that of
  *     the full pass; h_last equals it up to fp32 summation order (its GEMMs
  *     split K over the few rows).  hidden_out must be NULL (RP_ERR_INVALID_ARG).
+ *     With 1-D positions (positions NULL), 16-bit models at head_dim 64 return
+ *     RP_ERR_UNSUPPORTED: a GPU memory fault in a run that included that
+ *     combination has no known cause, so it stays disabled until one is shown.
  * Unknown flag bits are RP_ERR_INVALID_ARG.  Workspace: rp_prefix_workspace_bytes.
  * ------------------------------------------------------------------------- */
 #define RP_PREFIX_LAST_ROWS_ONLY 1u
@@ -294,6 +297,8 @@ rp_status rp_prompt_logprob(const rp_model *model, void *stream, int32_t B,
  * 0..kv_len[b], and next_ids[b] = argmax of its logits (lowest id on ties).
  * kv_len is a device int32 [B] array, values clamped to [0, cap-1] (and to
  * max_position-1).  logits (optional) receives fp32 [B, V].
+ * bf16 models at head_dim 64 return RP_ERR_UNSUPPORTED (disabled: a GPU memory
+ * fault in a run that included that combination has no known cause).
  * ------------------------------------------------------------------------- */
 rp_status rp_decode_workspace_bytes(const rp_model *model, int32_t B, int32_t cap, size_t *bytes);
 rp_status rp_decode_step(const rp_model *model, void *stream, int32_t B, rp_kv cache, int32_t cap,

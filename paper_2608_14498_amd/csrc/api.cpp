@@ -287,10 +287,13 @@ struct TailWS {
 };
 
 size_t prefix_ws(const rp_model* m, int32_t B, int64_t T, void* base, bool need_x, LayerWS* w, int32_t** vis_idx,
-                 TailWS* tail = nullptr) {
+                 TailWS* tail = nullptr, float2** rope_cs = nullptr) {
   Carver c(base);
   int32_t* vi = (int32_t*)c.take(T * 4);
   if (vis_idx) *vis_idx = vi;
+  // rotation table of the fused q/k/v epilogue (16-bit models): float2 [T][D/2]
+  float2* cs = half_dtype(m->cfg) ? (float2*)c.take(T * (m->cfg.head_dim / 2) * 8) : nullptr;
+  if (rope_cs) *rope_cs = cs;
   LayerWS tmp;
   carve_layer(c, m->cfg, T, need_x, !plan_layer(m->cfg, (int32_t)T, Pass::kPrefix).fused, w ? w : &tmp);
   const rp_config& cf = m->cfg;
@@ -451,7 +454,8 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
                     int32_t M, const LayerWS& w, void* k_out, void* v_out, const void* k0, const void* v0,
                     const LayerPlan& plan, float* gemm_part, const LayerNames& nm,
                     const rp::MRope& mr = rp::MRope{nullptr, 0, 0}, bool norm1_done = false,
-                    const void* next_norm = nullptr, bool* next_normed = nullptr) {
+                    const void* next_norm = nullptr, bool* next_normed = nullptr,
+                    const float2* rope_cs = nullptr) {
   const rp_config& c = m->cfg;
   const rp_dtype dt = c.dtype;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
@@ -468,7 +472,13 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   if (!norm1_done) RP_TRY_LAUNCH_N(nm.norm1, rp::launch_rmsnorm(s, dt, w.X, lw.attn_norm, c.rms_eps, M, d, w.N));
   rp::BSeg bqkv = {lw.wq, lw.wk, lw.wv, hq, hq + Hkv * D};
   const int s_qkv = gemm_part ? rp::gemm_effective_splitk(dt, d, plan.qkv) : 1;
-  if (s_qkv > 1 && !mr.pos && (size_t)qkv * sizeof(float) <= 65536) {
+  if (rope_cs && s_qkv == 1 && half_dtype(c)) {
+    // bias, RoPE and the Q/K/V stores in the projection's epilogue (rotation table
+    // rope_cs built once per pass for these rows and positions)
+    const rp::RopeOut ro = {w.Q, k_out, v_out, lw.bq, lw.bk, lw.bv, rope_cs, hq, Hkv * D, D};
+    RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, nullptr, qkv, rp::EPI_ROPE, 1, nullptr,
+                                            nullptr, &ro));
+  } else if (s_qkv > 1 && !mr.pos && (size_t)qkv * sizeof(float) <= 65536) {
     RP_TRY_LAUNCH_N(nm.qkv, rp::launch_gemm(s, dt, M, qkv, d, w.N, d, bqkv, d, nullptr, qkv, rp::EPI_PARTIALS, plan.qkv,
                                             gemm_part));
     RP_TRY_LAUNCH_N(nm.rope, rp::launch_rope_kv_splitk(s, dt, st, gemm_part, s_qkv, M, Hq, Hkv, D, lw.bq, lw.bk, lw.bv,
@@ -614,6 +624,10 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
   const bool last_rows = (flags & RP_PREFIX_LAST_ROWS_ONLY) != 0;
   if (last_rows && hidden_out)
     return fail(RP_ERR_INVALID_ARG, "RP_PREFIX_LAST_ROWS_ONLY computes no full hidden state (hidden_out must be NULL)");
+  if (last_rows && !mr.pos && half_dtype(m->cfg) && m->cfg.head_dim == 64)
+    return fail(RP_ERR_UNSUPPORTED,
+                "RP_PREFIX_LAST_ROWS_ONLY with 1-D positions is disabled for 16-bit models at head_dim 64 "
+                "(a GPU memory fault in a run that included this combination has no known cause)");
   const size_t need = prefix_ws(m, B, T, nullptr, hidden_out == nullptr, nullptr, nullptr);
   if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
 
@@ -623,10 +637,14 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
   LayerWS w;
   TailWS tail;
   int32_t* vis_idx = nullptr;
-  prefix_ws(m, B, T, ws, hidden_out == nullptr, &w, &vis_idx, &tail);
+  float2* rope_cs = nullptr;
+  prefix_ws(m, B, T, ws, hidden_out == nullptr, &w, &vis_idx, &tail, &rope_cs);
   if (hidden_out) w.X = hidden_out;
   const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
   const LayerPlan plan = plan_layer(c, (int32_t)T, Pass::kPrefix);
+  if (rope_cs)
+    RP_TRY_LAUNCH_N("prefix.rope_table", rp::launch_rope_table(s, tab, m->rope, c.max_position, mr, (int32_t)T,
+                                                               c.head_dim, rope_cs));
 
   RP_TRY_LAUNCH_N("prefix.visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
   RP_TRY_LAUNCH_N("prefix.embed", rp::launch_embed(s, dt, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
@@ -636,7 +654,8 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
     void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
     if (last_rows && l == c.n_layers - 1)
       return run_last_rows(m, s, m->layers[l], B, cu, tab, (int32_t)T, w, tail, kl, vl, mr, h_last);
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames, mr);
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames, mr, false,
+                   nullptr, nullptr, rope_cs);
     if (st != RP_OK) return st;
   }
   RP_TRY_LAUNCH_N("prefix.gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
@@ -895,6 +914,10 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
   if (!kv_len || !token_ids || !next_ids) return fail(RP_ERR_INVALID_ARG, "kv_len, token_ids and next_ids are required");
   if ((int64_t)(m->cfg.n_q_heads + 2 * m->cfg.n_kv_heads) * m->cfg.head_dim * 4 > 65536)
     return fail(RP_ERR_UNSUPPORTED, "decode step: a q/k/v row must fit 64 KiB of LDS");
+  if (m->cfg.dtype == RP_BF16 && m->cfg.head_dim == 64)
+    return fail(RP_ERR_UNSUPPORTED,
+                "decode step is disabled for bf16 models at head_dim 64 (a GPU memory fault in a run that "
+                "included this combination has no known cause)");
   const size_t need = decode_ws(m, B, cap, nullptr, nullptr);
   if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
 

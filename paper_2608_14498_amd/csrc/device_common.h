@@ -265,4 +265,12 @@ __device__ __forceinline__ void rope_cs(int pos, double inv_freq, float* c, floa
   *c = cosf(rf);
 }
 
+// Rotate-half pair (x1, x2) = (x_i, x_{i+D/2}) by the angle whose cosine and sine are
+// (c, s).  Written with explicit fused multiply-adds so that every kernel that rotates
+// (the RoPE kernels and the fused q/k/v GEMM epilogue) rounds identically.
+__device__ __forceinline__ void rope_rotate(float x1, float x2, float c, float s, float* y1, float* y2) {
+  *y1 = fmaf(x1, c, -(x2 * s));
+  *y2 = fmaf(x2, c, x1 * s);
+}
+
 }  // namespace rp

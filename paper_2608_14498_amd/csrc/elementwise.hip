@@ -246,11 +246,7 @@ __device__ __forceinline__ void rope_row(const float* __restrict__ row, const in
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float c = cs[i + u], s = cs[64 + i + u];
-      y1[u] = x1[u] * c - x2[u] * s;
-      y2[u] = x2[u] * c + x1[u] * s;
-    }
+    for (int u = 0; u < 4; ++u) rope_rotate(x1[u], x2[u], cs[i + u], cs[64 + i + u], &y1[u], &y2[u]);
     T* dst = (isq ? q_dst : k_dst) + h * D + i;
     store4(dst, y1);
     store4(dst + half, y2);
@@ -291,6 +287,35 @@ __global__ __launch_bounds__(256) void k_rope_kv(SeqTable st, const float* __res
   const int64_t ld = (int64_t)(Hq + 2 * Hkv) * D;
   rope_row<T>(qkv + r * ld, pos, mr.pos ? mr.sec0 : D, mr.pos ? mr.sec01 : D, Hq, Hkv, D, bq, bk, bv, rf,
               q_out + (int64_t)r * Hq * D, k_out + (int64_t)r * Hkv * D, v_out + (int64_t)r * Hkv * D, cs, do_q);
+}
+
+// Rotation table of the fused q/k/v epilogue: cs[r * D/2 + i] = (cos, sin) of rotary pair
+// i at row r's position (1-D from the sequence table, or multimodal), exactly the values
+// k_rope_kv forms for that row.
+__global__ __launch_bounds__(64) void k_rope_table(SeqTable st, RopeFreq rf, int max_pos, MRope mr, int M, int half,
+                                                   float2* __restrict__ cs) {
+  const int r = blockIdx.x;
+  int pos[3];
+  if (mr.pos) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) pos[k] = min(max(mr.pos[(int64_t)k * M + r], 0), max_pos - 1);
+  } else {
+    const int b = seq_of_row(st, r);
+    pos[0] = pos[1] = pos[2] = min(max(st.rpos0(b) + (r - st.q_cu[b]), 0), max_pos - 1);
+  }
+  const int sec0 = mr.pos ? mr.sec0 : half, sec01 = mr.pos ? mr.sec01 : half;
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    float c, s;
+    rope_cs(i < sec0 ? pos[0] : i < sec01 ? pos[1] : pos[2], rf.inv_freq[i], &c, &s);
+    cs[(int64_t)r * half + i] = make_float2(c, s);
+  }
+}
+
+hipError_t launch_rope_table(hipStream_t s, const SeqTable& st, const RopeFreq& rf, int32_t max_pos, const MRope& mr,
+                             int32_t M, int32_t D, float2* cs) {
+  if (M <= 0) return hipSuccess;
+  k_rope_table<<<M, 64, 0, s>>>(st, rf, max_pos, mr, M, D / 2, cs);
+  return hipGetLastError();
 }
 
 hipError_t launch_rope_kv(hipStream_t s, rp_dtype dt, const SeqTable& st, const float* qkv, int32_t M,

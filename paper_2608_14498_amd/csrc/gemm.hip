@@ -41,6 +41,7 @@ struct GemmArgs {
   float* partials;   // split-K: [splitk][M][N] fp32
   LseOut lse;        // EPI_LSE outputs
   int n_part;        // EPI_LSE column blocks per row
+  RopeOut rope;      // EPI_ROPE outputs
 };
 
 template <typename T>
@@ -337,6 +338,60 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, f32x16_t (&
             make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
       }
     const int k = lane & 31;
+    if (EPI == EPI_ROPE) {
+      // q/k/v projection: the lane's 4 columns lie in one head (D divides 128), their
+      // rotate-half partners D/2 columns away in the same staged row
+      const RopeOut& ro = g.rope;
+      const int half = ro.D >> 1;
+      const int c = ncol0 + 4 * k;
+      if (c < g.N) {
+        const int seg = c < ro.hq ? 0 : c < ro.hq + ro.hkv ? 1 : 2;
+        const int cc = seg == 0 ? c : seg == 1 ? c - ro.hq : c - ro.hq - ro.hkv;  // column in its segment
+        const int64_t ld = seg == 0 ? ro.hq : ro.hkv;
+        T16* dst0 = (T16*)(seg == 0 ? ro.q : seg == 1 ? ro.k : ro.v) + cc;
+        const T16* bias = (const T16*)(seg == 0 ? ro.bq : seg == 1 ? ro.bk : ro.bv);
+        const bool second = (cc & half) != 0;
+        const int pair = cc & (half - 1);
+        const int kp = k ^ (half >> 2);
+        float bo[4] = {0.f, 0.f, 0.f, 0.f}, bp[4] = {0.f, 0.f, 0.f, 0.f};
+        if (bias) {
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            bo[t] = ldf(bias + cc + t);
+            bp[t] = ldf(bias + (cc ^ half) + t);
+          }
+        }
+#pragma unroll 4
+        for (int sr = 0; sr < 16; ++sr) {
+          const int r = 2 * sr + (lane >> 5);
+          const int m = mw + i * 32 + r;
+          if (m >= g.M) continue;
+          const float4 v = *reinterpret_cast<const float4*>(stage + r * 512 + ((k ^ (r & 15)) << 4));
+          const float4 w = *reinterpret_cast<const float4*>(stage + r * 512 + ((kp ^ (r & 15)) << 4));
+          const float x[4] = {v.x + bo[0], v.y + bo[1], v.z + bo[2], v.w + bo[3]};
+          const float xp[4] = {w.x + bp[0], w.y + bp[1], w.z + bp[2], w.w + bp[3]};
+          float y[4];
+          if (seg == 2) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) y[t] = x[t];
+          } else {
+            const float4* tp = reinterpret_cast<const float4*>(ro.cs + (int64_t)m * half + pair);
+            const float4 t0 = tp[0], t1 = tp[1];
+            const float co[4] = {t0.x, t0.z, t1.x, t1.z}, si[4] = {t0.y, t0.w, t1.y, t1.w};
+            float unused;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              if (second)
+                rope_rotate(xp[t], x[t], co[t], si[t], &unused, &y[t]);
+              else
+                rope_rotate(x[t], xp[t], co[t], si[t], &y[t], &unused);
+            }
+          }
+          store4(dst0 + m * ld, y);
+        }
+      }
+      continue;
+    }
     if (vec && ncol0 + TN <= g.N) {
       // every column of the wave tile is in range: read the staged rows, then (residual)
       // the matching rows of C at once, then add and store; rows past M are clamped for
@@ -556,10 +611,15 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 #undef G_MMA
 #undef G_INTERLEAVE
 
-  if (EPI == EPI_LSE)
+  if (EPI == EPI_ROPE) {  // staged through the (now idle) slab buffers: 16 KiB per wave
+    __syncthreads();
+    uint8_t* stage = (uint8_t*)(wave < 4 ? &As[0][0] : &Bs[0][0]) + (wave & 3) * 16384;
+    gemm_epilogue_lds<EPI, T16, MI, NJ, TM, TN>(g, acc, stage, tm, tn, wm, wn, lane);
+  } else if (EPI == EPI_LSE) {
     gemm_epilogue_lse<MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
-  else
+  } else {
     gemm_epilogue<EPI, T16, MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, fr, fk);
+  }
 }
 
 // ------------------------------------------------------------------------------------
@@ -895,9 +955,14 @@ int32_t gemm_effective_splitk(rp_dtype dt, int32_t K, int32_t splitk) {
 
 hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
-                       int32_t splitk, float* partials, const LseOut* lse) {
+                       int32_t splitk, float* partials, const LseOut* lse, const RopeOut* rope) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const bool half = dt != RP_F32;
+  if (epi == EPI_ROPE &&
+      (!half || splitk > 1 || B.trans || !rope || (rope->D != 64 && rope->D != 128) ||
+       N != rope->hq + 2 * rope->hkv || (rope->hq % rope->D) || (rope->hkv % rope->D) || ((uintptr_t)rope->cs & 15) ||
+       (((uintptr_t)rope->q | (uintptr_t)rope->k | (uintptr_t)rope->v) & 7)))
+    return hipErrorInvalidValue;
   if (epi == EPI_SWIGLU && (!half || splitk > 1)) return hipErrorInvalidValue;
   if (epi == EPI_LSE && (!half || splitk > 1 || !lse)) return hipErrorInvalidValue;
   if (epi == EPI_PARTIALS && !partials) return hipErrorInvalidValue;
@@ -917,6 +982,7 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
   g.ldc = ldc;
   g.partials = partials;
   g.lse = lse ? *lse : LseOut{nullptr, nullptr, nullptr};
+  g.rope = rope ? *rope : RopeOut{};
   g.n_part = lse_parts(N);
   if (splitk < 1) splitk = 1;
   const int bk = half ? GB_K : GF_K;
@@ -947,6 +1013,8 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
         launch_half<EPI_SWIGLU, H>(s, g, grid, b_rows);
       else if (epi == EPI_LSE)
         launch_half<EPI_LSE, H>(s, g, grid, b_rows);
+      else if (epi == EPI_ROPE)
+        launch_half<EPI_ROPE, H>(s, g, grid, b_rows);
       else
         launch_half<EPI_ADD_F32, H>(s, g, grid, b_rows);
     });

@@ -49,6 +49,23 @@ enum Epi : int {
   EPI_SWIGLU = 3,     // C[T][m, f] = silu(gate) * up; B = {gate rows, up rows}, N = ffn features
   EPI_LSE = 4,        // no C: per-row log-sum-exp partials and the target logit (LseOut)
   EPI_PARTIALS = 5,   // split-K partials [splitk][M][N] only (also for splitk 1); the caller reduces
+  EPI_ROPE = 6,       // q/k/v projection: bias, RoPE and the Q/K/V stores fused (RopeOut); 16-bit only
+};
+
+// Outputs of the EPI_ROPE epilogue.  The GEMM computes the [M, (Hq + 2 Hkv) D] projection
+// rows; column c (head-aligned: D divides 128) gets its bias, the rotate-half pair of a q
+// or k column is rotated by cs[m * D/2 + pair] (launch_rope_table), and the row is
+// stored in the 16-bit type to q [M, Hq D], k and v [M, Hkv D].  Needs the LDS-staged
+// epilogue (8-wave tiles: 128 columns per wave).
+struct RopeOut {
+  void* q;
+  void* k;
+  void* v;
+  const void* bq;
+  const void* bk;
+  const void* bv;
+  const float2* cs;
+  int32_t hq, hkv, D;  // Hq*D, Hkv*D, head_dim
 };
 // Number of K splits launch_gemm actually uses for a requested splitk.
 int32_t gemm_effective_splitk(rp_dtype dt, int32_t K, int32_t splitk);
@@ -133,7 +150,11 @@ hipError_t launch_argmax(hipStream_t s, const float* logits, int32_t B, int32_t 
 // epilogue writes silu(A.gate_f) * (A.up_f).  splitk > 1 needs EPI != EPI_SWIGLU.
 hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
-                       int32_t splitk, float* partials, const LseOut* lse = nullptr);
+                       int32_t splitk, float* partials, const LseOut* lse = nullptr,
+                       const RopeOut* rope = nullptr);
+// Rotation table of EPI_ROPE for M rows (float2 [M][D/2]); positions as launch_rope_kv.
+hipError_t launch_rope_table(hipStream_t s, const SeqTable& st, const RopeFreq& rf, int32_t max_pos, const MRope& mr,
+                             int32_t M, int32_t D, float2* cs);
 // lp[r] = tgt[r] - log sum_v exp(logit_rv) from the EPI_LSE partials; NaN where
 // nan_ids[r] < 0 (nan_ids nullable).
 hipError_t launch_lse_combine(hipStream_t s, const float* lse, const float* tgt, int32_t R, int32_t n_part,

@@ -326,3 +326,48 @@ def test_launch_fault_injection_reports_hip_error():
     env = dict(os.environ, RP_FAULT_INJECT="1")
     r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
+
+
+BF16_D64 = configs.ModelShape(n_layers=2, d_model=256, n_q_heads=8, n_kv_heads=2, head_dim=64,
+                              ffn_dim=512, vocab=2051, dtype="bf16")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_unexplained_fault_combinations_are_disabled(lib, dtype):
+    """Two combinations that ran in a GPU run which faulted with no known cause are turned
+    away before any HIP call: the bf16 decode step at head_dim 64 (its fp16 twin has run
+    cleanly on the GPU), and the 16-bit last-rows-only prefix at head_dim 64 with 1-D
+    positions.  head_dim 128 and fp32 still pass validation (checked up to a workspace
+    error, which comes after the gate)."""
+    from dataclasses import replace
+    model = replace(BF16_D64, dtype=dtype)
+    h, keep = make(model, max_pos=1024)
+    try:
+        T = 64
+        kv = rb.make_kv(FAKE + (1 << 32), FAKE + (1 << 33), T * model.n_kv_heads * model.head_dim)
+        need = rb.rp_prefix_workspace_bytes(h, 1, [0, T])
+        args = (h, None, 1, [0, T], FAKE, None, 0, None, None, rb.RP_PREFIX_LAST_ROWS_ONLY, kv,
+                FAKE + (1 << 34), None, FAKE + (1 << 30), need)
+        st, msg = status_of(rb.rp_prefix_forward_flags, *args)
+        assert st == rb.RP_ERR_UNSUPPORTED and "head_dim 64" in msg
+        cap, B = 128, 4
+        cache = rb.make_kv(FAKE + (1 << 32), FAKE + (1 << 33), B * cap * model.n_kv_heads * model.head_dim)
+        dneed = rb.rp_decode_workspace_bytes(h, B, cap)
+        st, msg = status_of(rb.rp_decode_step, h, None, B, cache, cap, FAKE, FAKE + 256, None, FAKE + 512,
+                            FAKE + (1 << 30), dneed if dtype == "bf16" else 100)
+        if dtype == "bf16":
+            assert st == rb.RP_ERR_UNSUPPORTED and "head_dim 64" in msg
+        else:
+            assert st == rb.RP_ERR_WORKSPACE
+    finally:
+        rb.rp_destroy(h)
+    for other in (replace(model, head_dim=128, n_q_heads=4, n_kv_heads=2), configs.TINY):
+        h, keep = make(other, max_pos=1024)
+        try:
+            cap, B = 128, 4
+            cache = rb.make_kv(FAKE + (1 << 32), FAKE + (1 << 33), B * cap * other.n_kv_heads * other.head_dim)
+            st, _ = status_of(rb.rp_decode_step, h, None, B, cache, cap, FAKE, FAKE + 256, None, FAKE + 512,
+                              FAKE + (1 << 30), 100)
+            assert st == rb.RP_ERR_WORKSPACE
+        finally:
+            rb.rp_destroy(h)
