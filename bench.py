@@ -4,8 +4,10 @@
 One step = the prefix pass (prompt prefill: KV + boundary state) followed by the
 suffix pass (response log-probs over the cached KV) for one packed batch of
 seeded synthetic inputs, all inputs resident in HBM.  Default workload: the
-Qwen2.5-VL-7B-shaped 4-layer slice, batch 4, prefix 4096 (3840 visual + 256
-text), suffix 256.
+largest single-GPU configuration, the Qwen2.5-VL-32B-shaped 2-layer slice,
+batch 2, prefix 16384 (15872 visual + 512 text), suffix 512.  The default run
+also reports the 7B-slice workloads (uniform and ragged batches) under
+"workloads" and the co-location arms of Eq. (1) under "colocation".
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -38,6 +40,8 @@ def cpu_baseline(w, hw, bt, prefix_len: int):
     ids = bt.token_ids[cp[0]:cp[1]]
     vis = inputs.to_f32(bt.visual[:bt.visual_lens[0]])
     resp = bt.response_ids[cs[0]:cs[1]]
+    if prefix_len < 0:  # automatic bound: about 10-30 s of float64 work on the host
+        prefix_len = 4096 if w.model.d_model * w.model.n_layers * len(ids) > 4 * 3584 * 4096 else 0
     P = len(ids) if prefix_len <= 0 else min(prefix_len, len(ids))
     ids = ids[:P]
     vis = vis[:int((ids < 0).sum())]
@@ -57,7 +61,8 @@ def cpu_baseline(w, hw, bt, prefix_len: int):
         pass
     n_tok = P + len(resp)
     return {"value": n_tok / (t2 - t0), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"sequence 0 of the workload: prefix {P} + suffix {len(resp)} tokens, all "
+            "sample": f"sequence 0 of the workload{'' if P == len(bt.token_ids[cp[0]:cp[1]]) else f' (its first {P} prefix tokens)'}: "
+                      f"prefix {P} + suffix {len(resp)} tokens, all "
                       f"{w.model.n_layers} layers, float64 numpy oracle; prefix {t1 - t0:.1f} s, "
                       f"suffix {t2 - t1:.1f} s",
             "prefix_s": t1 - t0, "suffix_s": t2 - t1, "cpu_model": cpu, "numpy": np.__version__, "blas": blas}
@@ -196,6 +201,7 @@ def colocation(args, w):
                 rb.rp_stream_destroy(raw[0])
                 rb.rp_stream_destroy(raw[1])
     best = min((a for a in arms if a["regime"] == "balanced"), key=lambda a: a["makespan_ms"])
+    serial = next(a for a in arms if a["regime"] == "balanced")
     out = {
         "metric": "co-location: prefix tokens/s and decode tokens/s co-running vs alone; Eq. (1) saving",
         "value": T / (best["makespan_ms"] * 1e-3),
@@ -207,10 +213,14 @@ def colocation(args, w):
                    "decode_batch": Bd, "decode_kv": kvl, "cus": ncu},
         "prefix_alone_ms": T_P, "prefix_alone_tokens_per_s": T / (T_P * 1e-3),
         "decode_step_alone_ms": step_ms, "decode_alone_tokens_per_s": Bd / (step_ms * 1e-3),
-        "decode_kernels": decode_kernels, "best_balanced_arm": best["arm"], "arms": arms,
+        "decode_kernels": decode_kernels, "best_balanced_arm": best["arm"],
+        "balanced_serial_ms": serial["serial_ms"], "balanced_best_makespan_ms": best["makespan_ms"],
+        "balanced_best_saving_ms": best["saving_measured_ms"], "arms": arms,
     }
     dm.close()
-    print(json.dumps(out), flush=True)
+    del K, V, ck, cv, ws_p, ws_d
+    torch.cuda.empty_cache()
+    return out
 
 
 def measured_traffic(kernel_src: str, path: str, sha_key: str = "gemm_source_sha1"):
@@ -226,20 +236,25 @@ def measured_traffic(kernel_src: str, path: str, sha_key: str = "gemm_source_sha
     return rec["traffic_bytes_per_launch"] if rec.get(sha_key) == cur else None
 
 
+HEADLINE = "qwen32b_b2_p16384_s512"
+EXTRA_WORKLOADS = ("qwen7b_b4_p4096_s256", "qwen7b_ragged_b8")
+COLOCATION = "qwen7b_coloc_p4x8192_d64"
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="qwen7b_b4_p4096_s256")
+    ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--profile-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-prefix-len", type=int, default=0,
-                    help="truncate the CPU-baseline sample prefix (0 = full)")
+    ap.add_argument("--cpu-prefix-len", type=int, default=-1,
+                    help="truncate the CPU-baseline sample prefix (0 = full, -1 = bounded automatically)")
     ap.add_argument("--dtype", choices=["bf16", "f16"], default=None,
                     help="run the workload's model in this 16-bit storage type (default: as named)")
-    ap.add_argument("--no-f16-variant", action="store_true",
-                    help="skip timing the fp16 variant of a bf16 workload")
+    ap.add_argument("--f16-variant", action="store_true",
+                    help="also time the workload with its model stored in fp16")
     ap.add_argument("--no-fused-variant", action="store_true",
                     help="skip timing the suffix with the fused lm_head + log-sum-exp scoring")
     ap.add_argument("--no-transposed-variant", action="store_true",
@@ -250,6 +265,8 @@ def main():
                     help="skip the matrix-core probe and the device-copy bandwidth measurement")
     ap.add_argument("--no-prompt-logprobs", action="store_true",
                     help="skip timing the prompt-token log-probs (rp_prompt_logprob)")
+    ap.add_argument("--no-extra-workloads", action="store_true",
+                    help="report the named workload only (no 7B-slice workloads, no co-location arms)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -269,15 +286,31 @@ def main():
               f"sequence and is measured on one GPU's share.", file=sys.stderr)
         sys.exit(2)
 
-    from paper_2608_14498_amd import configs, perf
+    from paper_2608_14498_amd import configs
 
     w = configs.get(args.workload)
     if args.dtype:
         w = configs.with_model(w, dtype=args.dtype)
     if w.decode is not None:
-        return colocation(args, w)
+        print(json.dumps(colocation(args, w)), flush=True)
+        return
+    out = workload_record(w, args, headline=True)
+    if not args.no_extra_workloads and args.workload == HEADLINE and not args.dtype:
+        out["workloads"] = {}
+        for name in EXTRA_WORKLOADS:
+            out["workloads"][name] = workload_record(configs.get(name), args, headline=False)
+        out["colocation"] = colocation(args, configs.get(COLOCATION))
+    print(json.dumps(out), flush=True)
+
+
+def workload_record(w, args, headline: bool) -> dict:
+    """Time one prefix + suffix workload.  The headline record carries the contract's keys,
+    the variants, the measured peaks and the CPU baseline; the others the throughputs, MFMA
+    fractions and rooflines only."""
+    from paper_2608_14498_amd import configs, perf
+
     m = w.model
-    res = run_passes(w, args, profile=True, prompt=True)
+    res = run_passes(w, args, profile=True, prompt=headline)
     T, R, B, kernels = res["T"], res["R"], res["B"], res["kernels"]
     ms_step, pre_ms, suf_ms = res["ms_step"], res["pre_ms"], res["suf_ms"]
     bt = res["bt"]
@@ -293,12 +326,13 @@ def main():
     if gu:
         ach = gu_flops / (gu["avg_ms"] * 1e-3) / 1e12
         traffic = None
-        if w.name == "qwen7b_b4_p4096_s256" and m.dtype == "bf16":
+        if m.dtype == "bf16":
             traffic = measured_traffic("paper_2608_14498_amd/csrc/gemm.hip",
-                                       "profiles/gemm_gate_up_qwen7b_b4_p4096_s256_traffic.json")
+                                       f"profiles/gemm_gate_up_{w.name}_traffic.json")
         roofline = {"kernel": "prefix.gemm_gate_up (fused SwiGLU)", "bound": "mfma", "achieved": ach,
                     "peak": peak / 1e12, "unit": "TFLOP/s", "frac": ach / (peak / 1e12),
                     "traffic": traffic, "algorithmic_per_launch": gu_flops,
+                    "algorithmic_per_unit": "2 * 2F * d flop per prefix token (T tokens per launch)",
                     "algorithmic_bytes_per_launch": 2 * (T * m.d_model + 2 * m.ffn_dim * m.d_model
                                                          + T * m.ffn_dim)}
     ls = kernels.get("suffix.logsoftmax_gather")
@@ -308,9 +342,9 @@ def main():
         k12 = {"bound": "hbm", "achieved": gbs, "peak": perf.PEAK_HBM_BPS / 1e9, "unit": "GB/s",
                "frac": gbs / (perf.PEAK_HBM_BPS / 1e9), "algorithmic_bytes_per_launch": perf.logsoftmax_bytes(R, m.vocab),
                "traffic": None}
-        if w.name == "qwen7b_b4_p4096_s256" and m.dtype == "bf16":
+        if m.dtype == "bf16":
             k12["traffic"] = measured_traffic("paper_2608_14498_amd/csrc/elementwise.hip",
-                                              "profiles/logsoftmax_gather_qwen7b_b4_p4096_s256_traffic.json",
+                                              f"profiles/logsoftmax_gather_{w.name}_traffic.json",
                                               "elementwise_source_sha1")
 
     out = {
@@ -343,12 +377,15 @@ def main():
         "step_ms": res["step_stats"],
         "roofline": roofline,
         "logsoftmax_roofline": k12,
-        "prompt_logprobs": res["prompt"],
-        "kernels": kernels,
     }
-    if m.dtype == "bf16" and not args.no_f16_variant:
+    if not headline:
+        out["kernels"] = {k: v for k, v in kernels.items() if v["ms_per_step"] >= 0.05}
+        return out
+    out["prompt_logprobs"] = res["prompt"]
+    out["kernels"] = kernels
+    if m.dtype == "bf16" and args.f16_variant:
         # the same model stored in fp16 (bf16 weights converted exactly): same kernels with
-        # fp16 MFMA, the precision that meets the full-size log-prob bar
+        # fp16 MFMA
         wf = configs.with_model(w, dtype="f16")
         rf = run_passes(wf, args, profile=False)
         out["f16_variant"] = {
@@ -404,7 +441,7 @@ def main():
     if not args.no_cpu_baseline:
         log("CPU baseline: oracle on sequence 0")
         out["cpu_baseline"] = cpu_baseline(w, res["hw"], bt, args.cpu_prefix_len)
-    print(json.dumps(out), flush=True)
+    return out
 
 
 def run_passes(w, args, profile: bool, flags: int = 0, weight_layout: int = 0, prompt: bool = False,
