@@ -306,6 +306,27 @@ rp_status rp_decode_step(const rp_model *model, void *stream, int32_t B, rp_kv c
                          int32_t *next_ids, void *workspace, size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
+ * rp_decode_step without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  Arguments and results are those of rp_decode_step; the
+ * scratch is a library-owned static device array of
+ * RP_DECODE_STATIC_SCRATCH_BYTES on each GPU the library runs on (held until the
+ * process ends).  The call allocates nothing; its first call on a device looks up
+ * that device's copy of the array.
+ * The scratch needed is rp_decode_workspace_bytes() less the [B, V] fp32 logits
+ * when logits is non-NULL (about 63 MiB for the 7B slice at B = 64 with logits
+ * given); larger needs return RP_ERR_WORKSPACE before any HIP call.  No part of
+ * the scratch needs to start at zero: every byte a step reads was written earlier
+ * in the same step.  Every call on a GPU shares that GPU's array, so calls that
+ * overlap on one GPU (concurrent streams, or a captured graph replayed while
+ * another call runs) race; serialise them.
+ * ------------------------------------------------------------------------- */
+#define RP_DECODE_STATIC_SCRATCH_BYTES (96u << 20)
+rp_status rp_decode_step_static(const rp_model *model, void *stream, int32_t B, rp_kv cache, int32_t cap,
+                                const int32_t *kv_len, const int32_t *token_ids, float *logits,
+                                int32_t *next_ids);
+
+/* ---------------------------------------------------------------------------
  * Co-location helpers (Section "Resource Sharing Policy": decode and prefix
  * share one GPU; static partitions are the analog of the paper's SM
  * partitions).  mask: n_words 32-bit words, bit i = compute unit i may run

@@ -28,7 +28,7 @@ SYMBOLS = ["rp_create", "rp_destroy", "rp_prefix_workspace_bytes", "rp_prefix_fo
            "rp_suffix_workspace_bytes", "rp_suffix_logprob", "rp_suffix_grouped_workspace_bytes",
            "rp_suffix_logprob_grouped", "rp_prompt_logprob_workspace_bytes", "rp_prompt_logprob",
            "rp_decode_workspace_bytes",
-           "rp_decode_step", "rp_stream_create_cu_masked", "rp_stream_destroy",
+           "rp_decode_step", "rp_decode_step_static", "rp_stream_create_cu_masked", "rp_stream_destroy",
            "rp_device_cu_count", "rp_calibrate_mfma", "rp_calibrate_read", "rp_last_error", "rp_status_string", "rp_version",
            "rp_profile_enable", "rp_profile_collect", "rp_profile_count", "rp_profile_read",
            "rp_profile_reset"]
@@ -102,6 +102,8 @@ def lib():
             "rp_calibrate_read": (c_int, [c_void_p, c_void_p, c_int64, c_int32, c_void_p, c_size_t]),
             "rp_decode_step": (c_int, [c_void_p, c_void_p, c_int32, RpKV, c_int32, c_void_p, c_void_p,
                                        c_void_p, c_void_p, c_void_p, c_size_t]),
+            "rp_decode_step_static": (c_int, [c_void_p, c_void_p, c_int32, RpKV, c_int32, c_void_p, c_void_p,
+                                              c_void_p, c_void_p]),
             "rp_stream_create_cu_masked": (c_int, [c_int, POINTER(c_uint32), c_uint32, POINTER(c_void_p)]),
             "rp_stream_destroy": (c_int, [c_void_p]),
             "rp_device_cu_count": (c_int, [c_int]),
@@ -256,6 +258,16 @@ def rp_decode_step(model: int, stream, B: int, cache: RpKV, cap: int, kv_len, to
                    workspace, workspace_bytes: int) -> None:
     _check(lib().rp_decode_step(model, _ptr(stream), B, cache, cap, _ptr(kv_len), _ptr(token_ids),
                                 _ptr(logits), _ptr(next_ids), _ptr(workspace), int(workspace_bytes)))
+
+
+RP_DECODE_STATIC_SCRATCH_BYTES = 96 << 20
+
+
+def rp_decode_step_static(model: int, stream, B: int, cache: RpKV, cap: int, kv_len, token_ids, logits,
+                          next_ids) -> None:
+    """rp_decode_step with the library's static scratch instead of a workspace."""
+    _check(lib().rp_decode_step_static(model, _ptr(stream), B, cache, cap, _ptr(kv_len), _ptr(token_ids),
+                                       _ptr(logits), _ptr(next_ids)))
 
 
 def rp_stream_create_cu_masked(device: int, mask_words: Sequence[int]) -> int:

@@ -8,6 +8,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -383,13 +384,15 @@ struct DecodeWS {
   float* gemm_part;
 };
 
-size_t decode_ws(const rp_model* m, int32_t B, int32_t cap, void* base, DecodeWS* w) {
+// own_logits: carve the [B, V] logits too (they go to the workspace when the caller
+// passes none).
+size_t decode_ws(const rp_model* m, int32_t B, int32_t cap, void* base, DecodeWS* w, bool own_logits = true) {
   Carver c(base);
   DecodeWS tmp;
   DecodeWS* s = w ? w : &tmp;
   const rp_config& cfg = m->cfg;
   carve_layer(c, cfg, B, true, true, &s->L);
-  s->logits = (float*)c.take((int64_t)B * cfg.vocab * 4);
+  s->logits = own_logits ? (float*)c.take((int64_t)B * cfg.vocab * 4) : nullptr;
   s->attn_part = (float*)c.take(rp::decode_attn_partial_floats(B, cfg.n_q_heads, cfg.head_dim, cap) * 4);
   const int64_t d = cfg.d_model, F = cfg.ffn_dim, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
   const int64_t hq = (int64_t)cfg.n_q_heads * cfg.head_dim;
@@ -904,8 +907,13 @@ rp_status rp_decode_workspace_bytes(const rp_model* m, int32_t B, int32_t cap, s
   return RP_OK;
 }
 
-rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache, int32_t cap, const int32_t* kv_len,
-                         const int32_t* token_ids, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes) {
+}  // extern "C"
+
+namespace {
+
+// Host-side checks of a decode step (before any HIP call).
+rp_status check_decode(const rp_model* m, int32_t B, const rp_kv& cache, int32_t cap, const int32_t* kv_len,
+                       const int32_t* token_ids, const int32_t* next_ids) {
   if (!m) return fail(RP_ERR_INVALID_ARG, "model is NULL");
   if (B < 1 || cap < 1) return fail(RP_ERR_SHAPE, "batch and cap must be >= 1");
   if ((int64_t)B * cap > (int64_t)1 << 31) return fail(RP_ERR_UNSUPPORTED, "batch * cap too large");
@@ -918,14 +926,18 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
     return fail(RP_ERR_UNSUPPORTED,
                 "decode step is disabled for bf16 models at head_dim 64 (a GPU memory fault in a run that "
                 "included this combination has no known cause)");
-  const size_t need = decode_ws(m, B, cap, nullptr, nullptr);
-  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
+  return RP_OK;
+}
 
+// The decode step's launches over a validated, large enough workspace (carved with
+// own_logits as sized).
+rp_status decode_run(const rp_model* m, void* stream, int32_t B, rp_kv cache, int32_t cap, const int32_t* kv_len,
+                     const int32_t* token_ids, float* logits, int32_t* next_ids, void* ws, bool own_logits) {
   hipStream_t s = (hipStream_t)stream;
   const rp_config& c = m->cfg;
   const rp_dtype dt = c.dtype;
   DecodeWS w;
-  decode_ws(m, B, cap, ws, &w);
+  decode_ws(m, B, cap, ws, &w, own_logits);
   float* lg = logits ? logits : w.logits;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
@@ -976,6 +988,62 @@ rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache
                                 decode_splitk(c, B, c.vocab, d), w.gemm_part));
   RP_TRY_LAUNCH_N("decode.argmax", rp::launch_argmax(s, lg, B, c.vocab, next_ids));
   return RP_OK;
+}
+
+// Library-owned scratch of rp_decode_step_static: one copy on every GPU the library
+// runs on, held until the process ends.  In host code the array's name is only a
+// stand-in: its device address on the current GPU comes from hipGetSymbolAddress, taken
+// once per device and kept in g_scratch_addr.
+static __device__ __align__(256) uint8_t scratch[RP_DECODE_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+rp_status static_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(RP_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(RP_ERR_UNSUPPORTED, "device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(RP_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return RP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rp_status rp_decode_step(const rp_model* m, void* stream, int32_t B, rp_kv cache, int32_t cap, const int32_t* kv_len,
+                         const int32_t* token_ids, float* logits, int32_t* next_ids, void* ws, size_t ws_bytes) {
+  rp_status st = check_decode(m, B, cache, cap, kv_len, token_ids, next_ids);
+  if (st != RP_OK) return st;
+  const size_t need = decode_ws(m, B, cap, nullptr, nullptr);
+  if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
+  return decode_run(m, stream, B, cache, cap, kv_len, token_ids, logits, next_ids, ws, true);
+}
+
+rp_status rp_decode_step_static(const rp_model* m, void* stream, int32_t B, rp_kv cache, int32_t cap,
+                                const int32_t* kv_len, const int32_t* token_ids, float* logits, int32_t* next_ids) {
+  rp_status st = check_decode(m, B, cache, cap, kv_len, token_ids, next_ids);
+  if (st != RP_OK) return st;
+  const bool own_logits = logits == nullptr;
+  const size_t need = decode_ws(m, B, cap, nullptr, nullptr, own_logits);
+  if (need > (size_t)RP_DECODE_STATIC_SCRATCH_BYTES)
+    return fail(RP_ERR_WORKSPACE,
+                "rp_decode_step_static: batch %d, cap %d needs %zu bytes of scratch%s; the static scratch holds %zu",
+                B, cap, need, own_logits ? " (logits included: pass a logits buffer to need less)" : "",
+                (size_t)RP_DECODE_STATIC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((st = static_scratch(&ws)) != RP_OK) return st;
+  return decode_run(m, stream, B, cache, cap, kv_len, token_ids, logits, next_ids, ws, own_logits);
 }
 
 rp_status rp_profile_enable(int enable, int32_t max_launches) {

@@ -371,3 +371,27 @@ def test_unexplained_fault_combinations_are_disabled(lib, dtype):
             assert st == rb.RP_ERR_WORKSPACE
         finally:
             rb.rp_destroy(h)
+
+
+def test_static_decode_validation(lib):
+    """rp_decode_step_static checks its arguments and the scratch it needs before any HIP
+    call: more than RP_DECODE_STATIC_SCRATCH_BYTES is RP_ERR_WORKSPACE."""
+    text = open(HEADER).read()
+    assert re.search(r"#define RP_DECODE_STATIC_SCRATCH_BYTES \(96u << 20\)", text)
+    assert rb.RP_DECODE_STATIC_SCRATCH_BYTES == 96 << 20
+    m = configs.QWEN7B_SLICE
+    h, keep = make(m, max_pos=8300)
+    try:
+        def call(B, cap, logits=FAKE + (1 << 36), next_ids=FAKE + 512):
+            cache = rb.make_kv(FAKE + (1 << 32), FAKE + (1 << 33), B * cap * m.n_kv_heads * m.head_dim)
+            return status_of(rb.rp_decode_step_static, h, None, B, cache, cap, FAKE, FAKE + 256, logits, next_ids)
+        st, msg = call(256, 8256)
+        assert st == rb.RP_ERR_WORKSPACE and "static scratch" in msg
+        st, msg = call(64, 8256, logits=None)   # the logits would need 37 MiB more
+        assert st == rb.RP_ERR_WORKSPACE and "logits" in msg
+        assert call(64, 8256, next_ids=None)[0] == rb.RP_ERR_INVALID_ARG
+        assert call(0, 8256)[0] == rb.RP_ERR_SHAPE
+        need = rb.rp_decode_workspace_bytes(h, 64, 8256) - 64 * m.vocab * 4
+        assert need <= rb.RP_DECODE_STATIC_SCRATCH_BYTES
+    finally:
+        rb.rp_destroy(h)
