@@ -689,8 +689,10 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   static_assert(NT % 3 == 0 || NT > 3, "ring");
   __shared__ u32x4_t Ks0[KT * CH], Ks1[KT * CH], Ks2[KT * CH], Vs0[KT * CH], Vs1[KT * CH], Vs2[KT * CH];
   const int lane = threadIdx.x;
-  const int c = blockIdx.x % nchunks, bg = blockIdx.x / nchunks;
-  const int g = bg % Hkv, b = bg / Hkv;
+  // kv head fastest: the Hkv waves that read the same cache rows (each its own 2*D-byte
+  // slice of a row) are dispatched together, so each row is fetched from HBM while open
+  const int g = blockIdx.x % Hkv, bc = blockIdx.x / Hkv;
+  const int c = bc % nchunks, b = bc / nchunks;
   const int G = Hq / Hkv;
   const int n = min(max(kv_len[b], 0), min(cap, max_pos) - 1);  // keys 0..n
   const int k_begin = c * DC_KEYS;

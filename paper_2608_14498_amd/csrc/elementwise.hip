@@ -102,6 +102,36 @@ hipError_t launch_decode_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, c
 template <typename T>
 __device__ __forceinline__ void rmsnorm_row(const float* __restrict__ x, const T* __restrict__ w,
                                             float eps, int d, T* __restrict__ out, float* red) {
+  constexpr int kMaxChunks = 4;  // rows of up to 4 x 8 values per thread stay in registers
+  const int step = blockDim.x * 8;
+  if (d <= kMaxChunks * step) {
+    // one read of the row; the same summation order as the two-pass loop below
+    float v[kMaxChunks][8];
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j) {
+      const int c = threadIdx.x * 8 + j * step;
+      if (c < d) {
+        load8(x + c, v[j]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ss = fmaf(v[j][i], v[j][i], ss);
+      }
+    }
+    const float tot = block_sum(ss, red);
+    const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j) {
+      const int c = threadIdx.x * 8 + j * step;
+      if (c < d) {
+        float g[8];
+        load8(w + c, g);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[j][i] = v[j][i] * inv * g[i];
+        store8(out + c, v[j]);
+      }
+    }
+    return;
+  }
   float ss = 0.f;
   for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
     float v[8];
