@@ -14,7 +14,10 @@ from ctypes import POINTER, Structure, byref, c_char_p, c_double, c_float, c_int
     c_size_t, c_uint32, c_void_p
 from typing import Optional, Sequence
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "librollplex.so")
+# RP_LIBRARY selects another build of the same library (the host-sanitized one of
+# build.py --sanitize); by default the in-tree gfx950 build.
+LIB_PATH = os.environ.get("RP_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib",
+                                                        "librollplex.so")
 
 RP_OK, RP_ERR_INVALID_ARG, RP_ERR_SHAPE, RP_ERR_UNSUPPORTED, RP_ERR_WORKSPACE, RP_ERR_HIP = range(6)
 RP_F32, RP_BF16, RP_F16 = 0, 1, 2

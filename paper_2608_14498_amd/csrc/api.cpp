@@ -8,6 +8,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -87,15 +88,36 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 size_t elem_size(const rp_config& c) { return c.dtype == RP_F32 ? 4 : 2; }
 bool half_dtype(const rp_config& c) { return c.dtype == RP_BF16 || c.dtype == RP_F16; }
 
+// RP_DEBUG (environment, read once): guard bytes after every workspace slice, checked
+// after the pass, and range checks of the device-side ids; each checked call then
+// synchronises its stream and reports what it found.  Workspace sizes include the guards.
+bool debug_mode() {
+  static const bool on = [] {
+    const char* e = getenv("RP_DEBUG");
+    return e && *e && strcmp(e, "0") != 0;
+  }();
+  return on;
+}
+
+// Guard offsets of the last carve into a real workspace (this thread).
+thread_local std::vector<uint64_t> g_last_guards;
+
 // Bump allocator over the caller's workspace (sizing pass when base == nullptr).
 struct Carver {
   char* base;
   size_t off = 0;
-  explicit Carver(void* b) : base((char*)b) {}
+  explicit Carver(void* b) : base((char*)b) {
+    if (base) g_last_guards.clear();
+  }
   void* take(size_t bytes) {
     off = (off + 255) & ~(size_t)255;
     void* p = base ? base + off : nullptr;
     off += bytes;
+    if (debug_mode()) {
+      off = (off + 255) & ~(size_t)255;
+      if (base) g_last_guards.push_back(off);
+      off += rp::kGuardBytes;
+    }
     return p;
   }
 };
@@ -126,8 +148,12 @@ void carve_layer(Carver& c, const rp_config& cfg, int64_t M, bool need_x, bool n
 
 rp_status check_config(const rp_config* c) {
   if (!c) return fail(RP_ERR_INVALID_ARG, "config is NULL");
-  if (c->dtype != RP_F32 && c->dtype != RP_BF16 && c->dtype != RP_F16)
-    return fail(RP_ERR_INVALID_ARG, "bad dtype %d", (int)c->dtype);
+  // The caller may store any integer in the enum field; reading it as rp_dtype before
+  // it is known to be one of the enumerators is undefined in C++, so read its bytes.
+  int dtype_value = 0;
+  memcpy(&dtype_value, &c->dtype, sizeof dtype_value);
+  if (dtype_value != RP_F32 && dtype_value != RP_BF16 && dtype_value != RP_F16)
+    return fail(RP_ERR_INVALID_ARG, "bad dtype %d", dtype_value);
   if (c->weight_layout & ~RP_WEIGHT_LAYOUTS)
     return fail(RP_ERR_INVALID_ARG, "unknown weight_layout bits 0x%x", c->weight_layout);
   if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn_dim < 1 ||
@@ -428,6 +454,83 @@ rp_status check_ws(void* ws, size_t have, size_t need) {
   return RP_OK;
 }
 
+// Device record of the debug checks: one copy per GPU (file-scope device array; its
+// address on the current device comes from hipGetSymbolAddress, taken once per device).
+static __device__ int debug_record[4];
+std::mutex g_debug_mu;
+int* g_debug_addr[64] = {};
+
+rp_status debug_record_addr(int** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(RP_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(RP_ERR_UNSUPPORTED, "device %d outside [0, 64)", dev);
+  std::lock_guard<std::mutex> lock(g_debug_mu);
+  if (!g_debug_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(debug_record));
+    if (e != hipSuccess || !p) return fail(RP_ERR_HIP, "hipGetSymbolAddress(debug_record): %s", hipGetErrorString(e));
+    g_debug_addr[dev] = (int*)p;
+  }
+  *out = g_debug_addr[dev];
+  return RP_OK;
+}
+
+// The checks of one call in debug mode (no-ops otherwise): begin() after the workspace is
+// carved fills its guards; check_ids() queues a range check; end() checks the guards,
+// synchronises the stream and turns the first recorded problem into the call's status.
+struct DebugPass {
+  bool on = false;
+  hipStream_t s = nullptr;
+  uint8_t* ws = nullptr;
+  rp::GuardTable gt{};
+  int* rec = nullptr;
+  struct Check {
+    const char* what;
+    int lo, hi;
+  };
+  std::vector<Check> checks;
+
+  rp_status begin(hipStream_t stream, void* workspace) {
+    on = debug_mode();
+    if (!on) return RP_OK;
+    s = stream;
+    ws = (uint8_t*)workspace;
+    gt.n = 0;
+    for (size_t i = 0; i < g_last_guards.size() && gt.n < rp::kMaxGuards; ++i) gt.off[gt.n++] = g_last_guards[i];
+    if (!ws) gt.n = 0;
+    rp_status st = debug_record_addr(&rec);
+    if (st != RP_OK) return st;
+    hipError_t e = rp::launch_debug_reset(s, rec);
+    if (e == hipSuccess) e = rp::launch_guard_fill(s, ws, gt);
+    return e == hipSuccess ? RP_OK : fail(RP_ERR_HIP, "RP_DEBUG set-up: %s", hipGetErrorString(e));
+  }
+  rp_status check_ids(const int32_t* v, int32_t n, int32_t lo, int32_t hi, const char* what, int code) {
+    if (!on) return RP_OK;
+    checks.push_back(Check{what, lo, hi});
+    const hipError_t e = rp::launch_check_range(s, v, n, lo, hi, code + 16 * (int)(checks.size() - 1), rec);
+    return e == hipSuccess ? RP_OK : fail(RP_ERR_HIP, "RP_DEBUG check: %s", hipGetErrorString(e));
+  }
+  rp_status end(rp_status st) {
+    if (!on || st != RP_OK) return st;
+    hipError_t e = hipSuccess;
+    const char* corrupt = getenv("RP_DEBUG_CORRUPT_GUARD");  // self-test: a forced overflow
+    if (corrupt && *corrupt && strcmp(corrupt, "0") != 0) e = rp::launch_guard_corrupt(s, ws, gt);
+    if (e == hipSuccess) e = rp::launch_guard_check(s, ws, gt, rec);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    int h[4] = {0, 0, 0, 0};
+    if (e == hipSuccess) e = hipMemcpy(h, rec, sizeof h, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail(RP_ERR_HIP, "RP_DEBUG check: %s", hipGetErrorString(e));
+    if (h[0] == 0) return RP_OK;
+    if (h[0] == rp::DBG_GUARD)
+      return fail(RP_ERR_HIP, "RP_DEBUG: workspace guard %d (after slice %d) was overwritten", h[1], h[1]);
+    const int idx = h[0] / 16, code = h[0] % 16;
+    const Check c = idx < (int)checks.size() ? checks[idx] : Check{"value", 0, 0};
+    return fail(code == rp::DBG_KV_LEN ? RP_ERR_SHAPE : RP_ERR_INVALID_ARG,
+                "RP_DEBUG: %s[%d] = %d outside [%d, %d)", c.what, h[1], h[2], c.lo, c.hi);
+  }
+};
+
 void* layer_ptr(const rp_model* m, void* base, int64_t stride, int l) {
   return (char*)base + (size_t)l * stride * elem_size(m->cfg);
 }
@@ -643,6 +746,9 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
   float2* rope_cs = nullptr;
   prefix_ws(m, B, T, ws, hidden_out == nullptr, &w, &vis_idx, &tail, &rope_cs);
   if (hidden_out) w.X = hidden_out;
+  DebugPass dbg;
+  if ((st = dbg.begin(s, ws)) != RP_OK) return st;
+  if ((st = dbg.check_ids(token_ids, (int32_t)T, -1, c.vocab, "token_ids", rp::DBG_ID_RANGE)) != RP_OK) return st;
   const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
   const LayerPlan plan = plan_layer(c, (int32_t)T, Pass::kPrefix);
   if (rope_cs)
@@ -656,13 +762,13 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
     void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
     void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
     if (last_rows && l == c.n_layers - 1)
-      return run_last_rows(m, s, m->layers[l], B, cu, tab, (int32_t)T, w, tail, kl, vl, mr, h_last);
+      return dbg.end(run_last_rows(m, s, m->layers[l], B, cu, tab, (int32_t)T, w, tail, kl, vl, mr, h_last));
     st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames, mr, false,
                    nullptr, nullptr, rope_cs);
     if (st != RP_OK) return st;
   }
   RP_TRY_LAUNCH_N("prefix.gather_h_last", rp::launch_gather_rows(s, tab, w.X, c.d_model, h_last));
-  return RP_OK;
+  return dbg.end(RP_OK);
 }
 
 // Suffix pass over n_suffix sequences; sequence s reads prefix grp[s] (s when grp is
@@ -686,6 +792,9 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   const rp_dtype dt = c.dtype;
   SuffixWS w;
   suffix_ws(m, R, flags, ws, &w);
+  DebugPass dbg;
+  if ((st = dbg.begin(s, ws)) != RP_OK) return st;
+  if ((st = dbg.check_ids(response_ids, (int32_t)R, 0, c.vocab, "response_ids", rp::DBG_ID_RANGE)) != RP_OK) return st;
   const rp::SeqTable tab = make_table(n_suffix, scu, n_prefix, pcu, grp, rope0);
   RP_TRY_LAUNCH_N("suffix.embed", rp::launch_decode_embed(s, dt, response_ids, m->embed, c.vocab, (int32_t)R, c.d_model, w.L.X));
   bool norm1_done = false;
@@ -707,12 +816,12 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
     RP_TRY_LAUNCH_N("suffix.gemm_lm_head_lse", rp::launch_gemm(s, dt, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm,
                                                           c.d_model, nullptr, c.vocab, rp::EPI_LSE, 1, nullptr, &lo));
     RP_TRY_LAUNCH_N("suffix.lse_combine", rp::launch_lse_combine(s, w.lse, w.tgt, (int32_t)R, rp::lse_parts(c.vocab), logprobs));
-    return RP_OK;
+    return dbg.end(RP_OK);
   }
   RP_TRY_LAUNCH_N("suffix.gemm_lm_head", rp::launch_gemm(s, dt, (int32_t)R, c.vocab, c.d_model, w.L.N, c.d_model, blm, c.d_model, w.logits,
                                 c.vocab, rp::EPI_STORE_F32, 1, nullptr));
   RP_TRY_LAUNCH_N("suffix.logsoftmax_gather", rp::launch_logsoftmax_gather(s, w.logits, response_ids, (int32_t)R, c.vocab, logprobs));
-  return RP_OK;
+  return dbg.end(RP_OK);
 }
 
 }  // namespace
@@ -881,6 +990,9 @@ rp_status rp_prompt_logprob(const rp_model* m, void* stream, int32_t B, const in
   const rp_dtype dt = c.dtype;
   PromptWS w;
   prompt_ws(m, n_rows, flags, ws, &w);
+  DebugPass dbg;
+  if ((st = dbg.begin(s, ws)) != RP_OK) return st;
+  if ((st = dbg.check_ids(token_ids, cu[B], -1, c.vocab, "token_ids", rp::DBG_ID_RANGE)) != RP_OK) return st;
   const rp::SeqTable tab = make_table(B, cu, 0, nullptr, nullptr);
   RP_TRY_LAUNCH_N("prompt.rows", rp::launch_prompt_rows(s, dt, tab, positions, n_rows, token_ids, cu[B], hidden,
                                                         m->final_norm, c.rms_eps, c.d_model, w.N, w.tid));
@@ -891,13 +1003,13 @@ rp_status rp_prompt_logprob(const rp_model* m, void* stream, int32_t B, const in
                                                                c.d_model, nullptr, c.vocab, rp::EPI_LSE, 1, nullptr, &lo));
     RP_TRY_LAUNCH_N("prompt.lse_combine",
                     rp::launch_lse_combine(s, w.lse, w.tgt, n_rows, rp::lse_parts(c.vocab), logprobs, w.tid));
-    return RP_OK;
+    return dbg.end(RP_OK);
   }
   RP_TRY_LAUNCH_N("prompt.gemm_lm_head", rp::launch_gemm(s, dt, n_rows, c.vocab, c.d_model, w.N, c.d_model, blm,
                                                          c.d_model, w.logits, c.vocab, rp::EPI_STORE_F32, 1, nullptr));
   RP_TRY_LAUNCH_N("prompt.logsoftmax_gather",
                   rp::launch_logsoftmax_gather(s, w.logits, w.tid, n_rows, c.vocab, logprobs, true));
-  return RP_OK;
+  return dbg.end(RP_OK);
 }
 
 rp_status rp_decode_workspace_bytes(const rp_model* m, int32_t B, int32_t cap, size_t* bytes) {
@@ -939,6 +1051,11 @@ rp_status decode_run(const rp_model* m, void* stream, int32_t B, rp_kv cache, in
   DecodeWS w;
   decode_ws(m, B, cap, ws, &w, own_logits);
   float* lg = logits ? logits : w.logits;
+  DebugPass dbg;
+  rp_status st;
+  if ((st = dbg.begin(s, ws)) != RP_OK) return st;
+  if ((st = dbg.check_ids(token_ids, B, 0, c.vocab, "token_ids", rp::DBG_ID_RANGE)) != RP_OK) return st;
+  if ((st = dbg.check_ids(kv_len, B, 0, std::min(cap, c.max_position), "kv_len", rp::DBG_KV_LEN)) != RP_OK) return st;
   const int d = c.d_model, Hq = c.n_q_heads, Hkv = c.n_kv_heads, D = c.head_dim, F = c.ffn_dim;
   const int qkv = (Hq + 2 * Hkv) * D, hq = Hq * D;
   const float scale = (float)(1.0 / sqrt((double)D));
@@ -987,7 +1104,7 @@ rp_status decode_run(const rp_model* m, void* stream, int32_t B, rp_kv cache, in
   RP_TRY_LAUNCH_N("decode.gemm_lm_head", rp::launch_gemm(s, dt, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
                                 decode_splitk(c, B, c.vocab, d), w.gemm_part));
   RP_TRY_LAUNCH_N("decode.argmax", rp::launch_argmax(s, lg, B, c.vocab, next_ids));
-  return RP_OK;
+  return dbg.end(RP_OK);
 }
 
 // Library-owned scratch of rp_decode_step_static: one copy on every GPU the library

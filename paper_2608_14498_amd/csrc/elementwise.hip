@@ -855,4 +855,72 @@ hipError_t launch_decode_embed_norm(hipStream_t s, rp_dtype dt, const int32_t* i
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------------
+// Debug-mode checks (RP_DEBUG): guard bytes between workspace slices, id ranges.
+// ------------------------------------------------------------------------------------
+__device__ __forceinline__ uint8_t guard_byte(int g, int i) { return (uint8_t)(0xA5 ^ (g * 7) ^ (i * 13)); }
+
+__global__ __launch_bounds__(64) void k_debug_reset(int* rec) {
+  if (threadIdx.x < 4) rec[threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(256) void k_guard_fill(uint8_t* __restrict__ ws, GuardTable t) {
+  const int g = blockIdx.x;
+  ws[t.off[g] + threadIdx.x] = guard_byte(g, threadIdx.x);
+}
+
+__global__ __launch_bounds__(256) void k_guard_check(const uint8_t* __restrict__ ws, GuardTable t, int* rec) {
+  const int g = blockIdx.x;
+  if (ws[t.off[g] + threadIdx.x] != guard_byte(g, threadIdx.x)) {
+    if (atomicCAS(&rec[0], 0, (int)DBG_GUARD) == 0) rec[1] = g;
+  }
+}
+
+__global__ void k_guard_corrupt(uint8_t* __restrict__ ws, uint64_t off) {
+  if (threadIdx.x == 0) ws[off + 17] ^= 0xFF;
+}
+
+__global__ __launch_bounds__(256) void k_check_range(const int32_t* __restrict__ v, int n, int lo, int hi, int code,
+                                                     int* rec) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    const int x = v[i];
+    if (x < lo || x >= hi) {
+      if (atomicCAS(&rec[0], 0, code) == 0) {
+        rec[1] = i;
+        rec[2] = x;
+      }
+    }
+  }
+}
+
+hipError_t launch_debug_reset(hipStream_t s, int* rec) {
+  k_debug_reset<<<1, 64, 0, s>>>(rec);
+  return hipGetLastError();
+}
+
+hipError_t launch_guard_fill(hipStream_t s, uint8_t* ws, const GuardTable& t) {
+  if (t.n <= 0) return hipSuccess;
+  k_guard_fill<<<t.n, kGuardBytes, 0, s>>>(ws, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_guard_check(hipStream_t s, const uint8_t* ws, const GuardTable& t, int* rec) {
+  if (t.n <= 0) return hipSuccess;
+  k_guard_check<<<t.n, kGuardBytes, 0, s>>>(ws, t, rec);
+  return hipGetLastError();
+}
+
+hipError_t launch_guard_corrupt(hipStream_t s, uint8_t* ws, const GuardTable& t) {
+  if (t.n <= 0) return hipSuccess;
+  k_guard_corrupt<<<1, 64, 0, s>>>(ws, t.off[0]);
+  return hipGetLastError();
+}
+
+hipError_t launch_check_range(hipStream_t s, const int32_t* v, int32_t n, int32_t lo, int32_t hi, int code, int* rec) {
+  if (n <= 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>(((int64_t)n + 255) / 256, 1024);
+  k_check_range<<<blocks, 256, 0, s>>>(v, n, lo, hi, code, rec);
+  return hipGetLastError();
+}
+
 }  // namespace rp

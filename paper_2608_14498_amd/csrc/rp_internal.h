@@ -187,6 +187,24 @@ hipError_t launch_mfma_probe(hipStream_t s, rp_dtype dt, int32_t blocks, int32_t
 // HBM read probe over bytes (a multiple of 16) of src; sink receives blocks * 256 words.
 hipError_t launch_read_probe(hipStream_t s, const void* src, int64_t bytes, int32_t blocks, uint32_t* sink);
 
+// Debug-mode checks (RP_DEBUG): guard bytes after every workspace slice and range checks
+// of device-side ids.  rec is a device int[4]: rec[0] = first error code (0 = none),
+// rec[1], rec[2] = its details.
+struct GuardTable {
+  int32_t n;             // guards used (at most kMaxGuards)
+  uint64_t off[64];      // byte offset of each 256-byte guard from the workspace base
+};
+constexpr int kMaxGuards = 64;
+constexpr int kGuardBytes = 256;
+enum DebugCode : int { DBG_OK = 0, DBG_ID_RANGE = 1, DBG_GUARD = 2, DBG_KV_LEN = 3 };
+hipError_t launch_debug_reset(hipStream_t s, int* rec);
+hipError_t launch_guard_fill(hipStream_t s, uint8_t* ws, const GuardTable& t);
+hipError_t launch_guard_check(hipStream_t s, const uint8_t* ws, const GuardTable& t, int* rec);
+// Writes one byte into guard 0 (the host-forced overflow of the debug mode's self-test).
+hipError_t launch_guard_corrupt(hipStream_t s, uint8_t* ws, const GuardTable& t);
+// Records v[i] outside [lo, hi) as code, i, v[i] (the first one to win the record).
+hipError_t launch_check_range(hipStream_t s, const int32_t* v, int32_t n, int32_t lo, int32_t hi, int code, int* rec);
+
 // Decode step pieces.
 hipError_t launch_decode_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const void* embed,
                                int32_t vocab, int32_t B, int32_t d, float* X);

@@ -395,3 +395,24 @@ def test_static_decode_validation(lib):
         assert need <= rb.RP_DECODE_STATIC_SCRATCH_BYTES
     finally:
         rb.rp_destroy(h)
+
+
+def test_debug_mode_workspaces_hold_guards():
+    """RP_DEBUG puts a 256-byte guard after every workspace slice: the sizes grow by that
+    much per slice (read in a child process: the mode is read once per process)."""
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "from tests.test_abi_cpu import make\n"
+        "from paper_2608_14498_amd import binding as rb, configs\n"
+        "h, keep = make(configs.QWEN7B_SLICE, max_pos=8300)\n"
+        "print(rb.rp_prefix_workspace_bytes(h, 2, [0, 100, 300]), rb.rp_suffix_workspace_bytes(h, 2, [0, 100, 300], [0, 5, 9]),"
+        " rb.rp_decode_workspace_bytes(h, 4, 128))\n" % ROOT)
+    sizes = []
+    for dbg in ("0", "1"):
+        env = dict(os.environ, RP_DEBUG=dbg)
+        r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=120)
+        assert r.returncode == 0, r.stderr
+        sizes.append([int(x) for x in r.stdout.split()])
+    for plain, guarded in zip(*sizes):
+        extra = guarded - plain
+        assert extra > 0 and extra % 256 == 0 and extra // 512 >= 4, (plain, guarded)
