@@ -130,6 +130,7 @@ struct LayerWS {
   void* O;    // attention output [M, Hq*D]
   void* GU;   // [M, 2F]
   void* ACT;  // [M, F]
+  float* attn_part = nullptr;  // split-KV attention partials (suffix pass, 16-bit models)
 };
 
 // bf16 prefix/suffix layers fuse SwiGLU into the gate/up GEMM and need no [M, 2F] buffer.
@@ -359,12 +360,22 @@ bool fused_scoring(const rp_model* m, uint32_t flags) {
   return (flags & RP_SUFFIX_FUSED_LOGPROB) && half_dtype(m->cfg);
 }
 
-size_t suffix_ws(const rp_model* m, int64_t R, uint32_t flags, void* base, SuffixWS* w) {
+// Split-KV ways of the suffix attention over prefixes 0 .. n_prefix-1 (the most split).
+int32_t suffix_attn_splits(const rp_model* m, int32_t n_prefix, const int32_t* pcu) {
+  if (!half_dtype(m->cfg)) return 1;
+  int32_t S = 1;
+  for (int p = 0; p < n_prefix; ++p) S = std::max(S, (int32_t)rp::attn_splits(pcu[p + 1] - pcu[p]));
+  return S;
+}
+
+size_t suffix_ws(const rp_model* m, int64_t R, uint32_t flags, int32_t splits, void* base, SuffixWS* w) {
   Carver c(base);
   SuffixWS tmp;
   SuffixWS* s = w ? w : &tmp;
   s->plan = plan_layer(m->cfg, (int32_t)R, Pass::kSuffix);
   carve_layer(c, m->cfg, R, true, !s->plan.fused, &s->L);
+  const size_t np = rp::attn_partial_floats(R, m->cfg.n_q_heads, m->cfg.head_dim, splits);
+  s->L.attn_part = np ? (float*)c.take(np * 4) : nullptr;
   const int64_t kvrow = (int64_t)m->cfg.n_kv_heads * m->cfg.head_dim;
   s->Ks = c.take(R * kvrow * elem_size(m->cfg));
   s->Vs = c.take(R * kvrow * elem_size(m->cfg));
@@ -607,6 +618,7 @@ rp_status run_layer(const rp_model* m, hipStream_t s, const rp_layer_weights& lw
   a.Hkv = Hkv;
   a.D = D;
   a.scale = (float)(1.0 / sqrt((double)D));
+  a.part = w.attn_part;
   RP_TRY_LAUNCH_N(nm.attn, rp::launch_attention(s, dt, st, a, M));
   const rp::BSeg bo = wo_operand(c, lw);
   if (s_o > 1) {
@@ -783,7 +795,8 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   if (!h_last) return fail(RP_ERR_INVALID_ARG, "h_last is NULL");
   if (!aligned16(h_last)) return fail(RP_ERR_INVALID_ARG, "h_last must be 16-byte aligned");
   if (R > 0 && (!response_ids || !logprobs)) return fail(RP_ERR_INVALID_ARG, "response_ids and logprobs are required");
-  const size_t need = suffix_ws(m, R, flags, nullptr, nullptr);
+  const int32_t splits = suffix_attn_splits(m, n_prefix, pcu);
+  const size_t need = suffix_ws(m, R, flags, splits, nullptr, nullptr);
   if ((st = check_ws(ws, ws_bytes, need)) != RP_OK) return st;
   if (R == 0) return RP_OK;
 
@@ -791,7 +804,7 @@ rp_status suffix_run(const rp_model* m, void* stream, int32_t n_prefix, const in
   const rp_config& c = m->cfg;
   const rp_dtype dt = c.dtype;
   SuffixWS w;
-  suffix_ws(m, R, flags, ws, &w);
+  suffix_ws(m, R, flags, splits, ws, &w);
   DebugPass dbg;
   if ((st = dbg.begin(s, ws)) != RP_OK) return st;
   if ((st = dbg.check_ids(response_ids, (int32_t)R, 0, c.vocab, "response_ids", rp::DBG_ID_RANGE)) != RP_OK) return st;
@@ -927,7 +940,7 @@ rp_status rp_suffix_workspace_bytes(const rp_model* m, int32_t B, const int32_t*
   if (!m || !bytes) return fail(RP_ERR_INVALID_ARG, "model and bytes are required");
   rp_status s = check_suffix_cu(m, B, pcu, scu);
   if (s != RP_OK) return s;
-  *bytes = suffix_ws(m, scu[B], 0u, nullptr, nullptr);
+  *bytes = suffix_ws(m, scu[B], 0u, suffix_attn_splits(m, B, pcu), nullptr, nullptr);
   return RP_OK;
 }
 
@@ -947,7 +960,7 @@ rp_status rp_suffix_grouped_workspace_bytes(const rp_model* m, int32_t n_prefix,
   if (flags & ~RP_SUFFIX_FLAGS) return fail(RP_ERR_INVALID_ARG, "unknown suffix flags 0x%x", flags);
   rp_status s = check_grouped_cu(m, n_prefix, pcu, n_suffix, prefix_of_suffix, scu);
   if (s != RP_OK) return s;
-  *bytes = suffix_ws(m, scu[n_suffix], flags, nullptr, nullptr);
+  *bytes = suffix_ws(m, scu[n_suffix], flags, suffix_attn_splits(m, n_prefix, pcu), nullptr, nullptr);
   return RP_OK;
 }
 

@@ -157,7 +157,20 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   const int qpos_first = n0 + (qb.q_begin - qrow0);
   const int qpos_last = n0 + (qb.q_end - 1 - qrow0);
   const int nk = qpos_last + 1;  // keys needed by this block
-  const int ntiles = (nk + KT - 1) / KT;
+  // Key tiles t_begin .. t_end-1 of this block.  Split-KV: a sequence with n0 first-
+  // segment keys has nsp = attn_splits(n0) splits; split sp takes its share of the P
+  // tiles that lie wholly in the first segment, and the last split also the rest (the
+  // boundary tile and the causal keys), so it is the longest and runs at blockIdx.y 0.
+  // Every split holds at least one tile (P / nsp >= RP_ATTN_SPLIT_KEYS / KT).
+  int t_begin = 0, t_end = (nk + KT - 1) / KT, sp = 0;
+  const int nsp = a.part ? attn_splits(n0) : 1;
+  if ((int)blockIdx.y >= nsp) return;
+  if (nsp > 1) {
+    sp = nsp - 1 - (int)blockIdx.y;
+    const int P = n0 / KT, per = (P + nsp - 1) / nsp;
+    t_begin = sp * per;
+    if (sp < nsp - 1) t_end = t_begin + per;
+  }
 
   // Key segments as buffer resources: segment 0 = the n0 prefix rows, segment 1 = the
   // nq rows of the queries; key kv of segment s is at byte (kv - start_s) * row_bytes.
@@ -254,7 +267,7 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   // is computed from (Kc, Vc); the closing barrier (which waits for this wave's loads)
   // makes them visible to every wave.
   auto tile = [&](const u32x4_t* Kc, const u32x4_t* Vc, u32x4_t* Kn, u32x4_t* Vn, int t) __attribute__((always_inline)) {
-    if (t + 1 < ntiles) FA_LOAD(Kn, Vn, t + 1);
+    if (t + 1 < t_end) FA_LOAD(Kn, Vn, t + 1);
 
     // ---- S^T = K Q^T: s[qi][kb][e] = score(key t*KT + kb*32 + 8(e/4) + 4 fk + e%4, query fr) ----
     f32x16_t s[QW][KB];
@@ -346,19 +359,36 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
     __syncthreads();
   };
 
-  FA_LOAD(Ks0, Vs0, 0);
+  FA_LOAD(Ks0, Vs0, t_begin);
   __syncthreads();
-  int t = 0;
-  for (; t + 2 <= ntiles; t += 2) {
+  int t = t_begin;
+  for (; t + 2 <= t_end; t += 2) {
     tile(Ks0, Vs0, Ks1, Vs1, t);
     tile(Ks1, Vs1, Ks0, Vs0, t + 1);
   }
-  if (t < ntiles) tile(Ks0, Vs0, Ks1, Vs1, t);
+  if (t < t_end) tile(Ks0, Vs0, Ks1, Vs1, t);
 #undef FA_DMA
 #undef FA_LOAD_SEG
 #undef FA_LOAD
 
   // ---- normalise and store: o[qi][db][e] = O^T(dh = db*32 + 8(e/4) + 4 fk + e%4, query fr) ----
+  if (nsp > 1) {  // split partial: (max in log2 units, sum, unnormalised o)
+#pragma unroll
+    for (int qi = 0; qi < QW; ++qi) {
+      const int qrow = qb.q_begin + (wave * QW + qi) * 32 + fr;
+      const float l = l_run[qi] + __shfl_xor(l_run[qi], 32, kWave);
+      if (qrow >= qb.q_end) continue;
+      float* pp = a.part + (((int64_t)qrow * a.Hq + h) * gridDim.y + sp) * (D + 4);
+      if (fk == 0) *reinterpret_cast<float2*>(pp) = make_float2(m_run[qi], l);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4)
+          *reinterpret_cast<float4*>(pp + 4 + db * 32 + 8 * e4 + 4 * fk) =
+              make_float4(o[qi][db][4 * e4], o[qi][db][4 * e4 + 1], o[qi][db][4 * e4 + 2], o[qi][db][4 * e4 + 3]);
+    }
+    return;
+  }
 #pragma unroll
   for (int qi = 0; qi < QW; ++qi) {
     const int qrow = qb.q_begin + (wave * QW + qi) * 32 + fr;
@@ -441,6 +471,45 @@ __global__ __launch_bounds__(64) void k_attn_f32(SeqTable st, AttnArgs a) {
   }
 }
 
+// Merge of split-KV partials: one wave per (query row, q head), lane i holding head
+// dimensions i*D/64 ..; rows of sequences that did not split were written by the
+// attention kernel.  Partial s of (row, head) is at ((row*Hq + head)*S + s)*(D + 4):
+// max (log2 units), sum, two pad floats, unnormalised o[D].
+template <typename T16, int D>
+__global__ __launch_bounds__(256) void k_attn_split_merge(SeqTable st, const float* __restrict__ part, int S, int Hq,
+                                                          int64_t items, T16* __restrict__ o) {
+  typedef Half16<T16> H;
+  constexpr int PER = D / 64;
+  const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= items) return;
+  const int lane = threadIdx.x & 63;
+  const int nsp = attn_splits(st.pos0(seq_of_row(st, (int)(item / Hq))));
+  if (nsp == 1) return;
+  const float* p = part + item * S * (D + 4);
+  float M = -INFINITY;
+  for (int sp = 0; sp < nsp; ++sp) M = fmaxf(M, p[(int64_t)sp * (D + 4)]);
+  float L = 0.f, acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  for (int sp = 0; sp < nsp; ++sp) {
+    const float* ps = p + (int64_t)sp * (D + 4);
+    const float w = __builtin_amdgcn_exp2f(ps[0] - M);
+    L = fmaf(ps[1], w, L);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] = fmaf(ps[4 + lane * PER + e], w, acc[e]);
+  }
+  const float inv = 1.0f / L;
+  T16* op = o + item * D + lane * PER;
+  if constexpr (PER == 2)
+    *reinterpret_cast<uint32_t*>(op) = H::pack2(acc[0] * inv, acc[1] * inv);
+  else
+    stf(op, acc[0] * inv);
+}
+
+size_t attn_partial_floats(int64_t R, int32_t Hq, int32_t D, int32_t max_splits) {
+  return max_splits > 1 ? (size_t)R * Hq * max_splits * (D + 4) : 0;
+}
+
 int count_qblocks(const SeqTable& st, int BQ) {
   int n = 0;
   for (int b = 0; b < st.n; ++b) n += (st.q_cu[b + 1] - st.q_cu[b] + BQ - 1) / BQ;
@@ -466,28 +535,44 @@ hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, cons
       const int64_t keys = (int64_t)st.pos0(b) + (st.q_cu[b + 1] - st.q_cu[b]);
       if ((keys + 64) * a.Hkv * a.D * 2 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
     }
+    int S = 1;  // split-KV ways of the most split sequence (grid y)
+    if (a.part)
+      for (int b = 0; b < st.n; ++b) S = std::max(S, attn_splits(st.pos0(b)));
+    AttnArgs as = a;
+    if (S == 1) as.part = nullptr;
+    hipError_t e = hipSuccess;
     with_half16(dt, [&](auto tag_) {
       using H = decltype(tag_);
       // Long sequences: 8 waves (256 queries) share each K/V tile, halving the tile loads
-      // per query; shorter ones keep 4 waves, whose smaller blocks balance better.  Each
-      // query sees the same key tiles in the same order either way (same results).
+      // per query; shorter ones keep 4 waves, whose smaller blocks balance better (also
+      // measured faster for split suffix passes).  Each query sees the same key tiles in
+      // the same order either way (same results).
       int max_q = 0;
       for (int b = 0; b < st.n; ++b) max_q = std::max(max_q, st.q_cu[b + 1] - st.q_cu[b]);
       const FaMap fm = fa_map(a.Hq, a.Hkv);
       if (max_q >= 8192) {
-        const int grid = fa_grid(fm, count_qblocks(st, 256), a.Hq);
+        const dim3 grid(fa_grid(fm, count_qblocks(st, 256), a.Hq), S);
         if (a.D == 128)
-          k_attn_bf16<H, 128, 1, 64, 8><<<grid, 512, 0, s>>>(st, a);
+          k_attn_bf16<H, 128, 1, 64, 8><<<grid, 512, 0, s>>>(st, as);
         else
-          k_attn_bf16<H, 64, 1, 64, 8><<<grid, 512, 0, s>>>(st, a);
+          k_attn_bf16<H, 64, 1, 64, 8><<<grid, 512, 0, s>>>(st, as);
       } else {
-        const int grid = fa_grid(fm, count_qblocks(st, 128), a.Hq);
+        const dim3 grid(fa_grid(fm, count_qblocks(st, 128), a.Hq), S);
         if (a.D == 128)
-          k_attn_bf16<H, 128, 1, 64><<<grid, 256, 0, s>>>(st, a);
+          k_attn_bf16<H, 128, 1, 64><<<grid, 256, 0, s>>>(st, as);
         else
-          k_attn_bf16<H, 64, 1, 64><<<grid, 256, 0, s>>>(st, a);
+          k_attn_bf16<H, 64, 1, 64><<<grid, 256, 0, s>>>(st, as);
+      }
+      if (S > 1 && (e = hipGetLastError()) == hipSuccess) {
+        const int64_t items = (int64_t)total_q * a.Hq;
+        const int mgrid = (int)((items + 3) / 4);
+        if (a.D == 128)
+          k_attn_split_merge<H, 128><<<mgrid, 256, 0, s>>>(st, as.part, S, a.Hq, items, (H*)a.o);
+        else
+          k_attn_split_merge<H, 64><<<mgrid, 256, 0, s>>>(st, as.part, S, a.Hq, items, (H*)a.o);
       }
     });
+    if (e != hipSuccess) return e;
   } else {
     const int nqb = count_qblocks(st, 64);
     if (a.D == 128)

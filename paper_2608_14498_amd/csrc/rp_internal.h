@@ -177,7 +177,23 @@ struct AttnArgs {
   void* o;
   int32_t Hq, Hkv, D;
   float scale;
+  // Split-KV (16-bit models): when set, a sequence whose first key segment holds n0 rows
+  // splits its keys attn_splits(n0) ways; the splits write (max, sum, unnormalised o)
+  // partials here and a merge kernel writes o.  attn_partial_floats() floats.
+  float* part = nullptr;
 };
+// Key splits of a sequence with n0 first-segment keys: a function of n0 alone, so a
+// sequence's result does not depend on the sequences packed with it.
+#ifndef RP_ATTN_SPLIT_KEYS
+#define RP_ATTN_SPLIT_KEYS 4096
+#endif
+constexpr int kAttnMaxSplits = 8;
+__host__ __device__ inline int attn_splits(int n0) {
+  const int sp = n0 / RP_ATTN_SPLIT_KEYS;
+  return sp < 1 ? 1 : (sp > kAttnMaxSplits ? kAttnMaxSplits : sp);
+}
+// Partial floats for R query rows whose sequences split at most max_splits ways.
+size_t attn_partial_floats(int64_t R, int32_t Hq, int32_t D, int32_t max_splits);
 hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, const AttnArgs& a,
                             int32_t total_q);
 

@@ -105,6 +105,54 @@ def test_packing_is_bitwise_invariant(model):
         assert np.array_equal(lp[cs[b]:cs[b + 1]], lp1)
 
 
+@pytest.mark.parametrize("model", [BF16_SMALL, F16_D64])
+def test_split_kv_suffix_matches_oracle_and_is_bitwise_invariant(model):
+    """Prefixes long enough that the suffix attention splits each sequence's keys (4096
+    keys a split: 1, 1, 3 and 2 ways here) next to ones that do not split.  Matches the
+    oracle; each sequence run alone gives bitwise its packed result (the split count is a
+    function of the sequence's prefix length alone); and responses scored against a
+    shared prefix equal bitwise the plain pass over a copy of it."""
+    from paper_2608_14498_amd.runtime import DeviceModel, to_device
+    P, Vis, S = [4100, 300, 12300, 8300], [0, 0, 0, 0], [130, 5, 300, 1]
+    w = configs.custom(model, P, Vis, S, index=67)
+    hw = inputs.make_weights(w, norm="random", bias=True)
+    bt = inputs.make_batch(w)
+    maxp = max(P) + max(S) + 1
+    K, V, H, lp = gpu_run(w, hw, bt, max_position=maxp)
+    for b in range(len(P)):
+        cp, cs = bt.cu_prefix, bt.cu_suffix
+        one = inputs.HostBatch([P[b]], [0], [S[b]], np.array([0, P[b]], np.int32), np.array([0, S[b]], np.int32),
+                               bt.token_ids[cp[b]:cp[b + 1]], bt.visual[:0], bt.response_ids[cs[b]:cs[b + 1]])
+        k1, v1, h1, lp1 = gpu_run(w, hw, one, max_position=maxp)
+        assert np.array_equal(lp[cs[b]:cs[b + 1]], lp1), b
+        assert np.array_equal(H[b], h1[0]), b
+    # two responses on prefix 2 and one on prefix 3, grouped vs over copies of the prefix
+    dm = DeviceModel(hw, maxp)
+    dev = dm.device
+    cp = [int(x) for x in bt.cu_prefix]
+    Kd, Vd, hd = dm.prefix(cp, to_device(bt.token_ids, dev), None)
+    grp, lens = [2, 3, 2], [40, 7, 129]
+    gcs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    resp = np.random.default_rng(68).integers(0, model.vocab, int(gcs[-1])).astype(np.int32)
+    rd = to_device(resp, dev)
+    lpg = dm.suffix_grouped(cp, grp, gcs.tolist(), Kd, Vd, hd, rd)
+    Kc = torch.cat([Kd[:, cp[g]:cp[g + 1]] for g in grp], dim=1).contiguous()
+    Vc = torch.cat([Vd[:, cp[g]:cp[g + 1]] for g in grp], dim=1).contiguous()
+    hc = hd[torch.as_tensor(grp, device=dev).long()].contiguous()
+    ccu = np.concatenate([[0], np.cumsum([P[g] for g in grp])]).astype(np.int32).tolist()
+    lpc = dm.suffix(ccu, gcs.tolist(), Kc, Vc, hc, rd)
+    torch.cuda.synchronize()
+    assert torch.equal(lpg, lpc)
+    dm.close()
+    ref = oracle_run(w, hw, bt)
+    name = f"split-KV {model.dtype} D={model.head_dim}"
+    r = _report(name, K, V, H, lp, *ref)
+    assert r["kv"] <= 3e-2 and r["h"] <= 3e-2
+    chk = TargetCheck(model.dtype)
+    chk.check(name, lp, ref[3], lambda: emulated_suffix(w, hw, bt))
+    chk.finish()
+
+
 # A GPU run that included the bf16 decode step at head_dim 64 and the last-rows-only
 # prefix at head_dim 64 with 1-D positions faulted (illegal memory access) and no cause has
 # been shown; the library returns RP_ERR_UNSUPPORTED for both until one is, and these cases
