@@ -250,9 +250,11 @@ rp::SeqTable make_table(int32_t B, const int32_t* q_cu, int32_t n_k, const int32
   return t;
 }
 
-// split-K factor for small-M GEMMs (decode): aim for >= 2 workgroups per CU.
+// split-K factor for small-M GEMMs (decode): up to 64 rows the skinny kernel's (about
+// four waves per CU); beyond, >= 2 workgroups of 256x256 tiles per CU.
 int decode_splitk(const rp_config& cfg, int32_t M, int32_t N, int32_t K) {
   if (!half_dtype(cfg)) return 1;
+  if (M <= 64 && K % 64 == 0) return rp::gemm_skinny_splitk(M, N, K);
   const int tiles = ((M + 255) / 256) * ((N + 255) / 256);
   int s = (512 + tiles - 1) / tiles;
   s = s < 1 ? 1 : s;

@@ -889,23 +889,35 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
     }
     __builtin_amdgcn_sched_barrier(0);
   };
-  // tile t reads stage t % 3; after it, the stage is refilled with tile t + 3 (tiles past
-  // the chunk's last key read as zeros and are never used)
+  // Tile t reads stage t % 3; after it, the stage is refilled with tile t + 3 (rows past
+  // the chunk's last key read as zeros and are never used).  The prologue and the steady
+  // loop issue every load unconditionally (a short chunk re-reads its last tile), so the
+  // compiler counts exactly which loads a stage waits for and the later ones stay in
+  // flight; only the last few tiles (no loop) take branches.
+  // The query fragments are in registers before the first copy is issued: a loop whose
+  // loads fill only LDS but which reads registers still loading from before it makes the
+  // compiler drain every load (these copies included) ahead of the loop.
+  __builtin_amdgcn_s_waitcnt(0);
   DM_LOAD(Ks0, Vs0, 0);
-  DM_LOAD(Ks1, Vs1, 1);
-  DM_LOAD(Ks2, Vs2, 2);
-  for (int t = 0; t < ntiles; t += 3) {
+  DM_LOAD(Ks1, Vs1, min(1, ntiles - 1));
+  DM_LOAD(Ks2, Vs2, min(2, ntiles - 1));
+  int t = 0;
+  for (; t + 6 <= ntiles; t += 3) {
     tile(Ks0, Vs0, t);
-    if (t + 3 < ntiles) { DM_LOAD(Ks0, Vs0, t + 3); }
-    if (t + 1 < ntiles) {
-      tile(Ks1, Vs1, t + 1);
-      if (t + 4 < ntiles) { DM_LOAD(Ks1, Vs1, t + 4); }
-    }
-    if (t + 2 < ntiles) {
-      tile(Ks2, Vs2, t + 2);
-      if (t + 5 < ntiles) { DM_LOAD(Ks2, Vs2, t + 5); }
-    }
+    DM_LOAD(Ks0, Vs0, t + 3);
+    tile(Ks1, Vs1, t + 1);
+    DM_LOAD(Ks1, Vs1, t + 4);
+    tile(Ks2, Vs2, t + 2);
+    DM_LOAD(Ks2, Vs2, t + 5);
   }
+  const int r = ntiles - t;  // 1 .. 5 tiles left, t .. t+2 in (or on their way to) the stages
+  tile(Ks0, Vs0, t);
+  if (r > 3) { DM_LOAD(Ks0, Vs0, t + 3); }
+  if (r > 1) tile(Ks1, Vs1, t + 1);
+  if (r > 4) { DM_LOAD(Ks1, Vs1, t + 4); }
+  if (r > 2) tile(Ks2, Vs2, t + 2);
+  if (r > 3) tile(Ks0, Vs0, t + 3);
+  if (r > 4) tile(Ks1, Vs1, t + 4);
 #undef DM_LOAD
   __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the wave
   // o[db][e] = O^T(dim db*32 + 8(e/4) + 4 fk + e%4, head fr), unnormalised

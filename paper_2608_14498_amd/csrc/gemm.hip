@@ -944,6 +944,245 @@ static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, b
     k_gemm_bf16<EPI, T16, 4, BT><<<grid, 512, 0, s>>>(g);
 }
 
+// ------------------------------------------------------------------------------------
+// Skinny GEMM: at most 64 rows of A (a decode batch, the last rows of a prefix), 16-bit.
+// Such a product reads each weight once and is bound by HBM bandwidth, so the weights
+// are streamed, not tiled for reuse.  A workgroup of SW waves owns 32*SW adjacent
+// columns (32 per wave) and one K split, and walks the split's 64-deep k slabs through a
+// 3-stage LDS ring filled by direct global->LDS loads: per stage one A slab (the few
+// rows, copied once and shared by the waves; rows past M repeat row M-1 and their
+// results are dropped) and each wave's 32 B rows (8 lanes read a whole 128-byte row
+// segment).  Per slab t: wait for this wave's copies of slab t (those of t+1 stay in
+// flight), barrier (every wave's copies of t have landed and every wave is done with the
+// stage that takes t+2), issue the copies of t+2, then the MFMAs of t.  The steady state
+// issues every copy unconditionally (past the end it re-reads the last slab), so the
+// outstanding count is known statically.  The MFMA takes the B fragment first and each
+// fragment has the k order of the tiled kernels, so every output is the MFMA chain it is
+// there (the same bits).  A transposed B ([K][N] storage) is staged k-row-major and read
+// with ds_read_b64_tr_b16 into the same fragments.  Output fp32 [split][M][ldo]
+// (partials), or C itself (stored or accumulated) for one split.
+// ------------------------------------------------------------------------------------
+struct SkinnyArgs {
+  int M, N, K;
+  const void* A;
+  int lda;
+  BSeg B;
+  int ldb;
+  float* out;
+  int ldo;
+  int64_t plane;  // elements between splits of out
+  int k_chunk;
+  int add;        // accumulate into out (one split)
+};
+
+template <typename T16, int RF, bool BT, int SW>
+__global__ __launch_bounds__(SW * 64) void k_gemm_skinny(SkinnyArgs g) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef __attribute__((address_space(3))) void lds_void;
+  typedef typename Half16<T16>::V8 V8;
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  constexpr int ACH = RF * 32 * 8;   // A chunks per stage: RF*32 rows x 8 chunks of 16 bytes
+  constexpr int BCH = 32 * 8;        // B chunks per wave per stage: 32 columns x 64 k
+  constexpr int AL = ACH / 64 / SW;  // A copy instructions per wave per stage
+  constexpr int BL = BCH / 64;       // B copy instructions per wave per stage
+  constexpr int L = AL + BL;         // copies per wave per stage
+  static_assert(AL >= 1 && ACH % (64 * SW) == 0, "A stage split over the waves");
+  __shared__ u32x4_t As0[ACH], As1[ACH], As2[ACH];
+  __shared__ u32x4_t Bs0[SW * BCH], Bs1[SW * BCH], Bs2[SW * BCH];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int fr = lane & 31, fk = lane >> 5;
+  const int nw0 = (blockIdx.x * SW + wave) * 32;  // first column of this wave
+  const int kbeg = blockIdx.y * g.k_chunk;
+  const int nst = (min(g.K, kbeg + g.k_chunk) - kbeg) / 64;  // >= 1 (the host sizes the splits)
+
+  // copy sources: byte offsets into A's buffer resource and into that of the B segment
+  // holding the instruction's rows (the host checked that they fit 32 bits)
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc((void*)g.A, 0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsB0 = __builtin_amdgcn_make_buffer_rsrc((void*)g.B.b0, 0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsB1 = __builtin_amdgcn_make_buffer_rsrc((void*)g.B.b1, 0, -1, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsB2 = __builtin_amdgcn_make_buffer_rsrc((void*)g.B.b2, 0, -1, 0x00020000);
+  uint32_t aoff[AL], boff[BL];
+  __amdgpu_buffer_rsrc_t rsB[BL];
+#pragma unroll
+  for (int i = 0; i < AL; ++i) {
+    const int q = (wave * AL + i) * 64 + lane, row = q / 8, lc = (q % 8) ^ swz(row);
+    aoff[i] = 2u * ((uint32_t)min(row, g.M - 1) * (uint32_t)g.lda + (uint32_t)(kbeg + lc * 8));
+  }
+#pragma unroll
+  for (int i = 0; i < BL; ++i) {
+    const int q = i * 64 + lane;
+    if (BT) {  // k row q/4 of the slab, 4 chunks of 8 columns; columns past N re-read the last chunk
+      const int kr = q / 4, lc = q % 4;
+      rsB[i] = rsB0;
+      boff[i] = 2u * ((uint32_t)(kbeg + kr) * (uint32_t)g.ldb + (uint32_t)min(nw0 + lc * 8, g.N - 8));
+    } else {  // column row q/8 (clamped to the last column), 8 rows per instruction
+      const int row = q / 8, lc = (q % 8) ^ swz(row);
+      const int r0 = min(nw0 + i * 8, g.N - 1), r = min(nw0 + row, g.N - 1);
+      const int seg = r0 < g.B.n1 ? 0 : r0 < g.B.n2 ? 1 : 2;
+      rsB[i] = seg == 0 ? rsB0 : seg == 1 ? rsB1 : rsB2;
+      const int sbeg = seg == 0 ? 0 : seg == 1 ? g.B.n1 : g.B.n2;
+      boff[i] = 2u * ((uint32_t)(r - sbeg) * (uint32_t)g.ldb + (uint32_t)(kbeg + lc * 8));
+    }
+  }
+  const uint32_t bstep = BT ? 64u * 2u * (uint32_t)g.ldb : 64u * 2u;
+  // transposed fragment reads: lane 16 gq + p addresses k row 8 (gq/2) + p/4 (+4 for the
+  // second read) at column 16 (gq%2) + 4 (p%4) of this wave's 32 columns
+  int btk = 0, btc = 0;
+  if (BT) {
+    const int gq = lane >> 4, p = lane & 15;
+    btk = 8 * (gq >> 1) + (p >> 2);
+    btc = 16 * (gq & 1) + 4 * (p & 3);
+  }
+
+  f32x16_t acc[RF];
+#pragma unroll
+  for (int rf = 0; rf < RF; ++rf)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[rf][e] = 0.f;
+
+  auto load = [&](u32x4_t* Ad, u32x4_t* Bd, int t) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < AL; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)(Ad + (wave * AL + i) * 64), 16,
+                                               aoff[i] + (uint32_t)t * 128u, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < BL; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB[i], (lds_void*)(Bd + wave * BCH + i * 64), 16,
+                                               boff[i] + (uint32_t)t * bstep, 0, 0, 0);
+  };
+  auto slab = [&](const u32x4_t* Ac, const u32x4_t* Bc) __attribute__((always_inline)) {
+    const u32x4_t* Bw = Bc + wave * BCH;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      V8 bf;
+      if (BT) {
+        const T16* base = reinterpret_cast<const T16*>(Bw);
+        const int kr = ks * 16 + btk;
+        const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + kr * 32 + btc));
+        const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + (kr + 4) * 32 + btc));
+        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        bf = Half16<T16>::as_v8(make_uint4(l2.x, l2.y, h2.x, h2.y));
+      } else {
+        bf = __builtin_bit_cast(V8, Bw[fr * 8 + ((ks * 2 + fk) ^ swz(fr))]);
+      }
+#pragma unroll
+      for (int rf = 0; rf < RF; ++rf) {
+        const int row = rf * 32 + fr;
+        const V8 af = __builtin_bit_cast(V8, Ac[row * 8 + ((ks * 2 + fk) ^ swz(row))]);
+        acc[rf] = Half16<T16>::mma(bf, af, acc[rf]);
+      }
+    }
+  };
+  // Wait for this wave's copies of the slab about to be read (exactly L copies, those of
+  // the next slab, may stay outstanding) and for its LDS reads, then the barrier.  The
+  // asm also keeps the compiler from moving LDS accesses across the barrier.
+#define SK_STEP(AC_, BC_, AN_, BN_, tt_)                                                \
+  {                                                                                     \
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(L) : "memory");    \
+    load(AN_, BN_, min((tt_) + 2, nst - 1));                                            \
+    if ((tt_) < nst) slab(AC_, BC_);                                                    \
+  }
+  load(As0, Bs0, 0);
+  load(As1, Bs1, min(1, nst - 1));
+  for (int t = 0; t < nst; t += 3) {
+    SK_STEP(As0, Bs0, As2, Bs2, t);
+    SK_STEP(As1, Bs1, As0, Bs0, t + 1);
+    SK_STEP(As2, Bs2, As1, Bs1, t + 2);
+  }
+#undef SK_STEP
+  __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the wave
+
+  // acc[rf][e] = C(row rf*32 + fr, column nw0 + 8 (e/4) + 4 fk + e%4)
+  float* outp = g.out + (int64_t)blockIdx.y * g.plane;
+  const bool vec = (g.ldo & 3) == 0 && ((uintptr_t)g.out & 15) == 0 && (g.plane & 3) == 0;
+#pragma unroll
+  for (int rf = 0; rf < RF; ++rf) {
+    const int m = rf * 32 + fr;
+    if (m >= g.M) continue;
+    float* row = outp + (int64_t)m * g.ldo;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const float v[4] = {acc[rf][4 * q4], acc[rf][4 * q4 + 1], acc[rf][4 * q4 + 2], acc[rf][4 * q4 + 3]};
+      const int n = nw0 + 8 * q4 + 4 * fk;
+      if (g.add)
+        store4<true>(row, n, g.N, v, vec);
+      else
+        store4<false>(row, n, g.N, v, vec);
+    }
+  }
+#endif
+}
+
+// Waves per workgroup of the skinny GEMM (32 columns each; they share the A slabs).
+// Four measured best at every decode shape: the shared A slab costs less per weight
+// byte, and the LDS (72 KiB a workgroup) still holds two workgroups per CU.
+constexpr int kSkinnyWaves = 4;
+
+#ifndef RP_SKINNY_BLOCKS
+#define RP_SKINNY_BLOCKS 512
+#endif
+int32_t gemm_skinny_splitk(int32_t M, int32_t N, int32_t K) {
+  if (M > 64 || K % 64) return 1;
+  const int cols = 32 * kSkinnyWaves;
+  const int tiles = (N + cols - 1) / cols;
+  const int s = (RP_SKINNY_BLOCKS + tiles - 1) / tiles;   // about two workgroups per CU
+  const int cap = std::max(1, std::min(16, K / 64 / 4));  // at least 4 slabs per split
+  return std::max(1, std::min(s, cap));
+}
+
+// Operands the skinny kernel takes (16-bit, as launch_gemm validated them).
+static bool skinny_setup(const GemmArgs& g, Epi epi, bool split) {
+  if (g.M > 64 || g.K % 64 || (g.lda & 7) || ((uintptr_t)g.A & 15)) return false;
+  if (((uint64_t)(g.M - 1) * (uint64_t)g.lda + (uint64_t)g.K) * 2u > 0xFFFFFF00ull) return false;
+  if (!(epi == EPI_PARTIALS || ((epi == EPI_STORE_F32 || epi == EPI_ADD_F32) && !split) || split)) return false;
+  if (epi == EPI_SWIGLU || epi == EPI_LSE || epi == EPI_ROPE) return false;
+  if (g.B.trans)
+    return !((g.N & 7) || (g.ldb & 7) || ((uintptr_t)g.B.b0 & 15)) &&
+           ((uint64_t)(g.K - 1) * (uint64_t)g.ldb + (uint64_t)g.N) * 2u <= 0x7FFFFF00ull;
+  const int64_t start[3] = {0, g.B.n1, g.B.n2};
+  const int64_t end[3] = {g.B.n1, g.B.n2, g.N};
+  for (int k = 0; k < 3; ++k) {
+    const int64_t rows = std::min<int64_t>(end[k], g.N) - start[k];
+    if (rows <= 0) continue;
+    if (k > 0 && start[k] % 8 != 0) return false;
+    if (((uint64_t)(rows - 1) * (uint64_t)g.ldb + (uint64_t)g.K) * 2u > 0xFFFFFF00ull) return false;
+  }
+  return true;
+}
+
+template <typename T16, bool BT, int SW>
+static void launch_skinny_w(hipStream_t s, const SkinnyArgs& a, dim3 grid) {
+  if (a.M <= 32)
+    k_gemm_skinny<T16, 1, BT, SW><<<grid, SW * 64, 0, s>>>(a);
+  else
+    k_gemm_skinny<T16, 2, BT, SW><<<grid, SW * 64, 0, s>>>(a);
+}
+
+template <typename T16>
+static void launch_skinny(hipStream_t s, const GemmArgs& g, int splitk, float* out, int ldo, int64_t plane,
+                          bool add) {
+  SkinnyArgs a;
+  a.M = g.M;
+  a.N = g.N;
+  a.K = g.K;
+  a.A = g.A;
+  a.lda = g.lda;
+  a.B = g.B;
+  a.ldb = g.ldb;
+  a.out = out;
+  a.ldo = ldo;
+  a.plane = plane;
+  a.k_chunk = g.k_chunk;
+  a.add = add ? 1 : 0;
+  constexpr int SW = kSkinnyWaves;
+  const dim3 grid((g.N + 32 * SW - 1) / (32 * SW), splitk);
+  if (g.B.trans)
+    launch_skinny_w<T16, true, SW>(s, a, grid);
+  else
+    launch_skinny_w<T16, false, SW>(s, a, grid);
+}
+
 int32_t gemm_effective_splitk(rp_dtype dt, int32_t K, int32_t splitk) {
   const int bk = dt != RP_F32 ? GB_K : GF_K;
   const int kblocks = (K + bk - 1) / bk;
@@ -992,7 +1231,16 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
   splitk = (K + g.k_chunk - 1) / g.k_chunk;
   // EPI_PARTIALS: the partials epilogue even for one split, and no reduction here
   const bool split = splitk > 1 || epi == EPI_PARTIALS;
-  if (half) {
+  if (half && skinny_setup(g, epi, split)) {
+    // split: partials (summed by the caller, or by the reduction below); else C itself
+    with_half16(dt, [&](auto tag_) {
+      using H = decltype(tag_);
+      if (split)
+        launch_skinny<H>(s, g, splitk, partials, N, (int64_t)M * N, false);
+      else
+        launch_skinny<H>(s, g, 1, (float*)C, ldc, 0, epi == EPI_ADD_F32);
+    });
+  } else if (half) {
     g.tiles_m = (M + GB_M - 1) / GB_M;
     g.tiles_n = epi == EPI_SWIGLU ? (N + 127) / 128 : (N + GB_N - 1) / GB_N;
     dim3 grid(g.tiles_m * g.tiles_n, splitk);

@@ -69,6 +69,8 @@ struct RopeOut {
 };
 // Number of K splits launch_gemm actually uses for a requested splitk.
 int32_t gemm_effective_splitk(rp_dtype dt, int32_t K, int32_t splitk);
+// Split-K factor suited to launch_gemm's skinny kernel (16-bit, M <= 64 rows, K % 64 == 0).
+int32_t gemm_skinny_splitk(int32_t M, int32_t N, int32_t K);
 
 // Outputs of the EPI_LSE epilogue (an lm_head GEMM whose logits are never stored):
 // lse[m * n_part + p] = (max, sum of 2^(x log2 e - max)) over column block p of row m, in

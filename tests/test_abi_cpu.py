@@ -387,7 +387,13 @@ def test_static_decode_validation(lib):
             return status_of(rb.rp_decode_step_static, h, None, B, cache, cap, FAKE, FAKE + 256, logits, next_ids)
         st, msg = call(256, 8256)
         assert st == rb.RP_ERR_WORKSPACE and "static scratch" in msg
-        st, msg = call(64, 8256, logits=None)   # the logits would need 37 MiB more
+        # a batch whose scratch fits only without the [B, V] logits: with logits=None the
+        # library would keep them in the scratch, and says so
+        lim = rb.RP_DECODE_STATIC_SCRATCH_BYTES
+        fits = [B for B in range(8, 257, 8)
+                if rb.rp_decode_workspace_bytes(h, B, 8256) - B * m.vocab * 4 <= lim < rb.rp_decode_workspace_bytes(h, B, 8256)]
+        assert fits
+        st, msg = call(fits[-1], 8256, logits=None)
         assert st == rb.RP_ERR_WORKSPACE and "logits" in msg
         assert call(64, 8256, next_ids=None)[0] == rb.RP_ERR_INVALID_ARG
         assert call(0, 8256)[0] == rb.RP_ERR_SHAPE
