@@ -940,22 +940,42 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
 #endif
 }
 
+// Merge of the decode chunks: one wave per (sequence, q head).  Lane c holds chunk c's
+// (max, sum) (chunks with keys come first; the rest have max -inf and stale o, never
+// read), the wave reduces them, and each lane then sums its D/64 head dimensions over the
+// chunks with every chunk's weight taken from its lane, all loads independent.
 template <typename T, int D>
-__global__ __launch_bounds__(D) void k_decode_attn_merge(const float* __restrict__ part, int nchunks,
-                                                         int Hq, T* __restrict__ o) {
-  const int bh = blockIdx.x;
-  const float* p = part + (int64_t)bh * nchunks * (D + 2);
+__global__ __launch_bounds__(256) void k_decode_attn_merge(const float* __restrict__ part, int nchunks, int items,
+                                                           T* __restrict__ o) {
+  constexpr int PER = D / 64;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (item >= items) return;
+  const float* p = part + (int64_t)item * nchunks * (D + 2);
   float M = -INFINITY;
-  for (int c = 0; c < nchunks; ++c) M = fmaxf(M, p[(int64_t)c * (D + 2)]);
-  float L = 0.f, acc = 0.f;
-  for (int c = 0; c < nchunks; ++c) {
-    const float mc = p[(int64_t)c * (D + 2)];
-    if (mc == -INFINITY) continue;
-    const float wgt = expf(mc - M);
-    L += p[(int64_t)c * (D + 2) + 1] * wgt;
-    acc += p[(int64_t)c * (D + 2) + 2 + threadIdx.x] * wgt;
+  for (int c = lane; c < nchunks; c += 64) M = fmaxf(M, p[(int64_t)c * (D + 2)]);
+  M = wave_max(M);
+  float L = 0.f, acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  for (int c0 = 0; c0 < nchunks; c0 += 64) {
+    const int c = c0 + lane;
+    const float mc = c < nchunks ? p[(int64_t)c * (D + 2)] : -INFINITY;
+    const bool has = mc > -INFINITY;
+    const float w = has ? expf(mc - M) : 0.f;
+    L += has ? w * p[(int64_t)c * (D + 2) + 1] : 0.f;
+    const int nv = __popcll(__ballot(has));  // chunks with keys: a prefix of c0 ..
+#pragma unroll 4
+    for (int j = 0; j < nv; ++j) {
+      const float wj = __shfl(w, j, kWave);
+      const float* oc = p + (int64_t)(c0 + j) * (D + 2) + 2 + lane * PER;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] = fmaf(wj, oc[e], acc[e]);
+    }
   }
-  stf(o + (int64_t)bh * D + threadIdx.x, acc / L);
+  L = wave_sum(L);
+  const float inv = 1.0f / L;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) stf(o + (int64_t)item * D + lane * PER + e, acc[e] * inv);
 }
 
 size_t decode_attn_partial_floats(int32_t B, int32_t Hq, int32_t D, int32_t cap) {
@@ -981,9 +1001,9 @@ hipError_t launch_decode_attention(hipStream_t s, rp_dtype dt, const void* q, in
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (D == 128)
-      k_decode_attn_merge<float, 128><<<B * Hq, 128, 0, s>>>(partials, nchunks, Hq, (float*)o);
+      k_decode_attn_merge<float, 128><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nchunks, B * Hq, (float*)o);
     else
-      k_decode_attn_merge<float, 64><<<B * Hq, 64, 0, s>>>(partials, nchunks, Hq, (float*)o);
+      k_decode_attn_merge<float, 64><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nchunks, B * Hq, (float*)o);
     return hipGetLastError();
   }
   // the 16-bit kernel addresses a sequence's cache rows with 32-bit byte offsets
@@ -994,11 +1014,11 @@ hipError_t launch_decode_attention(hipStream_t s, rp_dtype dt, const void* q, in
     if (D == 128) {
       k_decode_attn_mfma<H, 128><<<grid, 64, 0, s>>>((const H*)q, q_ld, (const H*)cache_k, (const H*)cache_v, kv_len,
                                                     cap, max_pos, B, Hq, Hkv, scale, nchunks, partials);
-      k_decode_attn_merge<H, 128><<<B * Hq, 128, 0, s>>>(partials, nchunks, Hq, (H*)o);
+      k_decode_attn_merge<H, 128><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nchunks, B * Hq, (H*)o);
     } else {
       k_decode_attn_mfma<H, 64><<<grid, 64, 0, s>>>((const H*)q, q_ld, (const H*)cache_k, (const H*)cache_v, kv_len,
                                                    cap, max_pos, B, Hq, Hkv, scale, nchunks, partials);
-      k_decode_attn_merge<H, 64><<<B * Hq, 64, 0, s>>>(partials, nchunks, Hq, (H*)o);
+      k_decode_attn_merge<H, 64><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nchunks, B * Hq, (H*)o);
     }
   });
   return hipGetLastError();
