@@ -296,7 +296,9 @@ rp_status rp_prompt_logprob(const rp_model *model, void *stream, int32_t B,
  * layer_stride >= B*cap*n_kv_heads*head_dim), it attends to slots
  * 0..kv_len[b], and next_ids[b] = argmax of its logits (lowest id on ties).
  * kv_len is a device int32 [B] array, values clamped to [0, cap-1] (and to
- * max_position-1).  logits (optional) receives fp32 [B, V].
+ * max_position-1).  logits (optional) receives fp32 [B, V]; when it is NULL, a
+ * 16-bit model with B <= 64 takes the argmax inside the lm_head product and the
+ * logits are never formed (same next_ids as the stored-logits path).
  * bf16 models at head_dim 64 return RP_ERR_UNSUPPORTED (disabled: a GPU memory
  * fault in a run that included that combination has no known cause).
  * ------------------------------------------------------------------------- */
@@ -314,8 +316,8 @@ rp_status rp_decode_step(const rp_model *model, void *stream, int32_t B, rp_kv c
  * process ends).  The call allocates nothing; its first call on a device looks up
  * that device's copy of the array.
  * The scratch needed is rp_decode_workspace_bytes() less the [B, V] fp32 logits
- * when logits is non-NULL (about 63 MiB for the 7B slice at B = 64 with logits
- * given); larger needs return RP_ERR_WORKSPACE before any HIP call.  No part of
+ * when logits is non-NULL or the argmax is fused (about 44 MiB for the 7B slice
+ * at B = 64, cap 8256); larger needs return RP_ERR_WORKSPACE before any HIP call.  No part of
  * the scratch needs to start at zero: every byte a step reads was written earlier
  * in the same step.  Every call on a GPU shares that GPU's array, so calls that
  * overlap on one GPU (concurrent streams, or a captured graph replayed while

@@ -421,10 +421,18 @@ struct DecodeWS {
   float* logits;
   float* attn_part;
   float* gemm_part;
+  rp::ArgmaxPart* arg_part;  // per-wave row candidates of the fused lm_head + argmax
 };
 
+// When the caller wants no logits, the lm_head of a 16-bit model with at most 64 rows
+// reduces each row to its argmax in the GEMM (the [B, V] logits are never stored).
+bool decode_fused_argmax(const rp_model* m, int32_t B) {
+  const rp_config& c = m->cfg;
+  return rp::gemm_argmax_supported(c.dtype, B, c.vocab, c.d_model, c.d_model, c.d_model);
+}
+
 // own_logits: carve the [B, V] logits too (they go to the workspace when the caller
-// passes none).
+// passes none and the argmax is not fused).
 size_t decode_ws(const rp_model* m, int32_t B, int32_t cap, void* base, DecodeWS* w, bool own_logits = true) {
   Carver c(base);
   DecodeWS tmp;
@@ -432,6 +440,9 @@ size_t decode_ws(const rp_model* m, int32_t B, int32_t cap, void* base, DecodeWS
   const rp_config& cfg = m->cfg;
   carve_layer(c, cfg, B, true, true, &s->L);
   s->logits = own_logits ? (float*)c.take((int64_t)B * cfg.vocab * 4) : nullptr;
+  s->arg_part = decode_fused_argmax(m, B)
+                    ? (rp::ArgmaxPart*)c.take(rp::gemm_argmax_parts(B, cfg.vocab) * sizeof(rp::ArgmaxPart))
+                    : nullptr;
   s->attn_part = (float*)c.take(rp::decode_attn_partial_floats(B, cfg.n_q_heads, cfg.head_dim, cap) * 4);
   const int64_t d = cfg.d_model, F = cfg.ffn_dim, qkv = (int64_t)(cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim;
   const int64_t hq = (int64_t)cfg.n_q_heads * cfg.head_dim;
@@ -1116,6 +1127,11 @@ rp_status decode_run(const rp_model* m, void* stream, int32_t B, rp_kv cache, in
                                                                         w.L.X, next_norm, c.rms_eps, w.L.N));
   }
   rp::BSeg blm = {m->lm_head, m->lm_head, m->lm_head, c.vocab, c.vocab};
+  if (!logits && w.arg_part) {
+    RP_TRY_LAUNCH_N("decode.gemm_lm_head_argmax", rp::launch_gemm_argmax(s, dt, B, c.vocab, d, w.L.N, d, blm, d,
+                                                                         w.arg_part, next_ids));
+    return dbg.end(RP_OK);
+  }
   RP_TRY_LAUNCH_N("decode.gemm_lm_head", rp::launch_gemm(s, dt, B, c.vocab, d, w.L.N, d, blm, d, lg, c.vocab, rp::EPI_STORE_F32,
                                 decode_splitk(c, B, c.vocab, d), w.gemm_part));
   RP_TRY_LAUNCH_N("decode.argmax", rp::launch_argmax(s, lg, B, c.vocab, next_ids));
@@ -1166,7 +1182,7 @@ rp_status rp_decode_step_static(const rp_model* m, void* stream, int32_t B, rp_k
                                 const int32_t* kv_len, const int32_t* token_ids, float* logits, int32_t* next_ids) {
   rp_status st = check_decode(m, B, cache, cap, kv_len, token_ids, next_ids);
   if (st != RP_OK) return st;
-  const bool own_logits = logits == nullptr;
+  const bool own_logits = logits == nullptr && !decode_fused_argmax(m, B);
   const size_t need = decode_ws(m, B, cap, nullptr, nullptr, own_logits);
   if (need > (size_t)RP_DECODE_STATIC_SCRATCH_BYTES)
     return fail(RP_ERR_WORKSPACE,

@@ -973,6 +973,7 @@ struct SkinnyArgs {
   int64_t plane;  // elements between splits of out
   int k_chunk;
   int add;        // accumulate into out (one split)
+  ArgmaxPart* arg;  // instead of out (one split): each wave's per-row (max, lowest column of it)
 };
 
 template <typename T16, int RF, bool BT, int SW>
@@ -1094,6 +1095,31 @@ __global__ __launch_bounds__(SW * 64) void k_gemm_skinny(SkinnyArgs g) {
   __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the wave
 
   // acc[rf][e] = C(row rf*32 + fr, column nw0 + 8 (e/4) + 4 fk + e%4)
+  if (g.arg) {  // argmax of each row over this wave's 32 columns; NaN never wins, ties go low
+#pragma unroll
+    for (int rf = 0; rf < RF; ++rf) {
+      float best = -INFINITY;
+      int bi = 0x7fffffff;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int n = nw0 + 8 * (e >> 2) + 4 * fk + (e & 3);
+        const float v = acc[rf][e];
+        if (n < g.N && (v > best || (v == best && n < bi))) {
+          best = v;
+          bi = n;
+        }
+      }
+      const float vo = __shfl_xor(best, 32, 64);
+      const int io = __shfl_xor(bi, 32, 64);
+      if (vo > best || (vo == best && io < bi)) {
+        best = vo;
+        bi = io;
+      }
+      const int m = rf * 32 + fr;
+      if (fk == 0 && m < g.M && nw0 < g.N) g.arg[(int64_t)(blockIdx.x * SW + wave) * g.M + m] = ArgmaxPart{best, bi};
+    }
+    return;
+  }
   float* outp = g.out + (int64_t)blockIdx.y * g.plane;
   const bool vec = (g.ldo & 3) == 0 && ((uintptr_t)g.out & 15) == 0 && (g.plane & 3) == 0;
 #pragma unroll
@@ -1161,7 +1187,7 @@ static void launch_skinny_w(hipStream_t s, const SkinnyArgs& a, dim3 grid) {
 
 template <typename T16>
 static void launch_skinny(hipStream_t s, const GemmArgs& g, int splitk, float* out, int ldo, int64_t plane,
-                          bool add) {
+                          bool add, ArgmaxPart* arg = nullptr) {
   SkinnyArgs a;
   a.M = g.M;
   a.N = g.N;
@@ -1175,6 +1201,7 @@ static void launch_skinny(hipStream_t s, const GemmArgs& g, int splitk, float* o
   a.plane = plane;
   a.k_chunk = g.k_chunk;
   a.add = add ? 1 : 0;
+  a.arg = arg;
   constexpr int SW = kSkinnyWaves;
   const dim3 grid((g.N + 32 * SW - 1) / (32 * SW), splitk);
   if (g.B.trans)
@@ -1293,6 +1320,88 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
     k_splitk_reduce<EPI_STORE_F32, float><<<blocks, 256, 0, s>>>(partials, splitk, M, N, C, ldc);
   else
     k_splitk_reduce<EPI_ADD_F32, float><<<blocks, 256, 0, s>>>(partials, splitk, M, N, C, ldc);
+  return hipGetLastError();
+}
+
+// C = A . B^T reduced to each row's argmax (the lowest column of the row's maximum; NaN
+// never wins; -1 for a row with no candidate), without storing C: the skinny kernel
+// writes each wave's per-row candidate and k_argmax_parts picks among them in column order.
+bool gemm_argmax_supported(rp_dtype dt, int32_t M, int32_t N, int32_t K, int32_t lda, int32_t ldb) {
+  if (dt == RP_F32 || M < 1 || N < 1 || M > 64 || K % 64) return false;
+  if (gemm_skinny_splitk(M, N, K) != 1 || gemm_effective_splitk(dt, K, gemm_skinny_splitk(M, N, K)) != 1) return false;
+  GemmArgs g;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = nullptr;
+  g.lda = lda;
+  g.B = BSeg{nullptr, nullptr, nullptr, N, N};
+  g.ldb = ldb;
+  return skinny_setup(g, EPI_STORE_F32, false);
+}
+
+size_t gemm_argmax_parts(int32_t M, int32_t N) { return (size_t)M * ((N + 31) / 32); }
+
+__global__ __launch_bounds__(256) void k_argmax_parts(const ArgmaxPart* __restrict__ part, int nparts, int M,
+                                                      int32_t* __restrict__ out) {
+  const int m = blockIdx.x;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int t = threadIdx.x; t < nparts; t += blockDim.x) {  // ascending column ranges
+    const ArgmaxPart p = part[(int64_t)t * M + m];
+    if (p.v > best || (p.v == best && p.i < bi)) {
+      best = p.v;
+      bi = p.i;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float vb = __shfl_xor(best, o, kWave);
+    const int ib = __shfl_xor(bi, o, kWave);
+    if (vb > best || (vb == best && ib < bi)) {
+      best = vb;
+      bi = ib;
+    }
+  }
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) {
+    sv[w] = best;
+    si[w] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < 4; ++k)
+      if (sv[k] > best || (sv[k] == best && si[k] < bi)) {
+        best = sv[k];
+        bi = si[k];
+      }
+    out[m] = bi == 0x7fffffff ? -1 : bi;
+  }
+}
+
+hipError_t launch_gemm_argmax(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
+                              int32_t lda, const BSeg& B, int32_t ldb, ArgmaxPart* parts, int32_t* out) {
+  if (!gemm_argmax_supported(dt, M, N, K, lda, ldb) || B.trans || ((uintptr_t)A & 15) || ((uintptr_t)B.b0 & 15) ||
+      !parts || !out)
+    return hipErrorInvalidValue;
+  GemmArgs g;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = A;
+  g.lda = lda;
+  g.B = B;
+  g.ldb = ldb;
+  g.k_chunk = K;
+  with_half16(dt, [&](auto tag_) {
+    using H = decltype(tag_);
+    launch_skinny<H>(s, g, 1, nullptr, 0, 0, false, parts);
+  });
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_argmax_parts<<<M, 256, 0, s>>>(parts, (N + 31) / 32, M, out);
   return hipGetLastError();
 }
 

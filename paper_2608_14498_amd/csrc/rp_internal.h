@@ -154,6 +154,18 @@ hipError_t launch_gemm(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t
                        int32_t lda, const BSeg& B, int32_t ldb, void* C, int32_t ldc, Epi epi,
                        int32_t splitk, float* partials, const LseOut* lse = nullptr,
                        const RopeOut* rope = nullptr);
+// out[m] = argmax over n of (A . B^T)[m][n] (lowest n among equal maxima; NaN never wins; -1
+// when a row has no candidate), C itself never stored.  16-bit, one B segment [N][K], M <= 64,
+// one K split (gemm_argmax_supported).  parts: gemm_argmax_parts(M, N) ArgmaxPart entries.
+struct ArgmaxPart {
+  float v;
+  int32_t i;
+};
+bool gemm_argmax_supported(rp_dtype dt, int32_t M, int32_t N, int32_t K, int32_t lda, int32_t ldb);
+size_t gemm_argmax_parts(int32_t M, int32_t N);
+hipError_t launch_gemm_argmax(hipStream_t s, rp_dtype dt, int32_t M, int32_t N, int32_t K, const void* A,
+                              int32_t lda, const BSeg& B, int32_t ldb, ArgmaxPart* parts, int32_t* out);
+
 // Rotation table of EPI_ROPE for M rows (float2 [M][D/2]); positions as launch_rope_kv.
 hipError_t launch_rope_table(hipStream_t s, const SeqTable& st, const RopeFreq& rf, int32_t max_pos, const MRope& mr,
                              int32_t M, int32_t D, float2* cs);

@@ -190,6 +190,11 @@ def test_decode_step_matches_oracle(model, cap, lens):
     print(f"[parity] decode {model.dtype}: logits max|d|={err}", flush=True)
     assert err <= tol
     got_ids = nxt.cpu().numpy()
+    # no logits buffer: 16-bit models take the argmax inside the lm_head product; the same
+    # step again (it rewrites the same cache slot with the same values) picks the same ids
+    nxt2 = dm.decode(ck, cv, to_device(dec.kv_len, dm.device), to_device(dec.token_ids, dm.device))
+    torch.cuda.synchronize()
+    assert np.array_equal(nxt2.cpu().numpy(), got_ids)
     for b in range(B):
         top2 = np.sort(lo[b])[-2:]
         if top2[1] - top2[0] > 2 * tol:

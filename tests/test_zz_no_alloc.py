@@ -2,7 +2,9 @@
 rp_decode_step with a caller workspace, through the C ABI: logits, next ids and the
 cache writes must be bitwise equal (same kernels, same order), over two calls in a
 row, the second with a smaller batch and cache (the shared scratch keeps the first
-call's contents)."""
+call's contents).  A static call given no logits buffer takes the argmax inside the
+lm_head product (16-bit models, at most 64 rows); its next ids must still equal those
+of the workspace call, which stores the logits."""
 import numpy as np
 import pytest
 import torch
@@ -66,5 +68,7 @@ def test_static_decode_equals_workspace_decode_7b_slice():
         _one_call(dm, w, B=64, cap=8256, kv0=8192, own_logits=False)
         print("[no-alloc] 7B slice B=16 cap=4096", flush=True)
         _one_call(dm, w, B=16, cap=4096, kv0=1000, own_logits=False)
+        print("[no-alloc] 7B slice B=64 cap=8256, no logits buffer (fused argmax)", flush=True)
+        _one_call(dm, w, B=64, cap=8256, kv0=8192, own_logits=True)
     finally:
         dm.close()
