@@ -156,18 +156,24 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   const int nq = __builtin_amdgcn_readfirstlane(st.q_cu[b + 1]) - qrow0;
   const int qpos_first = n0 + (qb.q_begin - qrow0);
   const int qpos_last = n0 + (qb.q_end - 1 - qrow0);
-  const int nk = qpos_last + 1;  // keys needed by this block
-  // Key tiles t_begin .. t_end-1 of this block.  Split-KV: a sequence with n0 first-
-  // segment keys has nsp = attn_splits(n0) splits; split sp takes its share of the P
-  // tiles that lie wholly in the first segment, and the last split also the rest (the
-  // boundary tile and the causal keys), so it is the longest and runs at blockIdx.y 0.
-  // Every split holds at least one tile (P / nsp >= RP_ATTN_SPLIT_KEYS / KT).
-  int t_begin = 0, t_end = (nk + KT - 1) / KT, sp = 0;
+  // Key tiles: the first P0 tiles hold the n0 first-segment keys (the last of them may be
+  // partial: its rows past n0 read as zeros and are masked), the rest the segment-1 keys
+  // n0 .. qpos_last this block needs, from position n0 on.  No tile mixes the segments,
+  // so each tile's copies name one buffer resource.  Tile t's first key position is
+  // kpos0(t).
+  const int P0 = (n0 + KT - 1) / KT;
+  auto kpos0 = [&](int t) { return t < P0 ? t * KT : n0 + (t - P0) * KT; };
+  // Tiles t_begin .. t_end-1 of this block.  Split-KV: a sequence with n0 first-segment
+  // keys has nsp = attn_splits(n0) splits; split sp takes its share of the P0 first-
+  // segment tiles, and the last split also the segment-1 tiles (the causal keys), so it
+  // is the longest and runs at blockIdx.y 0.  Every split holds at least one tile
+  // (P0 / nsp >= RP_ATTN_SPLIT_KEYS / KT).
+  int t_begin = 0, t_end = P0 + (qpos_last - n0 + KT) / KT, sp = 0;
   const int nsp = a.part ? attn_splits(n0) : 1;
   if ((int)blockIdx.y >= nsp) return;
   if (nsp > 1) {
     sp = nsp - 1 - (int)blockIdx.y;
-    const int P = n0 / KT, per = (P + nsp - 1) / nsp;
+    const int per = (P0 + nsp - 1) / nsp;
     t_begin = sp * per;
     if (sp < nsp - 1) t_end = t_begin + per;
   }
@@ -208,27 +214,17 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
     FA_DMA(RK_, koff[j] + (so_), KD_, j);               \
     FA_DMA(RV_, voff[j] + (so_), VD_, j);               \
   }
-  // Every branch names its buffer resources (a selected resource would be formed in
-  // vector registers); all offsets go in the range-checked vector offset (the scalar
-  // offset is not range-checked).
+  // Each (uniform) branch names its buffer resources (a selected resource would be formed
+  // in vector registers); all offsets go in the range-checked vector offset (the scalar
+  // offset is not range-checked).  Both branches issue the same copies, so the compiler
+  // counts the outstanding ones exactly.
 #define FA_LOAD(KD_, VD_, t_)                                                         \
   {                                                                                   \
-    const int klo = (t_) * KT;                                                        \
-    if (klo >= n0) {                                                                  \
-      FA_LOAD_SEG(rsK1, rsV1, KD_, VD_, (uint32_t)(klo - n0) * row_bytes);            \
-    } else if (klo + KT <= n0) {                                                      \
-      FA_LOAD_SEG(rsK0, rsV0, KD_, VD_, (uint32_t)klo * row_bytes);                   \
-    } else { /* the tile straddling the segment boundary: segment per lane */         \
-      _Pragma("unroll") for (int j = 0; j < LOADS; ++j) {                             \
-        const int kv = klo + (wave * LOADS + j) * (64 / CH) + lane / CH;              \
-        if (kv < n0) {                                                                \
-          FA_DMA(rsK0, koff[j] + (uint32_t)klo * row_bytes, KD_, j);                  \
-          FA_DMA(rsV0, voff[j] + (uint32_t)klo * row_bytes, VD_, j);                  \
-        } else {                                                                      \
-          FA_DMA(rsK1, koff[j] + (uint32_t)(klo - n0) * row_bytes, KD_, j);           \
-          FA_DMA(rsV1, voff[j] + (uint32_t)(klo - n0) * row_bytes, VD_, j);           \
-        }                                                                             \
-      }                                                                               \
+    const int tt_ = __builtin_amdgcn_readfirstlane(t_);  /* uniform: scalar branch */ \
+    if (tt_ < P0) {                                                                   \
+      FA_LOAD_SEG(rsK0, rsV0, KD_, VD_, (uint32_t)(tt_ * KT) * row_bytes);            \
+    } else {                                                                          \
+      FA_LOAD_SEG(rsK1, rsV1, KD_, VD_, (uint32_t)((tt_ - P0) * KT) * row_bytes);     \
     }                                                                                 \
   }
 
@@ -263,12 +259,8 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   const int tr_key = fk * 4 + (tr_p >> 2);                     // + kb*32 + hh*16 (+8 for the second read)
   const int tr_col = ((lane & 16) ? 16 : 0) + 4 * (tr_p & 3);  // + db*32
 
-  // One key tile: loads of tile t+1 into (Kn, Vn) are issued first and land while tile t
-  // is computed from (Kc, Vc); the closing barrier (which waits for this wave's loads)
-  // makes them visible to every wave.
-  auto tile = [&](const u32x4_t* Kc, const u32x4_t* Vc, u32x4_t* Kn, u32x4_t* Vn, int t) __attribute__((always_inline)) {
-    if (t + 1 < t_end) FA_LOAD(Kn, Vn, t + 1);
-
+  // One key tile computed from (Kc, Vc).
+  auto compute = [&](const u32x4_t* Kc, const u32x4_t* Vc, int t) __attribute__((always_inline)) {
     // ---- S^T = K Q^T: s[qi][kb][e] = score(key t*KT + kb*32 + 8(e/4) + 4 fk + e%4, query fr) ----
     f32x16_t s[QW][KB];
 #pragma unroll
@@ -288,11 +280,14 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
     // running max m is raised only when some lane's tile max exceeds it by more than
     // kLazy (wave-uniform test), so p <= 2^kLazy and the O^T rescale is skipped on most
     // tiles; numerator and denominator share the same m, so the result is unchanged.
-    const bool need_mask = (t * KT + KT - 1) > qpos_first;
+    // masked: first-segment keys past n0 (the last first-segment tile only) and causal
+    // keys past the query (segment-1 tiles that reach past the block's first query)
+    const bool seg0 = t < P0;
+    const bool need_mask = seg0 ? (t * KT + KT > n0) : (kpos0(t) + KT - 1 > qpos_first);
 #pragma unroll
     for (int qi = 0; qi < QW; ++qi) {
       if (need_mask) {
-        const int lim = qpos[qi] - t * KT - 4 * fk;  // key offset in the tile - 4 fk
+        const int lim = (seg0 ? n0 - 1 : qpos[qi]) - kpos0(t) - 4 * fk;  // last visible offset - 4 fk
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -356,9 +351,17 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
         }
       }
     }
-    __syncthreads();
   };
 
+  // Loads of tile t+1 into (Kn, Vn) are issued first and land while tile t is computed
+  // from (Kc, Vc); the closing barrier (which waits for this wave's loads) makes them
+  // visible to every wave.  (A third buffer with two tiles in flight and explicit
+  // per-tile waits measured slower: 5.47 against 4.96 ms per layer at 2 x 16384 keys.)
+  auto tile = [&](const u32x4_t* Kc, const u32x4_t* Vc, u32x4_t* Kn, u32x4_t* Vn, int t) __attribute__((always_inline)) {
+    if (t + 1 < t_end) FA_LOAD(Kn, Vn, t + 1);
+    compute(Kc, Vc, t);
+    __syncthreads();
+  };
   FA_LOAD(Ks0, Vs0, t_begin);
   __syncthreads();
   int t = t_begin;
