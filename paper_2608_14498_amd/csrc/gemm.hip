@@ -1347,13 +1347,22 @@ __global__ __launch_bounds__(256) void k_argmax_parts(const ArgmaxPart* __restri
   const int m = blockIdx.x;
   float best = -INFINITY;
   int bi = 0x7fffffff;
-  for (int t = threadIdx.x; t < nparts; t += blockDim.x) {  // ascending column ranges
-    const ArgmaxPart p = part[(int64_t)t * M + m];
+  auto merge = [&](const ArgmaxPart& p) {
     if (p.v > best || (p.v == best && p.i < bi)) {
       best = p.v;
       bi = p.i;
     }
+  };
+  // the candidates of row m are M entries apart: eight loads in flight per thread
+  int t = threadIdx.x;
+  for (; t + 7 * 256 < nparts; t += 8 * 256) {
+    ArgmaxPart p[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) p[u] = part[(int64_t)(t + u * 256) * M + m];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) merge(p[u]);
   }
+  for (; t < nparts; t += 256) merge(part[(int64_t)t * M + m]);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float vb = __shfl_xor(best, o, kWave);
