@@ -380,7 +380,8 @@ def test_transposed_row_parallel_weights(model):
     w = configs.custom(model, P, Vis, S, index=85)
     hw = inputs.make_weights(w, norm="random", bias=True)
     bt = inputs.make_batch(w)
-    cap, lens = 400, [0, 131, 399]
+    # 40 decode rows: the skinny GEMM's two-row-block form (33..64 rows) in both layouts
+    cap, lens = 400, [0, 131, 399] + [(37 * i + 5) % 400 for i in range(37)]
     dec = inputs.make_decode(w, batch=len(lens), kv_len=np.array(lens, np.int32), cap=cap)
     cp, cs = [int(x) for x in bt.cu_prefix], [int(x) for x in bt.cu_suffix]
     outs = []
