@@ -1265,8 +1265,12 @@ rp_status rp_stream_create_cu_masked(int device, const uint32_t* mask, uint32_t 
   if ((e = hipSetDevice(device)) != hipSuccess) return fail(RP_ERR_HIP, "hipSetDevice(%d): %s", device, hipGetErrorString(e));
   hipStream_t s = nullptr;
   e = hipExtStreamCreateWithCUMask(&s, n_words, mask);
-  hipSetDevice(prev);
+  const hipError_t er = hipSetDevice(prev);
   if (e != hipSuccess) return fail(RP_ERR_HIP, "hipExtStreamCreateWithCUMask: %s", hipGetErrorString(e));
+  if (er != hipSuccess) {
+    (void)hipStreamDestroy(s);
+    return fail(RP_ERR_HIP, "hipSetDevice(%d) after creating the stream: %s", prev, hipGetErrorString(er));
+  }
   *out = (void*)s;
   return RP_OK;
 }

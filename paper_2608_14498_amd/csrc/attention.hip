@@ -381,13 +381,14 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
       const int qrow = qb.q_begin + (wave * QW + qi) * 32 + fr;
       const float l = l_run[qi] + __shfl_xor(l_run[qi], 32, kWave);
       if (qrow >= qb.q_end) continue;
-      float* pp = a.part + (((int64_t)qrow * a.Hq + h) * gridDim.y + sp) * (D + 4);
-      if (fk == 0) *reinterpret_cast<float2*>(pp) = make_float2(m_run[qi], l);
+      float* pp = a.part + ((int64_t)qrow * a.Hq + h) * attn_part_record(gridDim.y, D);
+      if (fk == 0) *reinterpret_cast<float2*>(pp + gridDim.y * D + 2 * sp) = make_float2(m_run[qi], l);
+      pp += sp * D;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int e4 = 0; e4 < 4; ++e4)
-          *reinterpret_cast<float4*>(pp + 4 + db * 32 + 8 * e4 + 4 * fk) =
+          *reinterpret_cast<float4*>(pp + db * 32 + 8 * e4 + 4 * fk) =
               make_float4(o[qi][db][4 * e4], o[qi][db][4 * e4 + 1], o[qi][db][4 * e4 + 2], o[qi][db][4 * e4 + 3]);
     }
     return;
@@ -488,18 +489,18 @@ __global__ __launch_bounds__(256) void k_attn_split_merge(SeqTable st, const flo
   const int lane = threadIdx.x & 63;
   const int nsp = attn_splits(st.pos0(seq_of_row(st, (int)(item / Hq))));
   if (nsp == 1) return;
-  const float* p = part + item * S * (D + 4);
+  const float* p = part + item * attn_part_record(S, D);
+  const float* ml = p + S * D;
   float M = -INFINITY;
-  for (int sp = 0; sp < nsp; ++sp) M = fmaxf(M, p[(int64_t)sp * (D + 4)]);
+  for (int sp = 0; sp < nsp; ++sp) M = fmaxf(M, ml[2 * sp]);
   float L = 0.f, acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
   for (int sp = 0; sp < nsp; ++sp) {
-    const float* ps = p + (int64_t)sp * (D + 4);
-    const float w = __builtin_amdgcn_exp2f(ps[0] - M);
-    L = fmaf(ps[1], w, L);
+    const float w = __builtin_amdgcn_exp2f(ml[2 * sp] - M);
+    L = fmaf(ml[2 * sp + 1], w, L);
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] = fmaf(ps[4 + lane * PER + e], w, acc[e]);
+    for (int e = 0; e < PER; ++e) acc[e] = fmaf(p[sp * D + lane * PER + e], w, acc[e]);
   }
   const float inv = 1.0f / L;
   T16* op = o + item * D + lane * PER;
@@ -510,7 +511,7 @@ __global__ __launch_bounds__(256) void k_attn_split_merge(SeqTable st, const flo
 }
 
 size_t attn_partial_floats(int64_t R, int32_t Hq, int32_t D, int32_t max_splits) {
-  return max_splits > 1 ? (size_t)R * Hq * max_splits * (D + 4) : 0;
+  return max_splits > 1 ? (size_t)R * Hq * attn_part_record(max_splits, D) : 0;
 }
 
 int count_qblocks(const SeqTable& st, int BQ) {
@@ -598,6 +599,9 @@ hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, cons
 // online softmax per head (log2 domain, running max raised only when a score exceeds it
 // by more than 2^8, so the rescale branch is rarely taken); the groups are merged with
 // lane shuffles and the wave writes (max, sum, o[D]) per head for the merge kernel.
+// Partial layout (both kernels and the merge): o of (item = b * Hq + q head, chunk c) at
+// part[(item * nchunks + c) * D], whole 128-byte lines written by one wave, then the
+// (max, sum) pairs at part[B * Hq * nchunks * D + (item * nchunks + c) * 2].
 // ------------------------------------------------------------------------------------
 constexpr int DC_KEYS = 512;  // keys per chunk (one wave)
 constexpr int DC_MAXG = 8;    // q heads per kv head (validated on the host)
@@ -622,12 +626,14 @@ __global__ __launch_bounds__(256) void k_decode_attn_part(const T* __restrict__ 
   const int n = min(max(kv_len[b], 0), min(cap, max_pos) - 1);  // new token slot; keys 0..n
   const int k_begin = c * DC_KEYS;
   const int nkeys = min(DC_KEYS, n + 1 - k_begin);
-  float* out = part + ((int64_t)(b * Hq + g * G) * nchunks + c) * (D + 2);
-  const int64_t head_stride = (int64_t)nchunks * (D + 2);
+  const int64_t rec = (int64_t)(b * Hq + g * G) * nchunks + c;
+  float* out = part + rec * D;                                  // o records
+  float* oml = part + (int64_t)B * Hq * nchunks * D + rec * 2;  // (max, sum)
+  const int64_t head_stride = (int64_t)nchunks * D, ml_stride = (int64_t)nchunks * 2;
   if (nkeys <= 0) {
     if (lane < G) {
-      out[lane * head_stride] = -INFINITY;
-      out[lane * head_stride + 1] = 0.f;
+      oml[lane * ml_stride] = -INFINITY;
+      oml[lane * ml_stride + 1] = 0.f;
     }
     return;
   }
@@ -739,12 +745,12 @@ __global__ __launch_bounds__(256) void k_decode_attn_part(const T* __restrict__ 
       }
       float* oh = out + h * head_stride;
       if (lane == 0) {
-        oh[0] = M * 0.6931471805599453f;
-        oh[1] = L;
+        oml[h * ml_stride] = M * 0.6931471805599453f;
+        oml[h * ml_stride + 1] = L;
       }
       if (kk == 0) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) oh[2 + sub * 8 + e] = ov[e];
+        for (int e = 0; e < 8; ++e) oh[sub * 8 + e] = ov[e];
       }
     }
   }
@@ -782,15 +788,27 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   const int g = blockIdx.x % Hkv, bc = blockIdx.x / Hkv;
   const int c = bc % nchunks, b = bc / nchunks;
   const int G = Hq / Hkv;
+  // query columns: lane column fr is q head g*G + fr (zero beyond G); issued first, so they
+  // are in flight while kv_len is read and are covered by the wait for the first tile
+  const int fr = lane & 31, fk = lane >> 5;
+  V8 qf[KSTEPS];
+#pragma unroll
+  for (int ks = 0; ks < KSTEPS; ++ks) {
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (fr < G) v = *reinterpret_cast<const uint4*>(q + (int64_t)b * q_ld + (g * G + fr) * D + ks * 16 + fk * 8);
+    qf[ks] = H::as_v8(v);
+  }
   const int n = min(max(kv_len[b], 0), min(cap, max_pos) - 1);  // keys 0..n
   const int k_begin = c * DC_KEYS;
   const int nkeys = min(DC_KEYS, n + 1 - k_begin);
-  float* out = part + ((int64_t)(b * Hq + g * G) * nchunks + c) * (D + 2);
-  const int64_t head_stride = (int64_t)nchunks * (D + 2);
+  const int64_t rec = (int64_t)(b * Hq + g * G) * nchunks + c;
+  float* out = part + rec * D;                                  // o records
+  float* oml = part + (int64_t)B * Hq * nchunks * D + rec * 2;  // (max, sum)
+  const int64_t head_stride = (int64_t)nchunks * D, ml_stride = (int64_t)nchunks * 2;
   if (nkeys <= 0) {
     if (lane < G) {
-      out[lane * head_stride] = -INFINITY;
-      out[lane * head_stride + 1] = 0.f;
+      oml[lane * ml_stride] = -INFINITY;
+      oml[lane * ml_stride + 1] = 0.f;
     }
     return;
   }
@@ -815,15 +833,6 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   _Pragma("unroll") for (int j = 0; j < LOADS; ++j) {                                                       \
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsK, (lds_void_t*)((KD_) + j * 64), 16, koff[j] + (uint32_t)(t_) * KT * row_bytes, 0, 0, 0); \
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsV, (lds_void_t*)((VD_) + j * 64), 16, voff[j] + (uint32_t)(t_) * KT * row_bytes, 0, 0, 0); \
-  }
-  // query columns: lane column fr is q head g*G + fr (zero beyond G)
-  const int fr = lane & 31, fk = lane >> 5;
-  V8 qf[KSTEPS];
-#pragma unroll
-  for (int ks = 0; ks < KSTEPS; ++ks) {
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (fr < G) v = *reinterpret_cast<const uint4*>(q + (int64_t)b * q_ld + (g * G + fr) * D + ks * 16 + fk * 8);
-    qf[ks] = H::as_v8(v);
   }
   f32x16_t o[DB];
 #pragma unroll
@@ -897,46 +906,45 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   // loop issue every load unconditionally (a short chunk re-reads its last tile), so the
   // compiler counts exactly which loads a stage waits for and the later ones stay in
   // flight; only the last few tiles (no loop) take branches.
-  // The query fragments are in registers before the first copy is issued: a loop whose
-  // loads fill only LDS but which reads registers still loading from before it makes the
-  // compiler drain every load (these copies included) ahead of the loop.
-  __builtin_amdgcn_s_waitcnt(0);
+  // Tile 0 runs before the loop: its wait for stage 0 also covers the query loads issued
+  // ahead of the copies, so no register load is pending when the loop starts (a loop
+  // whose loads fill only LDS but which reads registers still loading from before it
+  // makes the compiler drain every load, these copies included, ahead of the loop).
   DM_LOAD(Ks0, Vs0, 0);
   DM_LOAD(Ks1, Vs1, min(1, ntiles - 1));
   DM_LOAD(Ks2, Vs2, min(2, ntiles - 1));
-  int t = 0;
+  tile(Ks0, Vs0, 0);
+  DM_LOAD(Ks0, Vs0, min(3, ntiles - 1));
+  int t = 1;  // tiles t, t+1, t+2 in (or on their way to) stages 1, 2, 0
   for (; t + 6 <= ntiles; t += 3) {
-    tile(Ks0, Vs0, t);
-    DM_LOAD(Ks0, Vs0, t + 3);
-    tile(Ks1, Vs1, t + 1);
-    DM_LOAD(Ks1, Vs1, t + 4);
-    tile(Ks2, Vs2, t + 2);
-    DM_LOAD(Ks2, Vs2, t + 5);
+    tile(Ks1, Vs1, t);
+    DM_LOAD(Ks1, Vs1, t + 3);
+    tile(Ks2, Vs2, t + 1);
+    DM_LOAD(Ks2, Vs2, t + 4);
+    tile(Ks0, Vs0, t + 2);
+    DM_LOAD(Ks0, Vs0, t + 5);
   }
-  const int r = ntiles - t;  // 1 .. 5 tiles left, t .. t+2 in (or on their way to) the stages
-  tile(Ks0, Vs0, t);
-  if (r > 3) { DM_LOAD(Ks0, Vs0, t + 3); }
-  if (r > 1) tile(Ks1, Vs1, t + 1);
-  if (r > 4) { DM_LOAD(Ks1, Vs1, t + 4); }
-  if (r > 2) tile(Ks2, Vs2, t + 2);
-  if (r > 3) tile(Ks0, Vs0, t + 3);
-  if (r > 4) tile(Ks1, Vs1, t + 4);
+  const int r = ntiles - t;  // 0 .. 5 tiles left
+  if (r > 0) tile(Ks1, Vs1, t);
+  if (r > 3) { DM_LOAD(Ks1, Vs1, t + 3); }
+  if (r > 1) tile(Ks2, Vs2, t + 1);
+  if (r > 4) { DM_LOAD(Ks2, Vs2, t + 4); }
+  if (r > 2) tile(Ks0, Vs0, t + 2);
+  if (r > 3) tile(Ks1, Vs1, t + 3);
+  if (r > 4) tile(Ks2, Vs2, t + 4);
 #undef DM_LOAD
   __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the wave
   // o[db][e] = O^T(dim db*32 + 8(e/4) + 4 fk + e%4, head fr), unnormalised
   const float l = l_run + __shfl_xor(l_run, 32, kWave);
   if (fr < G) {
     float* oh = out + fr * head_stride;
-    if (fk == 0) {
-      oh[0] = m_run * 0.6931471805599453f;
-      oh[1] = l;
-    }
+    if (fk == 0) *reinterpret_cast<float2*>(oml + fr * ml_stride) = make_float2(m_run * 0.6931471805599453f, l);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int e4 = 0; e4 < 4; ++e4) {
         const int dh = db * 32 + 8 * e4 + 4 * fk;
-        *reinterpret_cast<float4*>(oh + 2 + dh) =
+        *reinterpret_cast<float4*>(oh + dh) =
             make_float4(o[db][4 * e4], o[db][4 * e4 + 1], o[db][4 * e4 + 2], o[db][4 * e4 + 3]);
       }
   }
@@ -953,24 +961,25 @@ __global__ __launch_bounds__(256) void k_decode_attn_merge(const float* __restri
   constexpr int PER = D / 64;
   const int item = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (item >= items) return;
-  const float* p = part + (int64_t)item * nchunks * (D + 2);
+  const float* p = part + (int64_t)item * nchunks * D;                                    // o records
+  const float* pml = part + (int64_t)items * nchunks * D + (int64_t)item * nchunks * 2;  // (max, sum)
   float M = -INFINITY;
-  for (int c = lane; c < nchunks; c += 64) M = fmaxf(M, p[(int64_t)c * (D + 2)]);
+  for (int c = lane; c < nchunks; c += 64) M = fmaxf(M, pml[2 * c]);
   M = wave_max(M);
   float L = 0.f, acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
   for (int c0 = 0; c0 < nchunks; c0 += 64) {
     const int c = c0 + lane;
-    const float mc = c < nchunks ? p[(int64_t)c * (D + 2)] : -INFINITY;
+    const float mc = c < nchunks ? pml[2 * c] : -INFINITY;
     const bool has = mc > -INFINITY;
     const float w = has ? expf(mc - M) : 0.f;
-    L += has ? w * p[(int64_t)c * (D + 2) + 1] : 0.f;
+    L += has ? w * pml[2 * c + 1] : 0.f;
     const int nv = __popcll(__ballot(has));  // chunks with keys: a prefix of c0 ..
 #pragma unroll 4
     for (int j = 0; j < nv; ++j) {
       const float wj = __shfl(w, j, kWave);
-      const float* oc = p + (int64_t)(c0 + j) * (D + 2) + 2 + lane * PER;
+      const float* oc = p + (int64_t)(c0 + j) * D + lane * PER;
 #pragma unroll
       for (int e = 0; e < PER; ++e) acc[e] = fmaf(wj, oc[e], acc[e]);
     }

@@ -193,9 +193,13 @@ struct AttnArgs {
   float scale;
   // Split-KV (16-bit models): when set, a sequence whose first key segment holds n0 rows
   // splits its keys attn_splits(n0) ways; the splits write (max, sum, unnormalised o)
-  // partials here and a merge kernel writes o.  attn_partial_floats() floats.
+  // partials here and a merge kernel writes o.  attn_partial_floats() floats: one record
+  // of attn_part_record(S, D) floats per (query row, head) for a launch of S split slots,
+  // split sp's o at sp * D and its (max, sum) at S * D + 2 sp, so each split's o is whole
+  // 128-byte lines written by one workgroup.
   float* part = nullptr;
 };
+__host__ __device__ inline int attn_part_record(int S, int D) { return S * D + 32; }
 // Key splits of a sequence with n0 first-segment keys: a function of n0 alone, so a
 // sequence's result does not depend on the sequences packed with it.
 #ifndef RP_ATTN_SPLIT_KEYS
