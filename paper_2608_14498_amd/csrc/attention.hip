@@ -119,9 +119,18 @@ constexpr float kLazy = 8.f;  // log2 headroom of the lazily updated softmax max
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
+// LDS chunk swizzles (16-byte chunks of a K or V row).  K rows are read 16 bytes per lane
+// (row = key), so consecutive keys take distinct chunks.  V rows are read with
+// ds_read_b64_tr_b16: in each 32-lane half, lane bits 0,1,4 pick the column within a
+// 32-column block and bits 2,3 the key within a group of four; XOR-ing the key's low two
+// bits into chunk bits 2,3 (D = 128: a row spans all 64 banks) or 1,2 (D = 64: two rows
+// do, the key's bit 0 picking the half) makes the 32 lanes of a half hit 64 distinct
+// banks.  (Chunk bits 1,2 at D = 128 left one bank bit fixed: half the banks, and the
+// LDS bank-conflict counter at 14% of the prefix kernel's cycles.)
 template <int D>
 __device__ __forceinline__ int kswz(int key) { return D == 128 ? (key & 15) : (key & 7); }
-__device__ __forceinline__ int vswz(int key) { return (key & 3) << 1; }
+template <int D>
+__device__ __forceinline__ int vswz(int key) { return D == 128 ? (key & 3) << 2 : (key & 3) << 1; }
 
 template <typename T16, int D, int QW, int KT, int NW = 4>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(QW == 1 ? 2 : 1, QW == 1 ? 2 : 1)))
@@ -205,7 +214,7 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
   for (int j = 0; j < LOADS; ++j) {
     const int slot = (wave * LOADS + j) * 64 + lane, key = slot / CH, cp = slot % CH;
     koff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ kswz<D>(key)) * 16);
-    voff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ vswz(key)) * 16);
+    voff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ vswz<D>(key)) * 16);
   }
 #define FA_DMA(RS_, OFF_, DST_, j_) \
   __builtin_amdgcn_raw_ptr_buffer_load_lds(RS_, (lds_void_t*)((DST_) + (wave * LOADS + (j_)) * 64), 16, OFF_, 0, 0, 0)
@@ -340,8 +349,8 @@ void k_attn_bf16(SeqTable st, AttnArgs a) {
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           const int col = db * 32 + tr_col;
-          const int ca = ((col >> 3) ^ vswz(ka)) * 8 + (col & 7);
-          const int cc = ((col >> 3) ^ vswz(kc)) * 8 + (col & 7);
+          const int ca = ((col >> 3) ^ vswz<D>(ka)) * 8 + (col & 7);
+          const int cc = ((col >> 3) ^ vswz<D>(kc)) * 8 + (col & 7);
           const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + ka * D + ca));
           const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + kc * D + cc));
           const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
@@ -827,7 +836,7 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   for (int j = 0; j < LOADS; ++j) {
     const int slot = j * 64 + lane, key = slot / CH, cp = slot % CH;
     koff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ kswz<D>(key)) * 16);
-    voff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ vswz(key)) * 16);
+    voff[j] = (uint32_t)key * row_bytes + (uint32_t)((cp ^ vswz<D>(key)) * 16);
   }
 #define DM_LOAD(KD_, VD_, t_)                                                                                \
   _Pragma("unroll") for (int j = 0; j < LOADS; ++j) {                                                       \
@@ -891,8 +900,8 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const int col = db * 32 + tr_col;
-        const int ca = ((col >> 3) ^ vswz(ka)) * 8 + (col & 7);
-        const int cc = ((col >> 3) ^ vswz(kc)) * 8 + (col & 7);
+        const int ca = ((col >> 3) ^ vswz<D>(ka)) * 8 + (col & 7);
+        const int cc = ((col >> 3) ^ vswz<D>(kc)) * 8 + (col & 7);
         const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + ka * D + ca));
         const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(vbase + kc * D + cc));
         const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
