@@ -612,7 +612,7 @@ hipError_t launch_attention(hipStream_t s, rp_dtype dt, const SeqTable& st, cons
 // part[(item * nchunks + c) * D], whole 128-byte lines written by one wave, then the
 // (max, sum) pairs at part[B * Hq * nchunks * D + (item * nchunks + c) * 2].
 // ------------------------------------------------------------------------------------
-constexpr int DC_KEYS = 512;  // keys per chunk (one wave)
+constexpr int DC_KEYS = 1024;  // keys per chunk (one wave)
 constexpr int DC_MAXG = 8;    // q heads per kv head (validated on the host)
 
 template <typename T, int D>
@@ -773,13 +773,18 @@ __global__ __launch_bounds__(256) void k_decode_attn_part(const T* __restrict__ 
 // direct global->LDS loads through a buffer resource whose extent ends at the
 // sequence's last key, so rows past it read as zeros; the wave needs no barrier: the
 // compiler waits on the loads that filled a stage before reading it, and a stage is
-// refilled only after the MFMAs that consumed it.
+// refilled only after the MFMAs that consumed it.  A workgroup holds DC_WAVES waves, the
+// consecutive chunks of one group; at the end they combine their (max, sum, o) through
+// LDS and the group writes one partial record, so the partials written and merged are a
+// DC_WAVES-th of one record per chunk.
+constexpr int DC_WAVES = 3;
+__host__ __device__ inline int decode_groups(int nchunks) { return (nchunks + DC_WAVES - 1) / DC_WAVES; }
 template <typename T16, int D>
-__global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__ q, int q_ld,
-                                                         const T16* __restrict__ ck, const T16* __restrict__ cv,
-                                                         const int32_t* __restrict__ kv_len, int cap, int max_pos,
-                                                         int B, int Hq, int Hkv, float scale, int nchunks,
-                                                         float* __restrict__ part) {
+__global__ __launch_bounds__(64 * DC_WAVES) void k_decode_attn_mfma(const T16* __restrict__ q, int q_ld,
+                                                                    const T16* __restrict__ ck, const T16* __restrict__ cv,
+                                                                    const int32_t* __restrict__ kv_len, int cap,
+                                                                    int max_pos, int B, int Hq, int Hkv, float scale,
+                                                                    int nchunks, float* __restrict__ part) {
 #if defined(__HIP_DEVICE_COMPILE__)
   typedef Half16<T16> H;
   typedef typename H::V8 V8;
@@ -790,12 +795,20 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   constexpr int DB = D / 32;
   constexpr int LOADS = (KT * CH) / 64;  // load instructions per matrix per tile
   static_assert(NT % 3 == 0 || NT > 3, "ring");
-  __shared__ u32x4_t Ks0[KT * CH], Ks1[KT * CH], Ks2[KT * CH], Vs0[KT * CH], Vs1[KT * CH], Vs2[KT * CH];
-  const int lane = threadIdx.x;
-  // kv head fastest: the Hkv waves that read the same cache rows (each its own 2*D-byte
-  // slice of a row) are dispatched together, so each row is fetched from HBM while open
-  const int g = blockIdx.x % Hkv, bc = blockIdx.x / Hkv;
-  const int c = bc % nchunks, b = bc / nchunks;
+  constexpr int PSL = KT * CH * 4 / 64;  // floats per lane in one K stage
+  static_assert(DB * 16 <= 2 * PSL && PSL >= 2, "merge data fits the wave's K stages");
+  __shared__ u32x4_t Ksa[DC_WAVES][KT * CH], Ksb[DC_WAVES][KT * CH], Ksc[DC_WAVES][KT * CH];
+  __shared__ u32x4_t Vsa[DC_WAVES][KT * CH], Vsb[DC_WAVES][KT * CH], Vsc[DC_WAVES][KT * CH];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  u32x4_t *Ks0 = Ksa[wave], *Ks1 = Ksb[wave], *Ks2 = Ksc[wave];
+  u32x4_t *Vs0 = Vsa[wave], *Vs1 = Vsb[wave], *Vs2 = Vsc[wave];
+  // kv head fastest: the Hkv workgroups that read the same cache rows (each its own
+  // 2*D-byte slice of a row) are dispatched together, so each row is fetched while open
+  const int nrec = decode_groups(nchunks);
+  const int g = blockIdx.x % Hkv, bgr = blockIdx.x / Hkv;
+  const int grp = bgr % nrec, b = bgr / nrec;
+  const int c = grp * DC_WAVES + wave;
   const int G = Hq / Hkv;
   // query columns: lane column fr is q head g*G + fr (zero beyond G); issued first, so they
   // are in flight while kv_len is read and are covered by the wait for the first tile
@@ -809,18 +822,14 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   }
   const int n = min(max(kv_len[b], 0), min(cap, max_pos) - 1);  // keys 0..n
   const int k_begin = c * DC_KEYS;
-  const int nkeys = min(DC_KEYS, n + 1 - k_begin);
-  const int64_t rec = (int64_t)(b * Hq + g * G) * nchunks + c;
-  float* out = part + rec * D;                                  // o records
-  float* oml = part + (int64_t)B * Hq * nchunks * D + rec * 2;  // (max, sum)
-  const int64_t head_stride = (int64_t)nchunks * D, ml_stride = (int64_t)nchunks * 2;
-  if (nkeys <= 0) {
-    if (lane < G) {
-      oml[lane * ml_stride] = -INFINITY;
-      oml[lane * ml_stride + 1] = 0.f;
-    }
-    return;
-  }
+  const int nkeys = c < nchunks ? min(DC_KEYS, n + 1 - k_begin) : 0;
+  f32x16_t o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[db][e] = 0.f;
+  float m_run = kMaskVal, l_run = 0.f;
+  if (nkeys > 0) {  // (uniform) this wave's chunk holds keys
   const int ntiles = (nkeys + KT - 1) / KT;
   // keys of this chunk as a buffer resource: rows k_begin .. n of (b, g); byte offsets
   // key * row_bytes fit 32 bits (cap * Hkv * D * 2 bytes is checked on the host)
@@ -843,12 +852,6 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsK, (lds_void_t*)((KD_) + j * 64), 16, koff[j] + (uint32_t)(t_) * KT * row_bytes, 0, 0, 0); \
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsV, (lds_void_t*)((VD_) + j * 64), 16, voff[j] + (uint32_t)(t_) * KT * row_bytes, 0, 0, 0); \
   }
-  f32x16_t o[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[db][e] = 0.f;
-  float m_run = kMaskVal, l_run = 0.f;
   const float c2 = scale * 1.4426950408889634f;
   const int tr_p = lane & 15;
   const int tr_key = fk * 4 + (tr_p >> 2);
@@ -942,12 +945,68 @@ __global__ __launch_bounds__(64) void k_decode_attn_mfma(const T16* __restrict__
   if (r > 3) tile(Ks1, Vs1, t + 3);
   if (r > 4) tile(Ks2, Vs2, t + 4);
 #undef DM_LOAD
-  __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the wave
-  // o[db][e] = O^T(dim db*32 + 8(e/4) + 4 fk + e%4, head fr), unnormalised
-  const float l = l_run + __shfl_xor(l_run, 32, kWave);
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed: its stages are free
+  }
+  // ---- combine the group's chunks: waves 1.. leave o in their own first two K stages and
+  // (max, sum) in the third (lane-major, conflict-free); wave 0 rescales them to the
+  // common max and adds ----
+  // o[db][e] = O^T(dim db*32 + 8(e/4) + 4 fk + e%4, head fr), unnormalised; m in log2 units
+  if (wave > 0) {
+    float* mine0 = reinterpret_cast<float*>(Ks0);
+    float* mine1 = reinterpret_cast<float*>(Ks1);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int i = db * 16 + e;
+        (i < PSL ? mine0 : mine1)[(i % PSL) * 64 + lane] = o[db][e];
+      }
+    reinterpret_cast<float*>(Ks2)[lane] = m_run;
+    reinterpret_cast<float*>(Ks2)[64 + lane] = l_run;
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  if (nkeys <= 0) {  // the group's first chunk is past the last key: so are the others
+    if (lane < G) {
+      const int64_t rec = (int64_t)(b * Hq + g * G + lane) * nrec + grp;
+      *reinterpret_cast<float2*>(part + (int64_t)B * Hq * nrec * D + rec * 2) = make_float2(-INFINITY, 0.f);
+    }
+    return;
+  }
+  float mw[DC_WAVES], M = m_run;
+  mw[0] = m_run;
+#pragma unroll
+  for (int w = 1; w < DC_WAVES; ++w) {
+    mw[w] = reinterpret_cast<const float*>(Ksc[w])[lane];
+    M = fmaxf(M, mw[w]);
+  }
+  const float f0 = __builtin_amdgcn_exp2f(m_run - M);
+  float lsum = l_run * f0;
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[db][e] *= f0;
+#pragma unroll
+  for (int w = 1; w < DC_WAVES; ++w) {
+    const float* t0 = reinterpret_cast<const float*>(Ksa[w]);
+    const float* t1 = reinterpret_cast<const float*>(Ksb[w]);
+    const float fw = __builtin_amdgcn_exp2f(mw[w] - M);  // 0 for an empty chunk (max kMaskVal)
+    lsum = fmaf(reinterpret_cast<const float*>(Ksc[w])[64 + lane], fw, lsum);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int i = db * 16 + e;
+        o[db][e] = fmaf((i < PSL ? t0 : t1)[(i % PSL) * 64 + lane], fw, o[db][e]);
+      }
+  }
+  const float l = lsum + __shfl_xor(lsum, 32, kWave);
   if (fr < G) {
-    float* oh = out + fr * head_stride;
-    if (fk == 0) *reinterpret_cast<float2*>(oml + fr * ml_stride) = make_float2(m_run * 0.6931471805599453f, l);
+    const int64_t rec = (int64_t)(b * Hq + g * G + fr) * nrec + grp;
+    float* oh = part + rec * D;
+    if (fk == 0)
+      *reinterpret_cast<float2*>(part + (int64_t)B * Hq * nrec * D + rec * 2) =
+          make_float2(M * 0.6931471805599453f, l);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -1029,17 +1088,20 @@ hipError_t launch_decode_attention(hipStream_t s, rp_dtype dt, const void* q, in
   }
   // the 16-bit kernel addresses a sequence's cache rows with 32-bit byte offsets
   if ((int64_t)cap * Hkv * D * 2 > (int64_t)INT32_MAX) return hipErrorInvalidValue;
-  const int grid = B * Hkv * nchunks;  // one wave per chunk
+  const int nrec = decode_groups(nchunks);
+  const int grid = B * Hkv * nrec;  // one workgroup per group of DC_WAVES chunks
   with_half16(dt, [&](auto tag_) {
     using H = decltype(tag_);
     if (D == 128) {
-      k_decode_attn_mfma<H, 128><<<grid, 64, 0, s>>>((const H*)q, q_ld, (const H*)cache_k, (const H*)cache_v, kv_len,
-                                                    cap, max_pos, B, Hq, Hkv, scale, nchunks, partials);
-      k_decode_attn_merge<H, 128><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nchunks, B * Hq, (H*)o);
+      k_decode_attn_mfma<H, 128><<<grid, 64 * DC_WAVES, 0, s>>>((const H*)q, q_ld, (const H*)cache_k,
+                                                               (const H*)cache_v, kv_len, cap, max_pos, B, Hq, Hkv,
+                                                               scale, nchunks, partials);
+      k_decode_attn_merge<H, 128><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nrec, B * Hq, (H*)o);
     } else {
-      k_decode_attn_mfma<H, 64><<<grid, 64, 0, s>>>((const H*)q, q_ld, (const H*)cache_k, (const H*)cache_v, kv_len,
-                                                   cap, max_pos, B, Hq, Hkv, scale, nchunks, partials);
-      k_decode_attn_merge<H, 64><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nchunks, B * Hq, (H*)o);
+      k_decode_attn_mfma<H, 64><<<grid, 64 * DC_WAVES, 0, s>>>((const H*)q, q_ld, (const H*)cache_k,
+                                                              (const H*)cache_v, kv_len, cap, max_pos, B, Hq, Hkv,
+                                                              scale, nchunks, partials);
+      k_decode_attn_merge<H, 64><<<(B * Hq + 3) / 4, 256, 0, s>>>(partials, nrec, B * Hq, (H*)o);
     }
   });
   return hipGetLastError();

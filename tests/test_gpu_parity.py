@@ -164,9 +164,12 @@ UNEXPLAINED_FAULT = pytest.mark.skip(reason="disabled in the library (RP_ERR_UNS
 @pytest.mark.parametrize("model,cap,lens", [(BF16_SMALL, 300, [0, 1, 63, 256, 299]),
                                             (configs.TINY, 300, [0, 1, 63, 256, 299]),
                                             (F16_SMALL, 300, [0, 1, 63, 256, 299]),
-                                            # several 512-key chunks per sequence, chunk edges
+                                            # 1024-key chunks (16-bit: three per workgroup),
+                                            # chunk and workgroup edges
                                             (BF16_SMALL, 1100, [511, 512, 1023, 700, 1099]),
                                             (configs.TINY, 1100, [0, 513, 1024, 1099, 5]),
+                                            (BF16_SMALL, 3300, [1023, 1024, 2047, 3071, 3072, 3299, 0]),
+                                            (configs.TINY, 3300, [3072, 2048, 1, 3299]),
                                             (F16_D64, 400, [0, 131, 399]),
                                             pytest.param(BF16_D64, 400, [0, 131, 399], marks=UNEXPLAINED_FAULT)])
 def test_decode_step_matches_oracle(model, cap, lens):
