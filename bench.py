@@ -179,7 +179,7 @@ def colocation(args, w):
         T_D = step_ms * steps
         streams = [("unmasked (MPS-Default analog)", torch.cuda.Stream(), torch.cuda.Stream(), None)]
         if regime == "balanced":
-            for k in (32, 64, 96, 128):
+            for k in (32, 64, 80, 96, 112, 128):
                 sd = rb.rp_stream_create_cu_masked(0, mask(0, k))
                 sa = rb.rp_stream_create_cu_masked(0, mask(k, ncu))
                 streams.append((f"decode {k} CUs / prefix {ncu - k} CUs", torch.cuda.ExternalStream(sa),
