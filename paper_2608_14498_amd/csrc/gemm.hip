@@ -756,7 +756,10 @@ void k_gemm_bf16_dma(GemmArgs g) {
     D_MMA(af0, bf0);                                                          \
     D_REGION(0, 0x000);                                                       \
     __builtin_amdgcn_sched_barrier(0);                                        \
-    __syncthreads();                                                          \
+    /* every copy of this wave has landed before any wave passes: the next */ \
+    /* slab is read from rows other waves copied (a plain __syncthreads()  */ \
+    /* did not always wait for the LDS-DMA copies)                         */ \
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); \
     D_FRAGS(af0, bf0, DA, DB, 0);                                             \
     D_MMA(af1, bf1);                                                          \
     D_LOAD(SA, SB, min((kt_) + 2, KT - 1));                                   \
