@@ -1195,7 +1195,7 @@ rp_status rp_decode_step_static(const rp_model* m, void* stream, int32_t B, rp_k
 }
 
 rp_status rp_profile_enable(int enable, int32_t max_launches) {
-  for (hipEvent_t e : g_prof.ev) hipEventDestroy(e);
+  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);  // teardown of timing events: nothing to report
   g_prof.ev.clear();
   g_prof.pending.clear();
   g_prof.on = false;
