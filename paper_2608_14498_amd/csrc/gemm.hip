@@ -624,14 +624,17 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 
 // ------------------------------------------------------------------------------------
 // bf16 MFMA GEMM fed by direct global->LDS loads (global_load_lds_dwordx4).
-// Same tile, wave layout, swizzle and epilogues as k_gemm_bf16, but the next slab is
-// copied straight into the idle LDS buffer by the load unit: the loads of slab kt+1 are
-// issued at the start of slab kt and have the whole slab's MFMA time to land (the
-// register-staged pipeline gives them about half of it), and no VGPRs or LDS store
-// instructions are spent on staging.  One load instruction writes 64 consecutive 16-byte
+// Same tile, wave layout, swizzle and epilogues as k_gemm_bf16, but the coming slabs are
+// copied straight into idle LDS buffers by the load unit, with no VGPRs or LDS store
+// instructions spent on staging.  One load instruction writes 64 consecutive 16-byte
 // LDS chunks (8 rows of one slab); the swizzle is applied by choosing which global
-// chunk each lane fetches.  The two LDS buffers are separate arrays and the k loop is
-// unrolled by two, so every LDS access names its buffer at compile time.
+// chunk each lane fetches.  The 8-wave form keeps three A slabs and two B slabs in LDS
+// (5 x 32 KiB, all of the CU's 160 KiB): A copies are issued two slabs ahead, B copies
+// one slab ahead, so each slab barrier waits only for the B copies issued one slab
+// earlier (with two stages of both, for all of them: the matrix cores were busy 68-69%
+// of the cycles and the prefix GEMMs took 4-6% longer).  The 4-wave form keeps two of
+// each.  The buffers are separate arrays and the k loop is unrolled over their
+// rotation (6 slabs, or 2), so every LDS access names its buffer at compile time.
 // ------------------------------------------------------------------------------------
 template <int EPI, typename T16, int WGM, bool BT = false>
 __global__ __launch_bounds__(WGM * 128) __attribute__((amdgpu_waves_per_eu(WGM == 2 ? 1 : 2, WGM == 2 ? 1 : 2)))
@@ -647,7 +650,7 @@ void k_gemm_bf16_dma(GemmArgs g) {
   typedef typename Half16<T16>::V8 V8;
   // native vector element type: each fragment read is one 16-byte LDS load in the IR
   typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-  __shared__ u32x4_t As0[GB_M * 8], As1[GB_M * 8];
+  __shared__ u32x4_t As0[GB_M * 8], As1[GB_M * 8], As2[GB_M * 8];
   __shared__ u32x4_t Bs0[GB_N * 8], Bs1[GB_N * 8];
 
   // 128x128 wave tiles hold 256 accumulator registers, which must live in the AGPR file.
@@ -712,6 +715,14 @@ void k_gemm_bf16_dma(GemmArgs g) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB[i], (lds_void*)(DB + (wave * LOADS + i) * 64), 16, boff[i], \
                                              (int)((uint32_t)(kt_) * bstep), 0, 0);                   \
   }
+#define D_LOADA(DA, kt_)                                                                               \
+  _Pragma("unroll") for (int i = 0; i < LOADS; ++i)                                                   \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)(DA + (wave * LOADS + i) * 64), 16, aoff[i], \
+                                             (kt_) * (GB_K * 2), 0, 0);
+#define D_LOADB(DB, kt_)                                                                               \
+  _Pragma("unroll") for (int i = 0; i < LOADS; ++i)                                                   \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB[i], (lds_void*)(DB + (wave * LOADS + i) * 64), 16, boff[i], \
+                                             (int)((uint32_t)(kt_) * bstep), 0, 0);
 #define D_FRAGS(AF, BF, SA, SB, ks_)                                          \
   _Pragma("unroll") for (int i = 0; i < MI; ++i) {                            \
     const int r_ = wm * TM + i * 32 + fr;                                     \
@@ -733,9 +744,12 @@ void k_gemm_bf16_dma(GemmArgs g) {
   // The barrier sits before the last k-step: every wave's copies of slab kt_+1 have
   // landed and every wave has finished reading (SA, SB), so the fragments of k-step 0 of
   // the next slab are read (from DA, DB) under the MFMAs of k-step 3, and the copies of
-  // slab kt_+2 go into (SA, SB) right there.  Issued straight after the barrier, a slab's
-  // copies have a whole slab of MFMA time to land and each CU keeps L2 misses in flight
-  // without a gap (the misses' fabric bandwidth, not the MFMAs, bounds the large GEMMs).
+  // the coming slabs go into (SA, SB) right there.  Issued straight after the barrier,
+  // copies have at least a whole slab of MFMA time to land and each CU keeps L2 misses in
+  // flight without a gap (the misses' fabric bandwidth, not the MFMAs, bounds the large
+  // GEMMs).  D_TILE (4 waves, two stages of A and B) issues slab kt_+2 and waits for
+  // every copy; D_TILE3 (8 waves) issues B of slab kt_+2, then A of slab kt_+3, and
+  // leaves those last LOADS copies (A, two slabs ahead) in flight at the barrier.
 #define D_REGION(n_mem_, mem_mask_)                                                        \
   __builtin_amdgcn_sched_group_barrier(0x100, NREAD, 0);                                   \
   _Pragma("unroll") for (int q = 0; q < MM; ++q) {                                         \
@@ -766,6 +780,30 @@ void k_gemm_bf16_dma(GemmArgs g) {
     D_REGION(2 * LOADS, 0x010);                                               \
     __builtin_amdgcn_sched_barrier(0);                                        \
   }
+#define D_TILE3(SA, SB, DA, DB, kt_)                                          \
+  {                                                                           \
+    D_FRAGS(af1, bf1, SA, SB, 1);                                             \
+    D_MMA(af0, bf0);                                                          \
+    D_REGION(0, 0x000);                                                       \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+    D_FRAGS(af0, bf0, SA, SB, 2);                                             \
+    D_MMA(af1, bf1);                                                          \
+    D_REGION(0, 0x000);                                                       \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+    D_FRAGS(af1, bf1, SA, SB, 3);                                             \
+    D_MMA(af0, bf0);                                                          \
+    D_REGION(0, 0x000);                                                       \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+    /* this wave's copies of slab kt_+1 (its A issued two slabs ago, its B */ \
+    /* one slab ago) have landed; the last LOADS copies (A of kt_+2) may not */ \
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LOADS) : "memory"); \
+    D_FRAGS(af0, bf0, DA, DB, 0);                                             \
+    D_MMA(af1, bf1);                                                          \
+    D_LOADB(SB, min((kt_) + 2, KT - 1));                                      \
+    D_LOADA(SA, min((kt_) + 3, KT - 1));                                      \
+    D_REGION(2 * LOADS, 0x010);                                               \
+    __builtin_amdgcn_sched_barrier(0);                                        \
+  }
 
   f32x16_t acc[MI][NJ];
 #pragma unroll
@@ -779,29 +817,58 @@ void k_gemm_bf16_dma(GemmArgs g) {
   int btoff[NJ];
   if (BT) bt_offsets<NJ>(lane, wn * TN, btoff);
   V8 af0[MI], bf0[NJ], af1[MI], bf1[NJ];
-  if (KT > 0) {
-    D_LOAD(As0, Bs0, 0);
-    __syncthreads();
-    D_FRAGS(af0, bf0, As0, Bs0, 0);
-    D_LOAD(As1, Bs1, min(1, KT - 1));  // beyond the last slab: a harmless re-load into an idle buffer
-    int kt = 0;
-    for (; kt + 2 <= KT; kt += 2) {
-      D_TILE(As0, Bs0, As1, Bs1, kt);
-      D_TILE(As1, Bs1, As0, Bs0, kt + 1);
+  if (WGM == 2) {
+    if (KT > 0) {
+      D_LOAD(As0, Bs0, 0);
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+      D_FRAGS(af0, bf0, As0, Bs0, 0);
+      D_LOAD(As1, Bs1, min(1, KT - 1));  // beyond the last slab: a harmless re-load into an idle buffer
+      int kt = 0;
+      for (; kt + 2 <= KT; kt += 2) {
+        D_TILE(As0, Bs0, As1, Bs1, kt);
+        D_TILE(As1, Bs1, As0, Bs0, kt + 1);
+      }
+      if (kt < KT) D_TILE(As0, Bs0, As1, Bs1, kt);
     }
-    if (kt < KT) D_TILE(As0, Bs0, As1, Bs1, kt);
+  } else if (KT > 0) {
+    // slab s lives in As[s % 3] and Bs[s % 2]; past the last slab the copies re-load it
+    // into a buffer no later slab reads
+    D_LOADA(As0, 0);
+    D_LOADB(Bs0, 0);
+    D_LOADA(As1, min(1, KT - 1));
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    D_FRAGS(af0, bf0, As0, Bs0, 0);
+    D_LOADB(Bs1, min(1, KT - 1));
+    D_LOADA(As2, min(2, KT - 1));
+    int kt = 0;
+    for (; kt + 6 <= KT; kt += 6) {
+      D_TILE3(As0, Bs0, As1, Bs1, kt);
+      D_TILE3(As1, Bs1, As2, Bs0, kt + 1);
+      D_TILE3(As2, Bs0, As0, Bs1, kt + 2);
+      D_TILE3(As0, Bs1, As1, Bs0, kt + 3);
+      D_TILE3(As1, Bs0, As2, Bs1, kt + 4);
+      D_TILE3(As2, Bs1, As0, Bs0, kt + 5);
+    }
+    if (kt < KT) D_TILE3(As0, Bs0, As1, Bs1, kt);
+    if (kt + 1 < KT) D_TILE3(As1, Bs1, As2, Bs0, kt + 1);
+    if (kt + 2 < KT) D_TILE3(As2, Bs0, As0, Bs1, kt + 2);
+    if (kt + 3 < KT) D_TILE3(As0, Bs1, As1, Bs0, kt + 3);
+    if (kt + 4 < KT) D_TILE3(As1, Bs0, As2, Bs1, kt + 4);
   }
 #undef D_LOAD
+#undef D_LOADA
+#undef D_LOADB
 #undef D_FRAGS
 #undef D_MMA
 #undef D_TILE
+#undef D_TILE3
 #undef D_REGION
+  // no copy into LDS is still in flight past here (the last slabs' re-loads included)
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   if (EPI == EPI_LSE) {
-    __syncthreads();  // no copy into LDS outlives the workgroup
     gemm_epilogue_lse<MI, NJ, TM, TN>(g, acc, tm, tn, wm, wn, lane & 31, lane >> 5);
     return;
   }
-  __syncthreads();  // every wave is done with the slab buffers
   uint8_t* stage = WGM == 2 ? (uint8_t*)(wave == 0 ? As0 : wave == 1 ? As1 : wave == 2 ? Bs0 : Bs1)
                             : (uint8_t*)(wave < 2 ? As0 : wave < 4 ? As1 : wave < 6 ? Bs0 : Bs1) + (wave & 1) * 16384;
   gemm_epilogue_lds<EPI, T16, MI, NJ, TM, TN>(g, acc, stage, tm, tn, wm, wn, lane);
