@@ -1021,14 +1021,16 @@ static void launch_half(hipStream_t s, GemmArgs& g, dim3 grid, int64_t b_rows, b
 // Such a product reads each weight once and is bound by HBM bandwidth, so the weights
 // are streamed, not tiled for reuse.  A workgroup of SW waves owns 32*SW adjacent
 // columns (32 per wave) and one K split, and walks the split's 64-deep k slabs through a
-// 3-stage LDS ring filled by direct global->LDS loads: per stage one A slab (the few
+// 2-stage LDS ring filled by direct global->LDS loads: per stage one A slab (the few
 // rows, copied once and shared by the waves; rows past M repeat row M-1 and their
 // results are dropped) and each wave's 32 B rows (8 lanes read a whole 128-byte row
-// segment).  Per slab t: wait for this wave's copies of slab t (those of t+1 stay in
-// flight), barrier (every wave's copies of t have landed and every wave is done with the
-// stage that takes t+2), issue the copies of t+2, then the MFMAs of t.  The steady state
-// issues every copy unconditionally (past the end it re-reads the last slab), so the
-// outstanding count is known statically.  The MFMA takes the B fragment first and each
+// segment).  Per slab t: wait for this wave's copies of slab t, barrier (every wave's
+// copies of t have landed and every wave is done with the stage that takes t+1), issue
+// the copies of t+1, then the MFMAs of t.  At 64 rows a workgroup holds 48 KiB of LDS,
+// so three fit on a CU and a launch of up to 768 workgroups runs in one round (a 3-stage
+// ring, 72 KiB, fitted two: the 592 workgroups of a 7B decode gate/up projection ran in
+// two rounds, and the decode step took 1.5% longer).  Past the end the copies re-read
+// the last slab into the idle stage.  The MFMA takes the B fragment first and each
 // fragment has the k order of the tiled kernels, so every output is the MFMA chain it is
 // there (the same bits).  A transposed B ([K][N] storage) is staged k-row-major and read
 // with ds_read_b64_tr_b16 into the same fragments.  Output fp32 [split][M][ldo]
@@ -1058,10 +1060,9 @@ __global__ __launch_bounds__(SW * 64) void k_gemm_skinny(SkinnyArgs g) {
   constexpr int BCH = 32 * 8;        // B chunks per wave per stage: 32 columns x 64 k
   constexpr int AL = ACH / 64 / SW;  // A copy instructions per wave per stage
   constexpr int BL = BCH / 64;       // B copy instructions per wave per stage
-  constexpr int L = AL + BL;         // copies per wave per stage
   static_assert(AL >= 1 && ACH % (64 * SW) == 0, "A stage split over the waves");
-  __shared__ u32x4_t As0[ACH], As1[ACH], As2[ACH];
-  __shared__ u32x4_t Bs0[SW * BCH], Bs1[SW * BCH], Bs2[SW * BCH];
+  __shared__ u32x4_t As0[ACH], As1[ACH];
+  __shared__ u32x4_t Bs0[SW * BCH], Bs1[SW * BCH];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int fr = lane & 31, fk = lane >> 5;
@@ -1147,21 +1148,19 @@ __global__ __launch_bounds__(SW * 64) void k_gemm_skinny(SkinnyArgs g) {
       }
     }
   };
-  // Wait for this wave's copies of the slab about to be read (exactly L copies, those of
-  // the next slab, may stay outstanding) and for its LDS reads, then the barrier.  The
-  // asm also keeps the compiler from moving LDS accesses across the barrier.
+  // Wait for this wave's copies of the slab about to be read and for its LDS reads, then
+  // the barrier.  The asm also keeps the compiler from moving LDS accesses across the
+  // barrier.
 #define SK_STEP(AC_, BC_, AN_, BN_, tt_)                                                \
   {                                                                                     \
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(L) : "memory");    \
-    load(AN_, BN_, min((tt_) + 2, nst - 1));                                            \
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");          \
+    load(AN_, BN_, min((tt_) + 1, nst - 1));                                            \
     if ((tt_) < nst) slab(AC_, BC_);                                                    \
   }
   load(As0, Bs0, 0);
-  load(As1, Bs1, min(1, nst - 1));
-  for (int t = 0; t < nst; t += 3) {
-    SK_STEP(As0, Bs0, As2, Bs2, t);
+  for (int t = 0; t < nst; t += 2) {
+    SK_STEP(As0, Bs0, As1, Bs1, t);
     SK_STEP(As1, Bs1, As0, Bs0, t + 1);
-    SK_STEP(As2, Bs2, As1, Bs1, t + 2);
   }
 #undef SK_STEP
   __builtin_amdgcn_s_waitcnt(0);  // no copy into LDS outlives the wave
