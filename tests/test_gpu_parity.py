@@ -47,6 +47,13 @@ BF16_D64 = configs.ModelShape(n_layers=2, d_model=256, n_q_heads=8, n_kv_heads=2
 # so that the down projection's partials are summed by the next layer's attention norm
 BF16_WIDE = configs.ModelShape(n_layers=2, d_model=2048, n_q_heads=16, n_kv_heads=2, head_dim=128,
                                ffn_dim=4096, vocab=1000, dtype="bf16")
+# contraction depths of 5, 3 and 7 slabs of 64 (q/k/v and gate/up, O-proj, down) and of 2,
+# 2 and 1: the tiled GEMM's slab ring ends after every possible remainder, and on the
+# shortest K ranges its prologue re-loads the last slab
+BF16_ODD_K = configs.ModelShape(n_layers=2, d_model=320, n_q_heads=3, n_kv_heads=1, head_dim=64,
+                                ffn_dim=448, vocab=1000, dtype="bf16")
+BF16_SHORT_K = configs.ModelShape(n_layers=2, d_model=128, n_q_heads=2, n_kv_heads=1, head_dim=64,
+                                  ffn_dim=64, vocab=1000, dtype="bf16")
 # the same models stored in fp16 (same kernels, fp16 MFMA)
 F16_SMALL = replace(BF16_SMALL, dtype="f16")
 F16_D64 = replace(BF16_D64, dtype="f16")
@@ -55,6 +62,7 @@ F16_WIDE = replace(BF16_WIDE, dtype="f16")
 
 @pytest.mark.parametrize("model,norm,bias", [(BF16_SMALL, "ones", False), (BF16_SMALL, "random", True),
                                              (BF16_D64, "random", True), (BF16_WIDE, "random", True),
+                                             (BF16_ODD_K, "random", True), (BF16_SHORT_K, "random", True),
                                              (F16_SMALL, "random", True), (F16_D64, "random", True),
                                              (F16_WIDE, "random", True)])
 def test_bf16_ragged_batch_matches_oracle(model, norm, bias):
