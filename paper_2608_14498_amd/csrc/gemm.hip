@@ -635,8 +635,9 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 // of the cycles and the prefix GEMMs took 4-6% longer).  Three A stages instead gain as
 // much time, but the early A copies cost the gate/up GEMM 23% more L2 misses (its B
 // panels are shared by twice as many concurrent tiles as its A panels).  The 4-wave
-// form keeps two of each.  The buffers are separate arrays and the k loop is unrolled over their
-// rotation (6 slabs, or 2), so every LDS access names its buffer at compile time.
+// form keeps two of each.  The buffers are separate arrays and the k loop is unrolled
+// over their rotation (6 slabs, or 2), so every LDS access names its buffer at compile
+// time.
 // ------------------------------------------------------------------------------------
 template <int EPI, typename T16, int WGM, bool BT = false>
 __global__ __launch_bounds__(WGM * 128) __attribute__((amdgpu_waves_per_eu(WGM == 2 ? 1 : 2, WGM == 2 ? 1 : 2)))
@@ -645,7 +646,7 @@ void k_gemm_bf16_dma(GemmArgs g) {
   constexpr int NT = WGM * 2 * 64;
   constexpr int TM = GB_M / WGM, TN = GB_N / 2;
   constexpr int MI = TM / 32, NJ = TN / 32;
-  constexpr int LOADS = (GB_M * 8) / NT;  // load instructions per matrix per wave: 4
+  constexpr int LOADS = (GB_M * 8) / NT;  // load instructions per matrix per wave: 4 (8 waves) or 8
   constexpr int MM = MI * NJ;
   constexpr int NREAD = MI + (BT ? 2 : 1) * NJ;  // LDS fragment reads per k-step
   typedef __attribute__((address_space(3))) void lds_void;
