@@ -781,14 +781,16 @@ rp_status prefix_run(const rp_model* m, void* stream, int32_t B, const int32_t* 
                                                                c.head_dim, rope_cs));
 
   RP_TRY_LAUNCH_N("prefix.visual_index", rp::launch_visual_index(s, token_ids, (int32_t)T, vis_idx));
-  RP_TRY_LAUNCH_N("prefix.embed", rp::launch_embed(s, dt, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab, (int32_t)T,
-                                 c.d_model, w.X));
+  // the embedding kernel also applies the first layer's attention norm
+  RP_TRY_LAUNCH_N("prefix.embed_norm", rp::launch_embed(s, dt, token_ids, vis_idx, visual, n_visual, m->embed, c.vocab,
+                                                        (int32_t)T, c.d_model, w.X, m->layers[0].attn_norm, c.rms_eps,
+                                                        w.N));
   for (int l = 0; l < c.n_layers; ++l) {
     void* kl = layer_ptr(m, kv_out.k, kv_out.layer_stride, l);
     void* vl = layer_ptr(m, kv_out.v, kv_out.layer_stride, l);
     if (last_rows && l == c.n_layers - 1)
       return dbg.end(run_last_rows(m, s, m->layers[l], B, cu, tab, (int32_t)T, w, tail, kl, vl, mr, h_last));
-    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames, mr, false,
+    st = run_layer(m, s, m->layers[l], tab, (int32_t)T, w, kl, vl, kl, vl, plan, nullptr, kPrefixNames, mr, l == 0,
                    nullptr, nullptr, rope_cs);
     if (st != RP_OK) return st;
   }

@@ -37,14 +37,79 @@ hipError_t launch_visual_index(hipStream_t s, const int32_t* ids, int32_t T, int
 }
 
 // ------------------------------------------------------------------------------------
-// Embedding + visual splice -> fp32 residual rows.
+// RMSNorm: out = x / sqrt(mean(x^2) + eps) * w, fp32 math, stored as T.
+// ------------------------------------------------------------------------------------
+// load(c, v) hands over the row's values c .. c+7.
+template <typename T, typename Load>
+__device__ __forceinline__ void rmsnorm_row_from(Load load, const T* __restrict__ w, float eps, int d,
+                                                 T* __restrict__ out, float* red) {
+  constexpr int kMaxChunks = 4;  // rows of up to 4 x 8 values per thread stay in registers
+  const int step = blockDim.x * 8;
+  if (d <= kMaxChunks * step) {
+    // one read of the row; the same summation order as the two-pass loop below
+    float v[kMaxChunks][8];
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j) {
+      const int c = threadIdx.x * 8 + j * step;
+      if (c < d) {
+        load(c, v[j]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ss = fmaf(v[j][i], v[j][i], ss);
+      }
+    }
+    const float tot = block_sum(ss, red);
+    const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+    for (int j = 0; j < kMaxChunks; ++j) {
+      const int c = threadIdx.x * 8 + j * step;
+      if (c < d) {
+        float g[8];
+        load8(w + c, g);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[j][i] = v[j][i] * inv * g[i];
+        store8(out + c, v[j]);
+      }
+    }
+    return;
+  }
+  float ss = 0.f;
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8];
+    load(c, v);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
+  }
+  const float tot = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8], g[8];
+    load(c, v);
+    load8(w + c, g);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = v[i] * inv * g[i];
+    store8(out + c, v);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void rmsnorm_row(const float* __restrict__ x, const T* __restrict__ w,
+                                            float eps, int d, T* __restrict__ out, float* red) {
+  rmsnorm_row_from([&](int c, float(&v)[8]) { load8(x + c, v); }, w, eps, d, out, red);
+}
+
+// ------------------------------------------------------------------------------------
+// Embedding + visual splice -> fp32 residual rows; with norm_w, also the first layer's
+// RMSNorm of each row, from the same registers (one pass over the row).
 // ------------------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ ids,
                                                const int32_t* __restrict__ vis_idx,
                                                const T* __restrict__ visual, int64_t n_visual,
                                                const T* __restrict__ embed, int vocab, int d,
-                                               float* __restrict__ X) {
+                                               float* __restrict__ X, const T* __restrict__ norm_w, float eps,
+                                               T* __restrict__ norm_out) {
+  __shared__ float red[16];
   const int t = blockIdx.x;
   const int id = ids[t];
   const T* src = nullptr;
@@ -55,21 +120,30 @@ __global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ ids,
     src = embed + (int64_t)min(id, vocab - 1) * d;
   }
   float* dst = X + (int64_t)t * d;
-  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
-    float v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  auto load = [&](int c, float(&v)[8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = 0.f;
     if (src) load8(src + c, v);
     store8(dst + c, v);
+  };
+  if (norm_w) {  // the values the norm reads are those stored to X, exactly
+    rmsnorm_row_from(load, norm_w, eps, d, norm_out + (int64_t)t * d, red);
+    return;
+  }
+  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
+    float v[8];
+    load(c, v);
   }
 }
 
 hipError_t launch_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const int32_t* vis_idx,
                         const void* visual, int64_t n_visual, const void* embed, int32_t vocab,
-                        int32_t T, int32_t d, float* X) {
+                        int32_t T, int32_t d, float* X, const void* norm_w, float eps, void* norm_out) {
   if (T <= 0) return hipSuccess;
   with_storage(dt, [&](auto tag_) {
     using E = decltype(tag_);
     k_embed<E><<<T, 256, 0, s>>>(ids, vis_idx, (const E*)visual, n_visual,
-                                      (const E*)embed, vocab, d, X);
+                                      (const E*)embed, vocab, d, X, (const E*)norm_w, eps, (E*)norm_out);
   });
   return hipGetLastError();
 }
@@ -94,61 +168,6 @@ hipError_t launch_decode_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, c
     k_decode_embed<E><<<B, 256, 0, s>>>(ids, (const E*)embed, vocab, d, X);
   });
   return hipGetLastError();
-}
-
-// ------------------------------------------------------------------------------------
-// RMSNorm: out = x / sqrt(mean(x^2) + eps) * w, fp32 math, stored as T.
-// ------------------------------------------------------------------------------------
-template <typename T>
-__device__ __forceinline__ void rmsnorm_row(const float* __restrict__ x, const T* __restrict__ w,
-                                            float eps, int d, T* __restrict__ out, float* red) {
-  constexpr int kMaxChunks = 4;  // rows of up to 4 x 8 values per thread stay in registers
-  const int step = blockDim.x * 8;
-  if (d <= kMaxChunks * step) {
-    // one read of the row; the same summation order as the two-pass loop below
-    float v[kMaxChunks][8];
-    float ss = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxChunks; ++j) {
-      const int c = threadIdx.x * 8 + j * step;
-      if (c < d) {
-        load8(x + c, v[j]);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) ss = fmaf(v[j][i], v[j][i], ss);
-      }
-    }
-    const float tot = block_sum(ss, red);
-    const float inv = 1.0f / sqrtf(tot / (float)d + eps);
-#pragma unroll
-    for (int j = 0; j < kMaxChunks; ++j) {
-      const int c = threadIdx.x * 8 + j * step;
-      if (c < d) {
-        float g[8];
-        load8(w + c, g);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) v[j][i] = v[j][i] * inv * g[i];
-        store8(out + c, v[j]);
-      }
-    }
-    return;
-  }
-  float ss = 0.f;
-  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
-    float v[8];
-    load8(x + c, v);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) ss = fmaf(v[i], v[i], ss);
-  }
-  const float tot = block_sum(ss, red);
-  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x * 8; c < d; c += blockDim.x * 8) {
-    float v[8], g[8];
-    load8(x + c, v);
-    load8(w + c, g);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = v[i] * inv * g[i];
-    store8(out + c, v);
-  }
 }
 
 template <typename T>

@@ -99,9 +99,11 @@ struct BSeg {
 
 // ---- launchers (return hipGetLastError() of the launch) ----
 hipError_t launch_visual_index(hipStream_t s, const int32_t* ids, int32_t T, int32_t* vis_idx);
+// With norm_w, also norm_out = RMSNorm(X) * norm_w (the first layer's attention norm).
 hipError_t launch_embed(hipStream_t s, rp_dtype dt, const int32_t* ids, const int32_t* vis_idx,
                         const void* visual, int64_t n_visual, const void* embed, int32_t vocab,
-                        int32_t T, int32_t d, float* X);
+                        int32_t T, int32_t d, float* X, const void* norm_w = nullptr, float eps = 0.f,
+                        void* norm_out = nullptr);
 hipError_t launch_rmsnorm(hipStream_t s, rp_dtype dt, const float* X, const void* w, float eps, int32_t M,
                           int32_t d, void* out);
 // Final norm of the suffix rows with boundary assembly: row r of sequence b reads
