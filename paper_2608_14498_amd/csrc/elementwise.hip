@@ -9,26 +9,35 @@ namespace rp {
 
 // ------------------------------------------------------------------------------------
 // Visual-slot numbering: vis_idx[t] = number of visual slots (id < 0) before t, or -1.
-// One workgroup; each thread scans a contiguous chunk (T is small next to the GEMMs).
+// One workgroup walks the ids 1024 at a time: each wave numbers its 64 slots with a
+// ballot (a lane's slot index is the count of set bits below it), wave totals are
+// combined through LDS, and a running base carries over to the next 1024 (whose ids are
+// loaded during the current round).
 // ------------------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void k_visual_index(const int32_t* __restrict__ ids, int T,
                                                        int32_t* __restrict__ vis_idx) {
-  __shared__ int32_t sc[1024];
-  const int tid = threadIdx.x, nt = blockDim.x;
-  const int chunk = (T + nt - 1) / nt;
-  const int lo = min(T, tid * chunk), hi = min(T, lo + chunk);
-  int c = 0;
-  for (int i = lo; i < hi; ++i) c += ids[i] < 0;
-  sc[tid] = c;
-  __syncthreads();
-  for (int off = 1; off < nt; off <<= 1) {  // inclusive Hillis-Steele scan
-    int v = tid >= off ? sc[tid - off] : 0;
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, nw = blockDim.x >> 6;
+  int base = 0;
+  int id = tid < T ? ids[tid] : 0;
+  for (int t0 = 0; t0 < T; t0 += blockDim.x) {
+    const int t = t0 + tid, tn = t + blockDim.x;
+    const int id_next = tn < T ? ids[tn] : 0;  // in flight during this round
+    const bool vis = t < T && id < 0;
+    id = id_next;
+    const uint64_t m = __ballot(vis);
+    const int below = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[w] = __popcll(m);
     __syncthreads();
-    sc[tid] += v;
-    __syncthreads();
+    int off = base, tot = 0;
+    for (int i = 0; i < nw; ++i) {
+      off += i < w ? wsum[i] : 0;
+      tot += wsum[i];
+    }
+    if (t < T) vis_idx[t] = vis ? off + below : -1;
+    __syncthreads();  // wsum is rewritten by the next round
+    base += tot;
   }
-  int run = sc[tid] - c;
-  for (int i = lo; i < hi; ++i) vis_idx[i] = ids[i] < 0 ? run++ : -1;
 }
 
 hipError_t launch_visual_index(hipStream_t s, const int32_t* ids, int32_t T, int32_t* vis_idx) {

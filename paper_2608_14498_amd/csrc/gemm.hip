@@ -1048,7 +1048,7 @@ struct SkinnyArgs {
   int64_t plane;  // elements between splits of out
   int k_chunk;
   int add;        // accumulate into out (one split)
-  ArgmaxPart* arg;  // instead of out (one split): each wave's per-row (max, lowest column of it)
+  ArgmaxPart* arg;  // instead of out (one split): each wave's per-row (max, lowest column of it), [M][ceil(N/32)]
 };
 
 template <typename T16, int RF, bool BT, int SW>
@@ -1188,7 +1188,9 @@ __global__ __launch_bounds__(SW * 64) void k_gemm_skinny(SkinnyArgs g) {
         bi = io;
       }
       const int m = rf * 32 + fr;
-      if (fk == 0 && m < g.M && nw0 < g.N) g.arg[(int64_t)(blockIdx.x * SW + wave) * g.M + m] = ArgmaxPart{best, bi};
+      // row-major candidates: row m's are contiguous for the reduction
+      if (fk == 0 && m < g.M && nw0 < g.N)
+        g.arg[(int64_t)m * ((g.N + 31) / 32) + blockIdx.x * SW + wave] = ArgmaxPart{best, bi};
     }
     return;
   }
@@ -1425,16 +1427,18 @@ __global__ __launch_bounds__(256) void k_argmax_parts(const ArgmaxPart* __restri
       bi = p.i;
     }
   };
-  // the candidates of row m are M entries apart: eight loads in flight per thread
+  // row m's candidates are contiguous: eight coalesced loads in flight per thread (the
+  // merge is order-independent: a total order on (value, -index), NaN never wins)
+  const ArgmaxPart* row = part + (int64_t)m * nparts;
   int t = threadIdx.x;
   for (; t + 7 * 256 < nparts; t += 8 * 256) {
     ArgmaxPart p[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) p[u] = part[(int64_t)(t + u * 256) * M + m];
+    for (int u = 0; u < 8; ++u) p[u] = row[t + u * 256];
 #pragma unroll
     for (int u = 0; u < 8; ++u) merge(p[u]);
   }
-  for (; t < nparts; t += 256) merge(part[(int64_t)t * M + m]);
+  for (; t < nparts; t += 256) merge(row[t]);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float vb = __shfl_xor(best, o, kWave);
