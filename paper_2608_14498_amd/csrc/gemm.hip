@@ -629,10 +629,12 @@ __global__ __launch_bounds__(WGM * 2 * 64) void k_gemm_bf16(GemmArgs g) {
 // instructions spent on staging.  One load instruction writes 64 consecutive 16-byte
 // LDS chunks (8 rows of one slab); the swizzle is applied by choosing which global
 // chunk each lane fetches.  The 8-wave form keeps three B slabs and two A slabs in LDS
-// (5 x 32 KiB, all of the CU's 160 KiB): B copies are issued two slabs ahead, A copies
-// one slab ahead, so each slab barrier waits only for the A copies issued one slab
-// earlier (with two stages of both, for all of them: the matrix cores were busy 68-69%
-// of the cycles and the prefix GEMMs took 4-6% longer).  Three A stages instead gain as
+// (5 x 32 KiB, all of the CU's 160 KiB): B copies are issued during the second k-step of
+// the slab two before theirs, A copies right after the barrier one slab ahead, so each
+// slab barrier waits only for the A copies issued one slab earlier (with two stages of
+// both, for all of them: the matrix cores were busy 68-69% of the cycles and the prefix
+// GEMMs took 4-6% longer; with the B copies issued beside the A copies after the
+// barrier, 1-1.5% longer).  Three A stages instead gain as
 // much time, but the early A copies cost the gate/up GEMM 23% more L2 misses (its B
 // panels are shared by twice as many concurrent tiles as its A panels).  The 4-wave
 // form keeps two of each.  The buffers are separate arrays and the k loop is unrolled
@@ -751,8 +753,9 @@ void k_gemm_bf16_dma(GemmArgs g) {
   // copies have at least a whole slab of MFMA time to land and each CU keeps L2 misses in
   // flight without a gap (the misses' fabric bandwidth, not the MFMAs, bounds the large
   // GEMMs).  D_TILE (4 waves, two stages of A and B) issues slab kt_+2 and waits for
-  // every copy; D_TILE3 (8 waves) issues A of slab kt_+2, then B of slab kt_+3, and
-  // leaves those last LOADS copies (B, two slabs ahead) in flight at the barrier.
+  // every copy.  D_TILE3 (8 waves) issues B of slab kt_+2 into PB (the B buffer slab
+  // kt_-1 used, free since the last barrier) under the MFMAs of k-step 1, and A of slab
+  // kt_+2 after the barrier; at the barrier only those B copies may still be in flight.
 #define D_REGION(n_mem_, mem_mask_)                                                        \
   __builtin_amdgcn_sched_group_barrier(0x100, NREAD, 0);                                   \
   _Pragma("unroll") for (int q = 0; q < MM; ++q) {                                         \
@@ -783,7 +786,7 @@ void k_gemm_bf16_dma(GemmArgs g) {
     D_REGION(2 * LOADS, 0x010);                                               \
     __builtin_amdgcn_sched_barrier(0);                                        \
   }
-#define D_TILE3(SA, SB, DA, DB, kt_)                                          \
+#define D_TILE3(SA, SB, DA, DB, PB, kt_)                                      \
   {                                                                           \
     D_FRAGS(af1, bf1, SA, SB, 1);                                             \
     D_MMA(af0, bf0);                                                          \
@@ -791,20 +794,20 @@ void k_gemm_bf16_dma(GemmArgs g) {
     __builtin_amdgcn_sched_barrier(0);                                        \
     D_FRAGS(af0, bf0, SA, SB, 2);                                             \
     D_MMA(af1, bf1);                                                          \
-    D_REGION(0, 0x000);                                                       \
+    D_LOADB(PB, min((kt_) + 2, KT - 1));                                      \
+    D_REGION(LOADS, 0x010);                                                   \
     __builtin_amdgcn_sched_barrier(0);                                        \
     D_FRAGS(af1, bf1, SA, SB, 3);                                             \
     D_MMA(af0, bf0);                                                          \
     D_REGION(0, 0x000);                                                       \
     __builtin_amdgcn_sched_barrier(0);                                        \
-    /* this wave's copies of slab kt_+1 (its B issued two slabs ago, its A */ \
-    /* one slab ago) have landed; the last LOADS copies (B of kt_+2) may not */ \
+    /* this wave's copies of slab kt_+1 (B issued during slab kt_-1, A after */ \
+    /* the last barrier) have landed; the B copies of kt_+2 may not have     */ \
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(LOADS) : "memory"); \
     D_FRAGS(af0, bf0, DA, DB, 0);                                             \
     D_MMA(af1, bf1);                                                          \
     D_LOADA(SA, min((kt_) + 2, KT - 1));                                      \
-    D_LOADB(SB, min((kt_) + 3, KT - 1));                                      \
-    D_REGION(2 * LOADS, 0x010);                                               \
+    D_REGION(LOADS, 0x010);                                                   \
     __builtin_amdgcn_sched_barrier(0);                                        \
   }
 
@@ -834,7 +837,8 @@ void k_gemm_bf16_dma(GemmArgs g) {
       if (kt < KT) D_TILE(As0, Bs0, As1, Bs1, kt);
     }
   } else if (KT > 0) {
-    // slab s lives in As[s % 2] and Bs[s % 3]; past the last slab the copies re-load it
+    // slab s lives in As[s % 2] and Bs[s % 3]; B of slab 2 goes out during slab 0, A of
+    // slab 1 after the first fragment reads; past the last slab the copies re-load it
     // into a buffer no later slab reads
     D_LOADB(Bs0, 0);
     D_LOADA(As0, 0);
@@ -842,21 +846,20 @@ void k_gemm_bf16_dma(GemmArgs g) {
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     D_FRAGS(af0, bf0, As0, Bs0, 0);
     D_LOADA(As1, min(1, KT - 1));
-    D_LOADB(Bs2, min(2, KT - 1));
     int kt = 0;
     for (; kt + 6 <= KT; kt += 6) {
-      D_TILE3(As0, Bs0, As1, Bs1, kt);
-      D_TILE3(As1, Bs1, As0, Bs2, kt + 1);
-      D_TILE3(As0, Bs2, As1, Bs0, kt + 2);
-      D_TILE3(As1, Bs0, As0, Bs1, kt + 3);
-      D_TILE3(As0, Bs1, As1, Bs2, kt + 4);
-      D_TILE3(As1, Bs2, As0, Bs0, kt + 5);
+      D_TILE3(As0, Bs0, As1, Bs1, Bs2, kt);
+      D_TILE3(As1, Bs1, As0, Bs2, Bs0, kt + 1);
+      D_TILE3(As0, Bs2, As1, Bs0, Bs1, kt + 2);
+      D_TILE3(As1, Bs0, As0, Bs1, Bs2, kt + 3);
+      D_TILE3(As0, Bs1, As1, Bs2, Bs0, kt + 4);
+      D_TILE3(As1, Bs2, As0, Bs0, Bs1, kt + 5);
     }
-    if (kt < KT) D_TILE3(As0, Bs0, As1, Bs1, kt);
-    if (kt + 1 < KT) D_TILE3(As1, Bs1, As0, Bs2, kt + 1);
-    if (kt + 2 < KT) D_TILE3(As0, Bs2, As1, Bs0, kt + 2);
-    if (kt + 3 < KT) D_TILE3(As1, Bs0, As0, Bs1, kt + 3);
-    if (kt + 4 < KT) D_TILE3(As0, Bs1, As1, Bs2, kt + 4);
+    if (kt < KT) D_TILE3(As0, Bs0, As1, Bs1, Bs2, kt);
+    if (kt + 1 < KT) D_TILE3(As1, Bs1, As0, Bs2, Bs0, kt + 1);
+    if (kt + 2 < KT) D_TILE3(As0, Bs2, As1, Bs0, Bs1, kt + 2);
+    if (kt + 3 < KT) D_TILE3(As1, Bs0, As0, Bs1, Bs2, kt + 3);
+    if (kt + 4 < KT) D_TILE3(As0, Bs1, As1, Bs2, Bs0, kt + 4);
   }
 #undef D_LOAD
 #undef D_LOADA
