@@ -756,10 +756,13 @@ void k_gemm_bf16_dma(GemmArgs g) {
   // every copy.  D_TILE3 (8 waves) issues B of slab kt_+2 into PB (the B buffer slab
   // kt_-1 used, free since the last barrier) under the MFMAs of k-step 1, and A of slab
   // kt_+2 after the barrier; at the barrier only those B copies may still be in flight.
+  // Within a k-step each MFMA is followed by one fragment read of the next k-step and
+  // then by one copy, so neither the reads nor the copies bunch up in front of the MFMAs
+  // (reads grouped ahead of the k-step's MFMAs: the prefix GEMMs took 2% longer).
 #define D_REGION(n_mem_, mem_mask_)                                                        \
-  __builtin_amdgcn_sched_group_barrier(0x100, NREAD, 0);                                   \
   _Pragma("unroll") for (int q = 0; q < MM; ++q) {                                         \
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                     \
+    if (q < NREAD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                      \
     if (q < (n_mem_)) __builtin_amdgcn_sched_group_barrier((mem_mask_), 1, 0);             \
   }
 #define D_TILE(SA, SB, DA, DB, kt_)                                           \
